@@ -1,0 +1,149 @@
+"""Seeded synthetic inputs for the TP-aware dequantization workloads.
+
+This module only draws random numbers and lays them out in the storage format
+the library consumes. It holds none of the method's arithmetic (no dequant, no
+sort, no permutation of weights), so that the CPU oracle and the HIP path can
+both take their inputs from it without sharing any computation.
+
+Workloads (MLP problem sizes of the paper's experiments section):
+  * Llama-70B MLP: hidden 8192, intermediate 28672 (single up_proj then
+    down_proj, no gate).
+  * Granite-20B MLP: hidden 6144, intermediate 24576.
+Act-order is emulated as in Eq. 2-3: a seeded random permutation phi of the
+K input channels and g_idx[i] = floor(phi(i) / G).
+
+Storage format (the library's, fixed here):
+  qweight int32 [K/8][N]   nibble j (bits 4j..4j+3) of word [r][n] = row 8r+j
+  scales  fp16  [K/G][N]
+  qzeros  int32 [K/G][N/8] nibble j of word [g][c] = column 8c+j
+Uniform int4 codes packed eight to a word are exactly uniform 32-bit words, so
+qweight and qzeros are drawn as random words.
+"""
+from __future__ import annotations
+
+import dataclasses
+
+import numpy as np
+
+BASE_SEED = 20240207
+
+# tensor ids for the per-tensor streams
+T_PHI1, T_PHI2, T_QW1, T_QW2, T_S1, T_S2, T_Z1, T_Z2, T_X = range(9)
+
+
+@dataclasses.dataclass(frozen=True)
+class Workload:
+    """One MLP (or single GEMM) problem: global sizes plus the TP degree.
+
+    K1 = hidden (input features of the column-parallel W1), N1 = intermediate
+    (W1 output features = W2 input features K2), N2 = W2 output features.
+    A workload with N2 == 0 is a single GEMM (only W1).
+    """
+    name: str
+    cfg_id: int
+    K1: int
+    N1: int
+    N2: int
+    G: int
+    tp: int
+    Ms: tuple
+
+    @property
+    def K2(self) -> int:
+        return self.N1
+
+
+WORKLOADS = {
+    "tiny_gemm": Workload("tiny_gemm", 0, 256, 128, 0, 32, 1, (4,)),
+    "llama70b_tp8": Workload("llama70b_tp8", 1, 8192, 28672, 8192, 128, 8, (1, 4, 16)),
+    "granite20b_tp4": Workload("granite20b_tp4", 2, 6144, 24576, 6144, 128, 4, (1, 8, 16)),
+    "llama70b_tp1": Workload("llama70b_tp1", 3, 8192, 28672, 8192, 128, 1, (1, 16, 64)),
+    "llama70b_tp2_prefill": Workload("llama70b_tp2_prefill", 4, 8192, 28672, 8192, 128, 2, (2048,)),
+}
+
+
+def rng_for(cfg_id: int, tensor_id: int, seed: int = BASE_SEED) -> np.random.Generator:
+    return np.random.Generator(np.random.PCG64([seed, cfg_id, tensor_id]))
+
+
+def random_permutation(n: int, rng: np.random.Generator) -> np.ndarray:
+    """phi of Eq. 2: a uniformly random permutation of 0..n-1 (int32)."""
+    return rng.permutation(n).astype(np.int32)
+
+
+def actorder_gidx(phi: np.ndarray, G: int) -> np.ndarray:
+    """Input synthesis by Eq. 3: g_idx[i] = floor(phi(i) / G)."""
+    return (phi // G).astype(np.int32)
+
+
+def random_words(shape, rng: np.random.Generator) -> np.ndarray:
+    """Uniform 32-bit words = eight uniform int4 codes each."""
+    return rng.integers(0, 1 << 32, size=shape, dtype=np.uint64).astype(np.uint32).view(np.int32)
+
+
+def random_scales(shape, rng: np.random.Generator, lo=0.002, hi=0.02, dtype=np.float16) -> np.ndarray:
+    return rng.uniform(lo, hi, size=shape).astype(dtype)
+
+
+def random_activations(M: int, K: int, rng: np.random.Generator, dtype=np.float16) -> np.ndarray:
+    return rng.standard_normal((M, K)).astype(dtype)
+
+
+@dataclasses.dataclass
+class QuantLinear:
+    """One GPTQ-style act-order layer in the library's storage format."""
+    qweight: np.ndarray   # int32 [K/8][N]
+    scales: np.ndarray    # fp16 [K/G][N]
+    qzeros: np.ndarray    # int32 [K/G][N/8]
+    g_idx: np.ndarray     # int32 [K]
+    phi: np.ndarray       # int32 [K], the emulated act-order permutation
+    G: int
+
+    @property
+    def K(self) -> int:
+        return self.qweight.shape[0] * 8
+
+    @property
+    def N(self) -> int:
+        return self.qweight.shape[1]
+
+
+def make_layer(K: int, N: int, G: int, cfg_id: int, t_phi: int, t_qw: int, t_s: int, t_z: int,
+               seed: int = BASE_SEED, scale_dtype=np.float16) -> QuantLinear:
+    if K % 8 or N % 8 or K % G or G % 8:
+        raise ValueError(f"unsupported layer shape K={K} N={N} G={G}")
+    phi = random_permutation(K, rng_for(cfg_id, t_phi, seed))
+    return QuantLinear(
+        qweight=random_words((K // 8, N), rng_for(cfg_id, t_qw, seed)),
+        scales=random_scales((K // G, N), rng_for(cfg_id, t_s, seed), dtype=scale_dtype),
+        qzeros=random_words((K // G, N // 8), rng_for(cfg_id, t_z, seed)),
+        g_idx=actorder_gidx(phi, G),
+        phi=phi,
+        G=G,
+    )
+
+
+def make_workload(w: Workload, seed: int = BASE_SEED):
+    """Global (unsharded) layers of a workload: (W1, W2-or-None)."""
+    w1 = make_layer(w.K1, w.N1, w.G, w.cfg_id, T_PHI1, T_QW1, T_S1, T_Z1, seed)
+    w2 = None
+    if w.N2:
+        w2 = make_layer(w.K2, w.N2, w.G, w.cfg_id, T_PHI2, T_QW2, T_S2, T_Z2, seed)
+    return w1, w2
+
+
+def make_x(w: Workload, M: int, seed: int = BASE_SEED, dtype=np.float16) -> np.ndarray:
+    rng = np.random.Generator(np.random.PCG64([seed, w.cfg_id, T_X, M]))
+    return random_activations(M, w.K1, rng, dtype)
+
+
+def make_custom(K1: int, N1: int, N2: int, G: int, seed: int, cfg_id: int = 100, identity_phi=False):
+    """Small ad-hoc layers for tests (ragged shapes, special cases)."""
+    w1 = make_layer(K1, N1, G, cfg_id, T_PHI1, T_QW1, T_S1, T_Z1, seed)
+    w2 = make_layer(N1, N2, G, cfg_id, T_PHI2, T_QW2, T_S2, T_Z2, seed) if N2 else None
+    if identity_phi:
+        for w in (w1, w2):
+            if w is not None:
+                w.phi = np.arange(w.K, dtype=np.int32)
+                w.g_idx = actorder_gidx(w.phi, G)
+    return w1, w2

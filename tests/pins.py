@@ -1,0 +1,365 @@
+"""Pins of the CPU oracle: checks against what the paper and the mathematics fix.
+
+Each pin is a plain function taking the oracle module, so that the mutation
+tests can run the same pin against an oracle with a planted mistake and see it
+fail. None of these re-types the oracle's own formula: they use hand-worked
+values, closed forms, invariants, and brute force by other means.
+"""
+from __future__ import annotations
+
+import os
+
+import numpy as np
+
+from paper_2402_04925_amd import inputs
+
+GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden")
+
+
+def load_golden(name):
+    out = {}
+    with open(os.path.join(GOLDEN, name)) as f:
+        for line in f:
+            line = line.strip()
+            if not line or line.startswith("#"):
+                continue
+            k, v = line.split(":", 1)
+            out[k.strip()] = v.split()
+    return out
+
+
+def hex_words(vals):
+    return np.array([int(v, 16) for v in vals], dtype=np.uint32).view(np.int32)
+
+
+def nibble_by_hex(word: int, j: int) -> int:
+    """Nibble j of a 32-bit word read off its hexadecimal spelling (digit 7-j),
+    a route independent of shifts and masks."""
+    return int(format(word & 0xFFFFFFFF, "08x")[7 - j], 16)
+
+
+# ---------------------------------------------------------------- storage ---
+
+def pin_unpack_bruteforce(o, seed=1):
+    """P1: every code of a random tiny weight and zero array, read one element
+    at a time off the hex spelling of its word."""
+    w1, _ = inputs.make_custom(64, 24, 0, 16, seed)
+    q = o.unpack_rows(w1.qweight)
+    z = o.unpack_cols(w1.qzeros)
+    words = w1.qweight.view(np.uint32)
+    for k in range(64):
+        for n in range(24):
+            assert q[k, n] == nibble_by_hex(int(words[k // 8, n]), k % 8), (k, n)
+    zw = w1.qzeros.view(np.uint32)
+    for g in range(4):
+        for n in range(24):
+            assert z[g, n] == nibble_by_hex(int(zw[g, n // 8]), n % 8), (g, n)
+
+
+def pin_pack_roundtrip(o, seed=2):
+    """P2: pack(unpack(words)) == words and unpack(pack(codes)) == codes."""
+    w1, _ = inputs.make_custom(128, 40, 0, 32, seed)
+    assert np.array_equal(o.pack_rows(o.unpack_rows(w1.qweight)), w1.qweight)
+    assert np.array_equal(o.pack_cols(o.unpack_cols(w1.qzeros)), w1.qzeros)
+    rng = np.random.default_rng(seed)
+    codes = rng.integers(0, 16, size=(48, 16))
+    assert np.array_equal(o.unpack_rows(o.pack_rows(codes)), codes)
+    assert np.array_equal(o.unpack_cols(o.pack_cols(codes)), codes)
+
+
+def pin_golden_gemm_codes(o):
+    """Hand-worked codes: word 0x76543210 holds code k in row k."""
+    gd = load_golden("gemm_worked_example.txt")
+    qw = hex_words(gd["qweight_hex"]).reshape(1, 8)
+    q = o.unpack_rows(qw)
+    for n in range(8):
+        expect = np.arange(8) + (8 if n % 2 else 0)
+        assert np.array_equal(q[:, n], expect)
+    z = o.unpack_cols(hex_words(gd["qzeros_hex"]).reshape(2, 1))
+    assert np.array_equal(z[0], np.ones(8)) and np.array_equal(z[1], 2 * np.ones(8))
+
+
+# ---------------------------------------------------------------- reorder ---
+
+def pin_worked_reorder(o):
+    """P10: the hand-worked Eq. 3 / Alg. 1 example."""
+    gd = load_golden("reorder_worked_example.txt")
+    G = int(gd["G"][0])
+    phi = np.array(gd["phi"], dtype=np.int64)
+    g = o.g_idx_actorder(phi, G)
+    assert np.array_equal(g, np.array(gd["g_idx"], dtype=np.int64))
+    P, gs = o.reorder(g)
+    assert np.array_equal(P, np.array(gd["P"], dtype=np.int64))
+    assert np.array_equal(gs, np.array(gd["g_sorted"], dtype=np.int64))
+
+
+def pin_reorder_closed_form(o, K=512, G=32, seed=3):
+    """P3: for a permutation phi and G | K the sorted g_idx is exactly Eq. 1,
+    P is a bijection, and g_idx[P[j]] == g_sorted[j]; within a group the
+    original rows keep ascending order (the stable reading)."""
+    phi = np.random.default_rng(seed).permutation(K)
+    g = o.g_idx_actorder(phi, G)
+    P, gs = o.reorder(g)
+    assert np.array_equal(gs, np.arange(K) // G)          # Eq. 1
+    assert np.array_equal(np.sort(P), np.arange(K))      # bijection
+    assert np.array_equal(g[P], gs)
+    assert np.all(np.diff(gs) >= 0)                      # monotone
+    for grp in range(K // G):
+        rows = P[grp * G:(grp + 1) * G]
+        assert np.all(np.diff(rows) > 0)                 # ascending inside a group
+        assert set(rows.tolist()) == set(np.flatnonzero(g == grp).tolist())
+
+
+def pin_identity_phi(o, K=256, G=32):
+    """P4: phi = identity -> Eq. 3 = Eq. 1 -> P = identity."""
+    g = o.g_idx_actorder(np.arange(K), G)
+    assert np.array_equal(g, o.g_idx_naive(K, G))
+    assert np.array_equal(g, np.arange(K) // G)
+    P, gs = o.reorder(g)
+    assert np.array_equal(P, np.arange(K))
+
+
+def pin_check_groups(o):
+    """Group validation accepts Eq. 3 output and rejects malformed g_idx."""
+    g = o.g_idx_actorder(np.random.default_rng(4).permutation(64), 8)
+    o.check_groups(g, 8)
+    for bad in (np.where(g == 0, 1, g),                   # group 0 empty
+                np.concatenate([g[:-1], [8]]),             # out of range
+                np.concatenate([[-1], g[1:]])):            # negative
+        try:
+            o.check_groups(bad, 8)
+        except o.GroupIndexError:
+            continue
+        raise AssertionError("malformed g_idx accepted")
+
+
+# ------------------------------------------------------------ dequant+GEMM ---
+
+def pin_golden_gemm(o):
+    """Hand-worked dequant + GEMM (act-order) and the same through Alg. 1."""
+    gd = load_golden("gemm_worked_example.txt")
+    qw = hex_words(gd["qweight_hex"]).reshape(1, 8)
+    qz = hex_words(gd["qzeros_hex"]).reshape(2, 1)
+    s = np.array([[float(gd["scales_group0"][0])] * 8, [float(gd["scales_group1"][0])] * 8],
+                 dtype=np.float16)
+    g = np.array(gd["g_idx"], dtype=np.int64)
+    X = np.array([gd["X0"], gd["X1"]], dtype=np.float64).astype(np.float16)
+    Y = o.w4a16_gemm(X, qw, s, qz, g)
+    expect = np.array([gd["Y0"], gd["Y1"]], dtype=np.float64)
+    assert np.array_equal(Y.astype(np.float64), expect), Y
+    P, gs = o.reorder(g)
+    assert np.array_equal(P, np.array(gd["P"], dtype=np.int64))
+    assert np.array_equal(gs, np.array(gd["g_sorted"], dtype=np.int64))
+    ws = o.permute_rows(dict(qweight=qw, scales=s, qzeros=qz), P)
+    assert np.array_equal(ws["qweight"], hex_words(gd["qweight_sorted_hex"]).reshape(1, 8))
+    Y2 = o.w4a16_gemm(X, ws["qweight"], s, qz, gs, x_perm=P)
+    assert np.array_equal(Y2.astype(np.float64), expect)
+
+
+def pin_gemm_bruteforce(o, seed=5):
+    """P6: the oracle's GEMM against a pure-Python triple loop on tiny inputs,
+    codes read off hex spellings, products summed as Python floats."""
+    K, N, G, M = 32, 16, 8, 3
+    w1, _ = inputs.make_custom(K, N, 0, G, seed)
+    X = inputs.random_activations(M, K, np.random.default_rng(seed))
+    qw = w1.qweight.view(np.uint32)
+    zw = w1.qzeros.view(np.uint32)
+    ref = np.zeros((M, N))
+    for m in range(M):
+        for n in range(N):
+            acc = 0.0
+            for k in range(K):
+                g = int(w1.g_idx[k])
+                q = nibble_by_hex(int(qw[k // 8, n]), k % 8)
+                z = nibble_by_hex(int(zw[g, n // 8]), n % 8)
+                acc += float(X[m, k]) * float(w1.scales[g, n]) * (q - z)
+            ref[m, n] = acc
+    Y = o.w4a16_gemm(X, w1.qweight, w1.scales, w1.qzeros, w1.g_idx, round_fp16=False)
+    assert np.max(np.abs(Y - ref)) <= 1e-12 * max(1.0, np.max(np.abs(ref)))
+    Y16 = o.w4a16_gemm(X, w1.qweight, w1.scales, w1.qzeros, w1.g_idx)
+    assert np.array_equal(Y16, ref.astype(np.float16))
+
+
+def pin_one_hot_rows(o, seed=6):
+    """Closed form: X = identity rows picks out rows of the dequantized weight,
+    and the dequantized row k of column n is s*(q-z) of its own group."""
+    K, N, G = 64, 16, 16
+    w1, _ = inputs.make_custom(K, N, 0, G, seed)
+    X = np.eye(K, dtype=np.float16)
+    Y = o.w4a16_gemm(X, w1.qweight, w1.scales, w1.qzeros, w1.g_idx, round_fp16=False)
+    qw = w1.qweight.view(np.uint32)
+    zw = w1.qzeros.view(np.uint32)
+    for k in range(0, K, 7):
+        g = int(w1.g_idx[k])
+        for n in range(N):
+            q = nibble_by_hex(int(qw[k // 8, n]), k % 8)
+            z = nibble_by_hex(int(zw[g, n // 8]), n % 8)
+            assert Y[k, n] == float(w1.scales[g, n]) * (q - z)
+
+
+def pin_special_cases(o, seed=7):
+    """P5: one group (G = K) and q == z everywhere -> Y == 0; G = K with every
+    code = zero + 1 -> Y[m][n] = s[n] * sum_k X[m][k]."""
+    K, N = 64, 16
+    rng = np.random.default_rng(seed)
+    zc = rng.integers(0, 15, size=(1, N))
+    qz = o.pack_cols(zc)
+    X = inputs.random_activations(3, K, rng)
+    s = inputs.random_scales((1, N), rng)
+    g = np.zeros(K, dtype=np.int64)
+    q_eq = np.repeat(zc, K, axis=0)
+    Y = o.w4a16_gemm(X, o.pack_rows(q_eq), s, qz, g, round_fp16=False)
+    assert np.all(Y == 0.0)
+    Y1 = o.w4a16_gemm(X, o.pack_rows(q_eq + 1), s, qz, g, round_fp16=False)
+    expect = np.outer(X.astype(np.float64).sum(axis=1), s[0].astype(np.float64))
+    assert np.max(np.abs(Y1 - expect)) <= 1e-12 * np.max(np.abs(expect))
+
+
+def pin_ordered_equals_actorder(o, seed=8):
+    """P7: X[:, P] @ deq(W[P], g[P]) == X @ deq(W, g) (the reorder only
+    relabels the terms of each dot product)."""
+    K, N, G, M = 256, 48, 32, 4
+    w1, _ = inputs.make_custom(K, N, 0, G, seed)
+    X = inputs.random_activations(M, K, np.random.default_rng(seed))
+    ref = o.w4a16_gemm(X, w1.qweight, w1.scales, w1.qzeros, w1.g_idx, round_fp16=False)
+    P, gs = o.reorder(w1.g_idx)
+    ws = o.permute_rows(dict(qweight=w1.qweight, scales=w1.scales, qzeros=w1.qzeros), P)
+    Y = o.w4a16_gemm(X, ws["qweight"], ws["scales"], ws["qzeros"], gs, x_perm=P, round_fp16=False)
+    assert np.max(np.abs(Y - ref)) <= 1e-12 * np.max(np.abs(ref))
+    # the ordered weight's group of row j is Eq. 1, so the g_idx need not be read
+    Y_eq1 = o.w4a16_gemm(X, ws["qweight"], ws["scales"], ws["qzeros"], o.g_idx_naive(K, G),
+                         x_perm=P, round_fp16=False)
+    assert np.array_equal(Y_eq1, Y)
+    Y32 = o.w4a16_gemm(X, ws["qweight"], ws["scales"], ws["qzeros"], gs, x_perm=P, acc="f32",
+                       round_fp16=False)
+    assert np.max(np.abs(Y32 - ref)) <= 1e-5 * np.max(np.abs(ref))
+
+
+# -------------------------------------------------------------------- MLP ---
+
+def _mlp_case(K1, N1, N2, G, seed):
+    w1, w2 = inputs.make_custom(K1, N1, N2, G, seed)
+    X = inputs.random_activations(3, K1, np.random.default_rng(seed))
+    d1 = dict(qweight=w1.qweight, scales=w1.scales, qzeros=w1.qzeros)
+    d2 = dict(qweight=w2.qweight, scales=w2.scales, qzeros=w2.qzeros)
+    return w1, w2, d1, d2, X
+
+
+def pin_tp_aware_mlp(o, seed=9, tps=(1, 2, 4, 8)):
+    """P8: the sum over ranks of Alg. 3's partials equals the unsharded
+    act-order MLP, for every TP degree (the paper's section 2.2 claim)."""
+    K1, N1, N2, G = 256, 512, 128, 32
+    w1, w2, d1, d2, X = _mlp_case(K1, N1, N2, G, seed)
+    ref64 = o.w4a16_gemm(o.w4a16_gemm(X, *_l(d1, w1.g_idx), round_fp16=False),
+                         *_l(d2, w2.g_idx), round_fp16=False)
+    P1, _ = o.reorder(w1.g_idx)
+    P2, _ = o.reorder(w2.g_idx)
+    w1f, w2f = o.fold(d1, d2, P1, P2)
+    for tp in tps:
+        parts = []
+        for r in range(tp):
+            _, y2 = o.mlp_tp_aware_rank(X, P1, o.column_shard(w1f, r, tp),
+                                        o.row_shard(w2f, r, tp, G), G, y1_fp16=False,
+                                        round_y2=False)
+            parts.append(y2)
+        tot = o.all_reduce_sum(parts, round_fp16=False)
+        assert np.max(np.abs(tot - ref64)) <= 1e-12 * np.max(np.abs(ref64)), tp
+        # with the paper's fp16 activations
+        y2_16, _ = o.mlp_tp_aware(X, P1, w1f, w2f, G, tp)
+        ref16 = o.mlp_reference(X, d1, w1.g_idx, d2, w2.g_idx)
+        assert o.rel_err(y2_16, ref16) <= 2e-3, tp
+
+
+def _l(d, g):
+    return d["qweight"], d["scales"], d["qzeros"], g
+
+
+def pin_actorder_shard_mlp(o, seed=10, tps=(2, 4)):
+    """The act-order (no reorder) rank: a row shard keeps its rows' global
+    g_idx values and the full metadata; the ranks' partials sum to the
+    unsharded MLP."""
+    K1, N1, N2, G = 128, 256, 64, 32
+    w1, w2, d1, d2, X = _mlp_case(K1, N1, N2, G, seed)
+    ref = o.w4a16_gemm(o.w4a16_gemm(X, *_l(d1, w1.g_idx), round_fp16=False),
+                       *_l(d2, w2.g_idx), round_fp16=False)
+    for tp in tps:
+        n = N1 // tp
+        parts = []
+        for r in range(tp):
+            _, y2 = o.mlp_actorder_rank(X, o.column_shard(d1, r, tp), w1.g_idx,
+                                        o.row_shard(d2, r, tp, G, keep_all_groups=True),
+                                        w2.g_idx[r * n:(r + 1) * n], y1_fp16=False, round_y2=False)
+            parts.append(y2)
+        tot = o.all_reduce_sum(parts, round_fp16=False)
+        assert np.max(np.abs(tot - ref)) <= 1e-12 * np.max(np.abs(ref)), tp
+
+
+def pin_alg2_equals_alg3(o, seed=11):
+    """P9: Alg. 2 (AllGather, Y1[:, P2], CHUNK) and Alg. 3 (P2 folded into
+    W1's columns) compute the same per-column dot products; in the oracle the
+    fp16 results agree bit for bit at every TP degree."""
+    K1, N1, N2, G = 128, 256, 64, 32
+    w1, w2, d1, d2, X = _mlp_case(K1, N1, N2, G, seed)
+    P1, _ = o.reorder(w1.g_idx)
+    P2, _ = o.reorder(w2.g_idx)
+    w1o = o.permute_rows(d1, P1)
+    w2o = o.permute_rows(d2, P2)
+    w1f, w2f = o.fold(d1, d2, P1, P2)
+    assert np.array_equal(w2f["qweight"], w2o["qweight"])
+    for tp in (1, 2, 4):
+        y_naive, parts_naive = o.mlp_naive_algorithm(X, P1, P2, w1o, w2o, G, tp)
+        y_aware, parts_aware = o.mlp_tp_aware(X, P1, w1f, w2f, G, tp)
+        for a, b in zip(parts_naive, parts_aware):
+            assert np.array_equal(a, b), tp
+        assert np.array_equal(y_naive, y_aware)
+
+
+def pin_fold_elementwise(o, seed=12):
+    """W1[P1, P2] element by element against the codes of W1, and the
+    metadata columns against P2 (brute force over a tiny layer)."""
+    K1, N1, N2, G = 32, 16, 8, 8
+    w1, w2, d1, d2, X = _mlp_case(K1, N1, N2, G, seed)
+    P1 = np.random.default_rng(seed).permutation(K1)
+    P2 = np.random.default_rng(seed + 1).permutation(N1)
+    w1f, w2f = o.fold(d1, d2, P1, P2)
+    qa = w1.qweight.view(np.uint32)
+    qb = w1f["qweight"].view(np.uint32)
+    for j in range(K1):
+        for c in range(N1):
+            assert nibble_by_hex(int(qb[j // 8, c]), j % 8) == \
+                nibble_by_hex(int(qa[P1[j] // 8, P2[c]]), P1[j] % 8)
+    za = w1.qzeros.view(np.uint32)
+    zb = w1f["qzeros"].view(np.uint32)
+    for g in range(K1 // G):
+        for c in range(N1):
+            assert w1f["scales"][g, c] == w1.scales[g, P2[c]]
+            assert nibble_by_hex(int(zb[g, c // 8]), c % 8) == nibble_by_hex(int(za[g, P2[c] // 8]), P2[c] % 8)
+    q2a = w2.qweight.view(np.uint32)
+    q2b = w2f["qweight"].view(np.uint32)
+    for j in range(N1):
+        for n in range(N2):
+            assert nibble_by_hex(int(q2b[j // 8, n]), j % 8) == nibble_by_hex(int(q2a[P2[j] // 8, n]), P2[j] % 8)
+    assert np.array_equal(w2f["scales"], w2.scales) and np.array_equal(w2f["qzeros"], w2.qzeros)
+
+
+def pin_distinct_groups(o, seed=13):
+    """P11: per 128-row tile, act-order rows touch about
+    ng*(1 - C(K-G,T)/C(K,T)) distinct metadata rows; sorted rows touch one."""
+    K, G, T = 8192, 128, 128
+    rng = np.random.default_rng(seed)
+    g = o.g_idx_actorder(rng.permutation(K), G)
+    d = o.distinct_groups_per_tile(g, T)
+    e = o.expected_distinct_groups(K, G, T)
+    assert abs(d.mean() - e) < 1.0, (d.mean(), e)
+    assert 55.0 < e < 56.5
+    _, gs = o.reorder(g)
+    assert np.all(o.distinct_groups_per_tile(gs, T) == 1)
+
+
+ALL_PINS = [
+    pin_unpack_bruteforce, pin_pack_roundtrip, pin_golden_gemm_codes, pin_worked_reorder,
+    pin_reorder_closed_form, pin_identity_phi, pin_check_groups, pin_golden_gemm,
+    pin_gemm_bruteforce, pin_one_hot_rows, pin_special_cases, pin_ordered_equals_actorder,
+    pin_tp_aware_mlp, pin_actorder_shard_mlp, pin_alg2_equals_alg3, pin_fold_elementwise,
+    pin_distinct_groups,
+]
