@@ -1,0 +1,338 @@
+#!/usr/bin/env python3
+"""Benchmark: one GPU's TP-aware MLP shard (Alg. 3 without its AllReduce).
+
+Default workload: the Llama-70B MLP problem size (hidden 8192, intermediate
+28672, up_proj then down_proj) at TP = 8, rank 0: W1 shard 8192 x 3584,
+W2 shard 3584 x 8192, int4 weights with G = 128, fp16 activations, decode
+batch M = 16 (M = 1 and 4 are reported alongside).
+
+A step is one pass of the hot path: gather X[:, P1] -> ordered W4A16 GEMM1 ->
+ordered W4A16 GEMM2 (tpdq_mlp_shard). Weights are resident in HBM and rotate
+over replicas whose total exceeds twice the 256 MB Infinity Cache, so every
+step streams its weights from HBM. The timed steps are replayed from one HIP
+graph (the library launches on torch's current stream, which torch captures),
+timed with events on that stream.
+
+Prints ONE JSON line on stdout.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "W4A16 MLP-shard latency (us) + achieved HBM GB/s vs peak, Llama-70B shapes"
+HBM_PEAK_GBS = 8000.0
+MFMA_F16_PEAK_TFLOPS = 2500.0
+MALL_BYTES = 256 << 20
+ROTATE_MIN_BYTES = 640 << 20
+
+
+def eprint(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def shard_bytes(K, N, G, ng=None):
+    """Algorithmic bytes of one W4 layer shard: packed weights, fp16 scales,
+    packed zeros (ng metadata rows)."""
+    ng = K // G if ng is None else ng
+    return K * N // 2 + ng * N * 2 + ng * N // 2
+
+
+def gemm_bytes(M, K, N, G, ng=None, gidx=False, xperm=False):
+    b = shard_bytes(K, N, G, ng) + M * K * 2 + M * N * 2
+    if gidx:
+        b += K * 4
+    if xperm:
+        b += K * 4
+    return b
+
+
+def kernel_source_hash():
+    h = hashlib.sha256()
+    for f in ("gemm_decode.hip", "tpdq_internal.h"):
+        with open(os.path.join(ROOT, "paper_2402_04925_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def read_traffic(workload, M):
+    """HBM traffic (FETCH_SIZE + WRITE_SIZE per launch of the ordered decode
+    kernel) from a committed counter summary, if one exists for the current
+    kernel source; None otherwise."""
+    path = os.path.join(ROOT, "profiles", f"traffic_decode_ordered_{workload}_M{M}.txt")
+    if not os.path.exists(path):
+        return None
+    vals = {}
+    with open(path) as f:
+        for line in f:
+            if "=" in line and not line.startswith("#"):
+                k, v = line.split("=", 1)
+                vals[k.strip()] = v.strip()
+    if vals.get("kernel_source_hash") != kernel_source_hash():
+        return None
+    try:
+        return float(vals["bytes_per_launch"])
+    except (KeyError, ValueError):
+        return None
+
+
+class Setup:
+    """Device-resident shards (rank 0) of one workload, replicated for rotation."""
+
+    def __init__(self, wl, dev, min_bytes=ROTATE_MIN_BYTES):
+        import torch
+        import paper_2402_04925_amd as tpdq
+        from paper_2402_04925_amd import inputs
+
+        self.wl = wl
+        t0 = time.time()
+        L1, L2 = inputs.make_workload(wl)
+        self.L1, self.L2 = L1, L2
+        eprint(f"[bench] generated {wl.name} layers in {time.time() - t0:.1f}s")
+
+        def dev_layer(L):
+            return tpdq.QuantWeight.from_tensors(
+                torch.from_numpy(L.qweight).to(dev), torch.from_numpy(L.scales).to(dev),
+                torch.from_numpy(L.qzeros).to(dev), torch.from_numpy(L.g_idx.astype(np.int32)).to(dev),
+                L.G)
+
+        d1, d2 = dev_layer(L1), dev_layer(L2)
+        P1, _, P2, _, w1o, w2o = tpdq.reorder(d1, d2)
+        torch.cuda.synchronize()
+        tp = wl.tp
+        self.P1 = P1
+        # rank-0 shards, materialised densely (what a deployment would ship)
+        ord1 = w1o.column_shard(0, tp)
+        ord2 = w2o.row_shard(0, tp, sorted_rows=True)
+        act1 = d1.column_shard(0, tp)
+        act2 = d2.row_shard(0, tp, sorted_rows=False)
+
+        def dense(q, with_g):
+            return tpdq.QuantWeight(q.qweight.contiguous(), q.scales.contiguous(), q.qzeros.contiguous(),
+                                    q.g_idx.contiguous() if with_g and q.g_idx is not None else None,
+                                    q.K, q.N, q.G, q.num_groups)
+
+        base = [dense(ord1, False), dense(ord2, False), dense(act1, True), dense(act2, True)]
+        per = sum(t.qweight.numel() * 4 + t.scales.numel() * 2 + t.qzeros.numel() * 4 for t in base[:2])
+        self.R = max(2, -(-min_bytes // per))
+        self.reps = [base]
+        for _ in range(self.R - 1):
+            self.reps.append([tpdq.QuantWeight(q.qweight.clone(), q.scales.clone(), q.qzeros.clone(),
+                                               q.g_idx.clone() if q.g_idx is not None else None,
+                                               q.K, q.N, q.G, q.num_groups) for q in base])
+        torch.cuda.synchronize()
+        del d1, d2, w1o, w2o
+        eprint(f"[bench] {self.R} weight replicas of {per / 1e6:.1f} MB (ordered pair)")
+
+
+def capture_and_time(fn_list, steps, warmup, dev):
+    """Replay the calls fn_list[i % len] for `steps` iterations from a HIP
+    graph; return ms per iteration (events on the capture stream)."""
+    import torch
+    s = torch.cuda.Stream(device=dev)
+    s.wait_stream(torch.cuda.current_stream(dev))
+    with torch.cuda.stream(s):
+        for i in range(min(3, len(fn_list))):   # eager warm-up on the capture stream
+            fn_list[i % len(fn_list)]()
+    torch.cuda.current_stream(dev).wait_stream(s)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g, stream=s):
+        for i in range(steps):
+            fn_list[i % len(fn_list)]()
+    torch.cuda.synchronize()
+    for _ in range(max(1, warmup // max(1, steps) + 1)):
+        g.replay()
+    torch.cuda.synchronize()
+    times = []
+    cur = torch.cuda.current_stream(dev)
+    for _ in range(5):
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record(cur)
+        g.replay()
+        e1.record(cur)
+        torch.cuda.synchronize()
+        times.append(e0.elapsed_time(e1) / steps)
+    del g
+    return float(np.median(times)), times
+
+
+def cpu_baseline(wl, M, L1, L2, budget_s=20.0):
+    """The oracle's rank-0 Alg. 3 partial, timed on the host on a bounded
+    sample of runs. Reported only."""
+    from oracle import tpdq_oracle as o
+    X = None
+    from paper_2402_04925_amd import inputs
+    X = inputs.make_x(wl, M)
+    P2, _ = o.reorder(L2.g_idx)
+    l1 = (L1.qweight, L1.scales, L1.qzeros, L1.g_idx)
+    l2 = (L2.qweight, L2.scales, L2.qzeros, L2.g_idx)
+    runs = []
+    t_start = time.time()
+    while not runs or (time.time() - t_start < budget_s and len(runs) < 20):
+        t0 = time.perf_counter()
+        o.mlp_rank_from_global(X, l1, l2, 0, wl.tp, True, P2=P2)
+        runs.append(time.perf_counter() - t0)
+    try:
+        from threadpoolctl import threadpool_info
+        cores = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
+    except Exception:
+        cores = os.cpu_count() or 1
+    return dict(value=float(np.median(runs)) * 1e6, unit="us", cores=int(cores), kind="oracle",
+                sample=f"{len(runs)} runs of the oracle's rank-0 MLP shard ({wl.name}, M={M}, "
+                       f"ordered, float64 dequant + GEMM), median")
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--workload", default="llama70b_tp8")
+    ap.add_argument("--M", type=int, default=16)
+    ap.add_argument("--sweep", default="1,4,16", help="extra batch sizes reported alongside")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+
+    if args.gpus != 1:
+        print(f"bench.py runs one GPU's TP share only (the MLP shard of one rank); "
+              f"--gpus {args.gpus} is not supported: collectives are outside this build.",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import paper_2402_04925_amd as tpdq
+    from paper_2402_04925_amd import inputs
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(1)
+    dev = torch.device("cuda:0")
+    wl = inputs.WORKLOADS[args.workload]
+    st = Setup(wl, dev)
+    lib = tpdq._abi.lib()
+    import ctypes
+
+    results = {}
+    Ms = sorted(set([args.M] + [int(m) for m in args.sweep.split(",") if m]))
+    for M in Ms:
+        X = torch.from_numpy(inputs.make_x(wl, M)).to(dev)
+        N1 = wl.N1 // wl.tp
+        K2 = wl.K2 // wl.tp
+        y1 = torch.empty(M, N1, dtype=torch.float16, device=dev)
+        y2 = torch.empty(M, wl.N2, dtype=torch.float16, device=dev)
+        xg = X[:, st.P1.long()].contiguous()   # X[:, P1] for the single-GEMM timings
+        ws = tpdq.Workspace(dev)
+
+        def mk_mlp(rep, path):
+            w1, w2 = (rep[0], rep[1]) if path == tpdq.PATH_ORDERED else (rep[2], rep[3])
+            c1, c2 = w1.c_struct(), w2.c_struct()
+            nb = lib.tpdq_workspace_bytes(tpdq.OP_MLP, M, ctypes.byref(c1), ctypes.byref(c2))
+            buf = ws.get(nb)
+            P1 = st.P1.data_ptr() if path == tpdq.PATH_ORDERED else None
+            keep = (c1, c2)
+
+            def call():
+                tpdq._abi.check(lib.tpdq_mlp_shard(
+                    X.data_ptr(), X.stride(0), M, P1, ctypes.byref(keep[0]), ctypes.byref(keep[1]),
+                    path, tpdq.FP16, y1.data_ptr(), y2.data_ptr(), buf.data_ptr(), buf.numel(),
+                    torch.cuda.current_stream(dev).cuda_stream))
+            return call
+
+        def mk_gemm(rep, which, path):
+            w = rep[which] if path == tpdq.PATH_ORDERED else rep[2 + which]
+            c = w.c_struct()
+            nb = lib.tpdq_workspace_bytes(tpdq.OP_GEMM, M, ctypes.byref(c), None)
+            buf = ws.get(nb)
+            xin = (xg if path == tpdq.PATH_ORDERED else X) if which == 0 else y1
+            out = y1 if which == 0 else y2
+
+            def call():
+                tpdq._abi.check(lib.tpdq_w4a16_gemm(
+                    xin.data_ptr(), xin.stride(0), M, None, ctypes.byref(c), path, tpdq.FP16,
+                    out.data_ptr(), out.stride(0), buf.data_ptr(), buf.numel(),
+                    torch.cuda.current_stream(dev).cuda_stream))
+            return call
+
+        r = {}
+        for pname, path in (("ordered", tpdq.PATH_ORDERED), ("actorder", tpdq.PATH_ACTORDER)):
+            ms, _ = capture_and_time([mk_mlp(rep, path) for rep in st.reps], args.steps, args.warmup, dev)
+            g1, _ = capture_and_time([mk_gemm(rep, 0, path) for rep in st.reps], args.steps, args.warmup, dev)
+            g2, _ = capture_and_time([mk_gemm(rep, 1, path) for rep in st.reps], args.steps, args.warmup, dev)
+            r[pname] = dict(mlp_us=ms * 1e3, gemm1_us=g1 * 1e3, gemm2_us=g2 * 1e3)
+            eprint(f"[bench] M={M} {pname}: mlp {ms*1e3:.2f} us, gemm1 {g1*1e3:.2f} us, gemm2 {g2*1e3:.2f} us")
+        ng2_act = wl.K2 // wl.G
+        b1 = gemm_bytes(M, wl.K1, N1, wl.G)
+        b2 = gemm_bytes(M, K2, wl.N2, wl.G)
+        b_mlp = b1 + b2 + wl.K1 * 4   # + P1 for the gather
+        b1a = gemm_bytes(M, wl.K1, N1, wl.G, gidx=True)
+        b2a = gemm_bytes(M, K2, wl.N2, wl.G, ng=ng2_act, gidx=True)
+        flops = 2 * M * (wl.K1 * N1 + K2 * wl.N2)
+        r["bytes"] = dict(gemm1=b1, gemm2=b2, mlp=b_mlp, gemm1_actorder=b1a, gemm2_actorder=b2a)
+        r["flops"] = flops
+        results[M] = r
+        torch.cuda.synchronize()
+
+    M = args.M
+    r = results[M]
+    o_ = r["ordered"]
+    b = r["bytes"]
+    mlp_us = o_["mlp_us"]
+    kern_us = o_["gemm1_us"] + o_["gemm2_us"]
+    achieved = (b["gemm1"] + b["gemm2"]) / (kern_us * 1e-6) / 1e9
+    traffic = read_traffic(wl.name, M)
+    roof = dict(bound="hbm", achieved=round(achieved, 1), peak=HBM_PEAK_GBS, unit="GB/s",
+                frac=round(achieved / HBM_PEAK_GBS, 4), traffic=traffic,
+                kernel="k_decode_ordered (GEMM1 and GEMM2 launches averaged)")
+    cpu = None
+    if not args.no_cpu_baseline:
+        cpu = cpu_baseline(wl, M, st.L1, st.L2)
+
+    sweep = {}
+    for m, rr in results.items():
+        bb = rr["bytes"]
+        sweep[str(m)] = dict(
+            ordered_mlp_us=round(rr["ordered"]["mlp_us"], 3),
+            actorder_mlp_us=round(rr["actorder"]["mlp_us"], 3),
+            speedup_ordered_vs_actorder=round(rr["actorder"]["mlp_us"] / rr["ordered"]["mlp_us"], 3),
+            ordered_gemm_us=[round(rr["ordered"]["gemm1_us"], 3), round(rr["ordered"]["gemm2_us"], 3)],
+            actorder_gemm_us=[round(rr["actorder"]["gemm1_us"], 3), round(rr["actorder"]["gemm2_us"], 3)],
+            ordered_mlp_gbs=round(bb["mlp"] / (rr["ordered"]["mlp_us"] * 1e-6) / 1e9, 1),
+            ordered_gemm_gbs=round((bb["gemm1"] + bb["gemm2"]) /
+                                   ((rr["ordered"]["gemm1_us"] + rr["ordered"]["gemm2_us"]) * 1e-6) / 1e9, 1),
+            actorder_gemm_gbs=round((bb["gemm1_actorder"] + bb["gemm2_actorder"]) /
+                                    ((rr["actorder"]["gemm1_us"] + rr["actorder"]["gemm2_us"]) * 1e-6) / 1e9, 1),
+            ordered_tflops=round(rr["flops"] / (rr["ordered"]["mlp_us"] * 1e-6) / 1e12, 2),
+        )
+    out = dict(
+        metric=METRIC, value=round(mlp_us, 3), unit="us", n_gpus=1, steps=args.steps,
+        warmup=args.warmup, ms_per_step=round(mlp_us / 1e3, 6), higher_is_better=False,
+        scaling="weak", vs_baseline=None, dtype="f16", data="synthetic",
+        config=dict(workload=f"{wl.name}: rank-0 TP-aware MLP shard, W1 {wl.K1}x{wl.N1 // wl.tp}, "
+                             f"W2 {wl.K2 // wl.tp}x{wl.N2}, int4 G={wl.G}, fp16 X, M={M}",
+                    M=M, tp=wl.tp, path="ordered (Alg. 3)", weight_replicas=st.R,
+                    timing="HIP graph replay, events, median of 5"),
+        hbm_gbs=round(b["mlp"] / (mlp_us * 1e-6) / 1e9, 1),
+        hbm_frac=round(b["mlp"] / (mlp_us * 1e-6) / 1e9 / HBM_PEAK_GBS, 4),
+        tflops=round(r["flops"] / (mlp_us * 1e-6) / 1e12, 3),
+        speedup_vs_actorder=round(r["actorder"]["mlp_us"] / mlp_us, 3),
+        roofline=roof, cpu_baseline=cpu, sweep=sweep,
+        paper_context="paper: up to 1.81x (Llama-70B) / 1.78x (Granite-20B) Alg. 3 vs Alg. 2 on "
+                      "A100/H100 DGX, multi-GPU, communication included; not comparable",
+    )
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

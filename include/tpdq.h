@@ -1,0 +1,188 @@
+/*
+ * tpdq.h - C ABI of libtpdq: TP-aware dequantization (arXiv 2402.04925) for
+ * AMD Instinct MI355X (gfx950).
+ *
+ * The library computes the hot path of the paper's method on one GPU:
+ *   - the offline reorder of an act-order GPTQ layer pair (Alg. 1, and the
+ *     TP-aware fold of section 2.2 / Alg. 3's inputs W1[P1, P2] and W2[P2]);
+ *   - the W4A16 dequantize-and-multiply, both with per-row metadata fetched
+ *     through an unordered g_idx (Eq. 3, the load of Fig. 1) and with sorted
+ *     rows whose group of row k is floor(k / G) (Eq. 1, the load of Fig. 2);
+ *   - one rank's share of the TP-aware MLP, Alg. 3 without its AllReduce:
+ *     Y1 = X[:, P1] @ W1_local, Y2 = Y1 @ W2_local.
+ *
+ * Conventions shared by every entry point
+ *   - Every tensor pointer is DEVICE memory owned by the caller. The library
+ *     never allocates device memory and never frees what it is given.
+ *   - Work is enqueued on `stream` (a hipStream_t passed as void*; NULL is the
+ *     legacy default stream). Unless stated otherwise a call returns right
+ *     after validation and launch; the results are ready when the stream is.
+ *   - Matrices are row-major; every leading dimension `ld_*` is in elements
+ *     of the array it describes.
+ *   - Arguments are validated on the host before anything is enqueued: a
+ *     non-OK status means no work was enqueued (except where stated for
+ *     tpdq_reorder). tpdq_last_error() then gives a one-line reason.
+ *   - Faults inside a kernel surface at the caller's next synchronisation.
+ *   - Outputs must not alias inputs.
+ *
+ * Storage format of a quantized layer (the paper fixes none; this is the
+ * GPTQ layout: group quantization of a K x N weight, section 1.1):
+ *   qweight int32 [K/8][ld_q]   nibble j (bits 4j..4j+3) of word [r][n] is
+ *                               the unsigned 4-bit code q of row 8r+j, col n
+ *   scales  fp16  [num_groups][ld_s]     one scale s per (group, column)
+ *   qzeros  int32 [num_groups][ld_z]     nibble j of word [g][c] is the
+ *                               4-bit zero code z of group g, column 8c+j
+ *   g_idx   int32 [K]           group of row k
+ *   dequantized weight: W[k][n] = s[g][n] * (q[k][n] - z[g][n]), g = g_idx[k]
+ * A sorted ("ordered") layer has g_idx[k] == floor(k / G) (Eq. 1); the
+ * ordered kernels then never read g_idx.
+ */
+#ifndef TPDQ_H
+#define TPDQ_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  TPDQ_OK = 0,
+  TPDQ_ERR_NULL = 1,        /* a required pointer is NULL                              */
+  TPDQ_ERR_SHAPE = 2,       /* K%8, N%8, G%8, K%G (sorted rows), K2 != N1, M < 1, ld too small */
+  TPDQ_ERR_ALIGN = 3,       /* a pointer or leading dimension breaks the vector alignment */
+  TPDQ_ERR_GIDX = 4,        /* g_idx out of range, or a group without exactly G rows    */
+  TPDQ_ERR_WORKSPACE = 5,   /* workspace NULL or smaller than tpdq_workspace_bytes()    */
+  TPDQ_ERR_UNSUPPORTED = 6, /* valid request this build does not implement              */
+  TPDQ_ERR_HIP = 7          /* a HIP runtime call or a kernel launch failed             */
+} tpdq_status;
+
+typedef enum { TPDQ_FP16 = 0, TPDQ_BF16 = 1 } tpdq_dtype;
+
+typedef enum {
+  /* Per-row metadata through g_idx (Eq. 3; the naive load of Fig. 1). The
+     scale and zero of row k are those of group g_idx[k]. */
+  TPDQ_PATH_ACTORDER = 0,
+  /* Rows sorted by group (Alg. 1; the optimized load of Fig. 2): the group of
+     local row k is floor(k / G); g_idx is ignored and may be NULL. */
+  TPDQ_PATH_ORDERED = 1
+} tpdq_path;
+
+/* One quantized layer, or a shard of one given as views (pointer offsets and
+ * leading dimensions). K = input features (rows), N = output features.
+ * num_groups is the number of metadata rows: K/G for a whole or sorted layer;
+ * an act-order row-parallel shard keeps the global metadata and global g_idx
+ * values, so there num_groups = K_global/G exceeds K/G.
+ * Alignment: qweight 16 B and ld_q % 4 == 0; scales 8 B and ld_s % 4 == 0;
+ * qzeros 4 B; g_idx 16 B. */
+typedef struct tpdq_w4 {
+  const int32_t* qweight;
+  int64_t ld_q;        /* >= N     */
+  const void* scales;  /* fp16 (TPDQ_FP16) or bf16 (TPDQ_BF16) */
+  int64_t ld_s;        /* >= N     */
+  const int32_t* qzeros;
+  int64_t ld_z;        /* >= N/8   */
+  const int32_t* g_idx;
+  int32_t K;
+  int32_t N;
+  int32_t group_size;  /* G, a multiple of 8 */
+  int32_t num_groups;
+} tpdq_w4;
+
+/*
+ * tpdq_reorder - offline reorder (Alg. 1) and TP-aware fold (section 2.2).
+ *
+ * For the global (unsharded) layers w1 (K1 x N1) and, optionally, w2
+ * (K2 x N2 with K2 == N1), both act-order (g_idx per Eq. 3):
+ *   P1 = stable ascending argsort of w1->g_idx, g1_sorted = w1->g_idx[P1];
+ *   if w2: P2 = stable argsort of w2->g_idx, g2_sorted = w2->g_idx[P2];
+ *   qweight1_out = W1[P1, P2]   (rows gathered by P1, columns by P2;
+ *                                without w2 the columns stay in place)
+ *   scales1_out  = scales1[:, P2], qzeros1_out = qzeros1[:, P2] (repacked)
+ *   qweight2_out = W2[P2]       (rows gathered by P2; scales2 and qzeros2 are
+ *                                indexed by group and are reused unchanged)
+ * A gather: new index j takes old index P[j]. Ties in the sort keep ascending
+ * row order, so P is unique (any stable sort gives the same P).
+ *
+ * Requirements: every g_idx value in [0, K/G) and every group holding exactly
+ * G rows (what Eq. 3 gives for a permutation phi with G | K); K%G == 0,
+ * G%8 == 0, N%8 == 0. Outputs are dense: qweight1_out int32 [K1/8][N1],
+ * scales1_out [K1/G][N1] (the dtype of w1->scales), qzeros1_out int32
+ * [K1/G][N1/8], qweight2_out int32 [K2/8][N2], P and g_sorted int32 [K].
+ * P2, g2_sorted and qweight2_out must be NULL when w2 is NULL.
+ *
+ * Workspace: at least tpdq_workspace_bytes(0, 0, w1, w2) bytes, any content.
+ * This call is synchronous in part: it runs the g_idx validation on `stream`
+ * and waits for it; on TPDQ_ERR_GIDX nothing has been written to the outputs.
+ * After a successful validation the permutation kernels are enqueued and the
+ * call returns without waiting for them.
+ */
+tpdq_status tpdq_reorder(const tpdq_w4* w1, const tpdq_w4* w2,
+                         int32_t* P1, int32_t* g1_sorted, int32_t* P2, int32_t* g2_sorted,
+                         int32_t* qweight1_out, void* scales1_out, int32_t* qzeros1_out,
+                         int32_t* qweight2_out, tpdq_dtype dtype,
+                         void* workspace, size_t ws_bytes, void* stream);
+
+/*
+ * tpdq_w4a16_gemm - Y = X' @ deq(W), fp32 accumulation, result rounded to
+ * the activation dtype (round to nearest even).
+ *
+ * X  [M][ldx] activations (K columns used); X' = X, or X[:, x_perm] when
+ *    x_perm (int32 [K], device) is given: column j of X' is column x_perm[j]
+ *    of X (the X[:, P1] gather of Alg. 2 and Alg. 3). Alignment 16 B and
+ *    ldx % 8 == 0 when x_perm is NULL; 2 B otherwise.
+ * w  the layer; path selects the metadata load (see tpdq_path).
+ *    TPDQ_PATH_ACTORDER needs w->g_idx; values outside [0, num_groups) are
+ *    clamped into range (no fault; such rows give unspecified results).
+ * Y  [M][ldy] output, 8 B aligned, ldy % 4 == 0, ldy >= N.
+ * Workspace: at least tpdq_workspace_bytes(1, M, w, NULL) bytes, zero-filled
+ * before its first use with this library; every call leaves its counter words
+ * zero again when it completes. Calls that overlap in time must not share a
+ * workspace. Deterministic: the same inputs give bit-identical outputs.
+ */
+tpdq_status tpdq_w4a16_gemm(const void* X, int64_t ldx, int32_t M, const int32_t* x_perm,
+                            const tpdq_w4* w, tpdq_path path, tpdq_dtype dtype,
+                            void* Y, int64_t ldy,
+                            void* workspace, size_t ws_bytes, void* stream);
+
+/*
+ * tpdq_mlp_shard - one rank's share of the MLP up to its AllReduce.
+ *
+ * TPDQ_PATH_ORDERED (Alg. 3): w1 is the rank's column shard of W1[P1, P2],
+ *   w2 its row shard of W2[P2] (sorted rows, so local groups are floor(k/G));
+ *   Y1 = X[:, P1] @ deq(w1), Y2_partial = Y1 @ deq(w2). No permute or gather
+ *   of Y1 happens between the GEMMs. P1 (int32 [K1], global) is required.
+ * TPDQ_PATH_ACTORDER: w1 is the rank's column shard of W1 with its g_idx, w2
+ *   the row shard of W2 with its rows' global g_idx values and the full
+ *   metadata (num_groups = K2_global/G); P1 must be NULL.
+ * Requirements: w2->K == w1->N. X [M][ldx] with w1->K columns used.
+ * Y1 [M][w1->N] and Y2_partial [M][w2->N], dense, written in the activation
+ * dtype; Y2_partial is this rank's summand of the AllReduce(SUM) of Alg. 3.
+ * Workspace: tpdq_workspace_bytes(2, M, w1, w2) bytes, zero-filled before
+ * first use, as for tpdq_w4a16_gemm.
+ */
+tpdq_status tpdq_mlp_shard(const void* X, int64_t ldx, int32_t M, const int32_t* P1,
+                           const tpdq_w4* w1, const tpdq_w4* w2, tpdq_path path,
+                           tpdq_dtype dtype, void* Y1, void* Y2_partial,
+                           void* workspace, size_t ws_bytes, void* stream);
+
+/* Workspace bytes for op 0 (tpdq_reorder: a = w1, b = w2 or NULL),
+ * 1 (tpdq_w4a16_gemm: a = w) or 2 (tpdq_mlp_shard: a = w1, b = w2) at batch
+ * M. Returns 0 when the arguments are invalid. */
+size_t tpdq_workspace_bytes(int op, int32_t M, const tpdq_w4* a, const tpdq_w4* b);
+
+/* Static description of a status code. */
+const char* tpdq_status_string(tpdq_status s);
+
+/* Detail of the last non-OK status returned on the calling thread. */
+const char* tpdq_last_error(void);
+
+/* Library version, e.g. "0.1.0". */
+const char* tpdq_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* TPDQ_H */

@@ -133,13 +133,17 @@ def dequant(qweight, scales, qzeros, g_idx, cols=None) -> np.ndarray:
     Row k takes its scale and zero from group g_idx[k] (Eq. 3 for act-order,
     Eq. 1 / the sorted g_idx for ordered weights). `cols` restricts the result
     to a subset of output columns."""
-    q = unpack_rows(qweight)
-    z = unpack_cols(qzeros)
-    s = np.asarray(scales).astype(np.float64)
     g = np.asarray(g_idx, dtype=np.int64)
-    if cols is not None:
+    if cols is None:
+        q = unpack_rows(qweight)
+        z = unpack_cols(qzeros)
+        s = np.asarray(scales).astype(np.float64)
+    else:
+        # codes are packed along K, so a column of words is a column of codes
         cols = np.asarray(cols, dtype=np.int64)
-        q, z, s = q[:, cols], z[:, cols], s[:, cols]
+        q = unpack_rows(np.asarray(qweight)[:, cols])
+        z = unpack_cols(qzeros)[:, cols]
+        s = np.asarray(scales)[:, cols].astype(np.float64)
     return s[g, :] * (q - z[g, :]).astype(np.float64)
 
 
@@ -180,15 +184,21 @@ def fold(w1, w2, P1, P2):
     P1 = np.asarray(P1, dtype=np.int64)
     P2 = np.asarray(P2, dtype=np.int64)
     q1 = unpack_rows(w1["qweight"])[P1][:, P2]
-    z1 = unpack_cols(w1["qzeros"])[:, P2]
-    s1 = np.asarray(w1["scales"])[:, P2]
-    out1 = dict(qweight=pack_rows(q1), scales=s1.copy(), qzeros=pack_cols(z1))
+    s1, z1 = fold_meta(w1["scales"], w1["qzeros"], P2)
+    out1 = dict(qweight=pack_rows(q1), scales=s1, qzeros=z1)
     out2 = None
     if w2 is not None:
         q2 = unpack_rows(w2["qweight"])[P2]
         out2 = dict(qweight=pack_rows(q2), scales=np.asarray(w2["scales"]).copy(),
                     qzeros=np.asarray(w2["qzeros"]).copy())
     return out1, out2
+
+
+def fold_meta(scales, qzeros, P2):
+    """Metadata of W1[P1, P2]: the scale and zero of each (group, column)
+    follow the column gather by P2 (rows are indexed by group, not by row)."""
+    P2 = np.asarray(P2, dtype=np.int64)
+    return np.asarray(scales)[:, P2].copy(), pack_cols(unpack_cols(qzeros)[:, P2])
 
 
 def permute_rows(w, P):
@@ -307,6 +317,39 @@ def mlp_tp_aware(X, P1, w1f, w2f, G, tp, acc="f64"):
         _, y2 = mlp_tp_aware_rank(X, P1, column_shard(w1f, r, tp), row_shard(w2f, r, tp, G), G, acc)
         partials.append(y2)
     return all_reduce_sum(partials), partials
+
+
+def fold_sample(qweight, P_row, P_col, rows, cols):
+    """Codes of W[P_row, P_col] at rows x cols (P_col None: columns in place),
+    read from the source words element by element; for layers too large to
+    unpack whole. New row j / column c take old row P_row[j] / column P_col[c]."""
+    src_rows = np.asarray(P_row, dtype=np.int64)[np.asarray(rows, dtype=np.int64)]
+    cols = np.asarray(cols, dtype=np.int64)
+    src_cols = cols if P_col is None else np.asarray(P_col, dtype=np.int64)[cols]
+    words = np.asarray(qweight).view(np.uint32)[np.ix_(src_rows // 8, src_cols)]
+    shift = (4 * (src_rows % 8)).astype(np.uint32)[:, None]
+    return ((words >> shift) & np.uint32(0xF)).astype(np.int64)
+
+
+def mlp_rank_from_global(X, l1, l2, rank, tp, ordered, P2=None, cols2=None, acc="f64"):
+    """One rank's (Y1, Y2 partial[:, cols2]) computed from the unpermuted
+    global layers l1 = (qweight, scales, qzeros, g_idx) and l2.
+
+    Act-order rank (Megatron shards of the original layers): W1 columns and
+    W2 rows [rank*n, (rank+1)*n), n = N1/tp.
+    TP-aware rank (Alg. 3): its W1[P1, P2] column block holds original columns
+    P2[block] with rows relabelled by P1, and its W2[P2] row block holds
+    original rows P2[block]; since relabelling the rows of W1 together with
+    the columns of X (X[:, P1]) leaves every dot product's terms unchanged, the
+    partial is X @ deq(W1)[:, P2[block]] then @ deq(W2)[P2[block], :]."""
+    N1 = np.asarray(l1[0]).shape[1]
+    n = N1 // tp
+    blk = np.arange(rank * n, (rank + 1) * n)
+    sel = np.asarray(P2, dtype=np.int64)[blk] if ordered else blk
+    Y1 = to_fp16(matmul(X, dequant(*l1, cols=sel), acc))
+    W2 = dequant(*l2, cols=cols2)[sel]
+    Y2 = to_fp16(matmul(Y1, W2, acc))
+    return Y1, Y2
 
 
 # ----------------------------------------------------------------------------

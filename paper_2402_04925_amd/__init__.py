@@ -1,0 +1,228 @@
+"""tpdq: TP-aware dequantization (arXiv 2402.04925) on AMD MI355X.
+
+Thin Python binding of libtpdq (include/tpdq.h). Every function here only
+marshals torch tensors (device memory and the current stream) into the C ABI;
+all computation runs in the library's HIP kernels. If the library is not
+built, calls raise: there is no fallback.
+"""
+from __future__ import annotations
+
+import ctypes
+import dataclasses
+from typing import Optional
+
+from . import _abi
+from ._abi import (BF16, FP16, OP_GEMM, OP_MLP, OP_REORDER, PATH_ACTORDER, PATH_ORDERED,
+                   TpdqError)
+
+__all__ = [
+    "QuantWeight", "reorder", "w4a16_gemm", "mlp_shard", "workspace_bytes", "Workspace",
+    "TpdqError", "PATH_ACTORDER", "PATH_ORDERED", "FP16", "BF16", "version",
+]
+
+
+def _torch():
+    import torch
+    return torch
+
+
+def version() -> str:
+    return _abi.lib().tpdq_version().decode()
+
+
+def _ptr(t) -> Optional[int]:
+    return None if t is None else t.data_ptr()
+
+
+def _stream_handle(device) -> int:
+    torch = _torch()
+    return torch.cuda.current_stream(device).cuda_stream
+
+
+def _dtype_code(dt) -> int:
+    torch = _torch()
+    if dt == torch.float16:
+        return FP16
+    if dt == torch.bfloat16:
+        return BF16
+    raise TypeError(f"activations and scales must be float16 or bfloat16, got {dt}")
+
+
+@dataclasses.dataclass
+class QuantWeight:
+    """A quantized layer (or a shard of one as views) in device memory.
+
+    qweight int32 [K/8][>=N], scales fp16 [num_groups][>=N],
+    qzeros int32 [num_groups][>=N/8], g_idx int32 [K] or None.
+    """
+    qweight: object
+    scales: object
+    qzeros: object
+    g_idx: object
+    K: int
+    N: int
+    G: int
+    num_groups: int
+
+    @classmethod
+    def from_tensors(cls, qweight, scales, qzeros, g_idx, G: int, num_groups: Optional[int] = None):
+        K = qweight.shape[0] * 8
+        N = qweight.shape[1]
+        ng = scales.shape[0] if num_groups is None else num_groups
+        return cls(qweight, scales, qzeros, g_idx, K, N, G, ng)
+
+    def c_struct(self) -> _abi.W4:
+        for name in ("qweight", "scales", "qzeros"):
+            t = getattr(self, name)
+            if t.stride(1) != 1:
+                raise ValueError(f"{name} must have unit column stride")
+        if self.g_idx is not None and not self.g_idx.is_contiguous():
+            raise ValueError("g_idx must be contiguous")
+        return _abi.W4(
+            qweight=_ptr(self.qweight), ld_q=self.qweight.stride(0),
+            scales=_ptr(self.scales), ld_s=self.scales.stride(0),
+            qzeros=_ptr(self.qzeros), ld_z=self.qzeros.stride(0),
+            g_idx=_ptr(self.g_idx), K=self.K, N=self.N, group_size=self.G,
+            num_groups=self.num_groups)
+
+    @property
+    def device(self):
+        return self.qweight.device
+
+    def column_shard(self, rank: int, tp: int) -> "QuantWeight":
+        """Megatron column-parallel shard (views): columns [rank*N/tp, ...)."""
+        n = self.N // tp
+        c0 = rank * n
+        return QuantWeight(self.qweight[:, c0:c0 + n], self.scales[:, c0:c0 + n],
+                           self.qzeros[:, c0 // 8:(c0 + n) // 8], self.g_idx, self.K, n, self.G,
+                           self.num_groups)
+
+    def row_shard(self, rank: int, tp: int, sorted_rows: bool) -> "QuantWeight":
+        """Megatron row-parallel shard (views): rows [rank*K/tp, ...).
+
+        Sorted rows keep only their own consecutive groups; act-order rows
+        keep the global g_idx values of their rows and all the metadata."""
+        k = self.K // tp
+        r0 = rank * k
+        qw = self.qweight[r0 // 8:(r0 + k) // 8]
+        g = None if self.g_idx is None else self.g_idx[r0:r0 + k]
+        if sorted_rows:
+            g0, ng = r0 // self.G, k // self.G
+            return QuantWeight(qw, self.scales[g0:g0 + ng], self.qzeros[g0:g0 + ng], g, k, self.N,
+                               self.G, ng)
+        return QuantWeight(qw, self.scales, self.qzeros, g, k, self.N, self.G, self.num_groups)
+
+
+class Workspace:
+    """Zero-initialised device scratch for the library calls, grown on demand.
+
+    The kernels leave their counter words at zero, so one workspace can serve
+    any number of calls issued one after another on one stream."""
+
+    def __init__(self, device=None):
+        self.device = device
+        self.buf = None
+
+    def get(self, nbytes: int):
+        torch = _torch()
+        if self.buf is None or self.buf.numel() < nbytes:
+            n = max(nbytes, 1 << 20)
+            self.buf = torch.zeros(n, dtype=torch.uint8, device=self.device)
+        return self.buf
+
+
+_default_ws = {}
+
+
+def _workspace(device, nbytes, ws: Optional[Workspace]):
+    if ws is None:
+        key = (str(device), _stream_handle(device))
+        ws = _default_ws.get(key)
+        if ws is None:
+            ws = _default_ws[key] = Workspace(device)
+    return ws.get(nbytes)
+
+
+def workspace_bytes(op: int, M: int, a: QuantWeight, b: Optional[QuantWeight] = None) -> int:
+    ca = a.c_struct()
+    cb = b.c_struct() if b is not None else None
+    return _abi.lib().tpdq_workspace_bytes(op, M, ctypes.byref(ca),
+                                          ctypes.byref(cb) if cb is not None else None)
+
+
+def reorder(w1: QuantWeight, w2: Optional[QuantWeight] = None, workspace: Optional[Workspace] = None):
+    """Alg. 1 on w1 (and w2) plus the TP-aware fold W1[P1, P2], W2[P2].
+
+    Returns (P1, g1_sorted, P2, g2_sorted, w1_out, w2_out); P2, g2_sorted and
+    w2_out are None without w2. w1_out/w2_out are sorted-row QuantWeights
+    (their g_idx is the sorted g_idx)."""
+    torch = _torch()
+    dev = w1.device
+    i32 = dict(dtype=torch.int32, device=dev)
+    P1 = torch.empty(w1.K, **i32)
+    g1 = torch.empty(w1.K, **i32)
+    q1 = torch.empty(w1.K // 8, w1.N, **i32)
+    s1 = torch.empty(w1.num_groups, w1.N, dtype=w1.scales.dtype, device=dev)
+    z1 = torch.empty(w1.num_groups, w1.N // 8, **i32)
+    P2 = g2 = q2 = None
+    if w2 is not None:
+        P2 = torch.empty(w2.K, **i32)
+        g2 = torch.empty(w2.K, **i32)
+        q2 = torch.empty(w2.K // 8, w2.N, **i32)
+    c1 = w1.c_struct()
+    c2 = w2.c_struct() if w2 is not None else None
+    lib = _abi.lib()
+    nbytes = lib.tpdq_workspace_bytes(OP_REORDER, 0, ctypes.byref(c1),
+                                      ctypes.byref(c2) if c2 is not None else None)
+    buf = _workspace(dev, nbytes, workspace)
+    _abi.check(lib.tpdq_reorder(
+        ctypes.byref(c1), ctypes.byref(c2) if c2 is not None else None,
+        _ptr(P1), _ptr(g1), _ptr(P2), _ptr(g2), _ptr(q1), _ptr(s1), _ptr(z1), _ptr(q2),
+        _dtype_code(w1.scales.dtype), _ptr(buf), buf.numel(), _stream_handle(dev)))
+    w1o = QuantWeight(q1, s1, z1, g1, w1.K, w1.N, w1.G, w1.num_groups)
+    w2o = None
+    if w2 is not None:
+        w2o = QuantWeight(q2, w2.scales, w2.qzeros, g2, w2.K, w2.N, w2.G, w2.num_groups)
+    return P1, g1, P2, g2, w1o, w2o
+
+
+def w4a16_gemm(X, w: QuantWeight, path: int, x_perm=None, out=None,
+               workspace: Optional[Workspace] = None):
+    """Y = X' @ deq(w) with X' = X or X[:, x_perm]; fp32 accumulation."""
+    torch = _torch()
+    if X.dim() != 2 or X.stride(1) != 1:
+        raise ValueError("X must be 2-D with unit column stride")
+    M = X.shape[0]
+    if out is None:
+        out = torch.empty(M, w.N, dtype=X.dtype, device=X.device)
+    cw = w.c_struct()
+    lib = _abi.lib()
+    nbytes = lib.tpdq_workspace_bytes(OP_GEMM, M, ctypes.byref(cw), None)
+    buf = _workspace(X.device, nbytes, workspace)
+    _abi.check(lib.tpdq_w4a16_gemm(
+        _ptr(X), X.stride(0), M, _ptr(x_perm), ctypes.byref(cw), path, _dtype_code(X.dtype),
+        _ptr(out), out.stride(0), _ptr(buf), buf.numel(), _stream_handle(X.device)))
+    return out
+
+
+def mlp_shard(X, w1: QuantWeight, w2: QuantWeight, path: int, P1=None, y1=None, y2=None,
+              workspace: Optional[Workspace] = None):
+    """One rank's Alg. 3 (ordered) or act-order MLP share, up to the AllReduce.
+    Returns (Y1, Y2_partial)."""
+    torch = _torch()
+    if X.dim() != 2 or X.stride(1) != 1:
+        raise ValueError("X must be 2-D with unit column stride")
+    M = X.shape[0]
+    if y1 is None:
+        y1 = torch.empty(M, w1.N, dtype=X.dtype, device=X.device)
+    if y2 is None:
+        y2 = torch.empty(M, w2.N, dtype=X.dtype, device=X.device)
+    c1, c2 = w1.c_struct(), w2.c_struct()
+    lib = _abi.lib()
+    nbytes = lib.tpdq_workspace_bytes(OP_MLP, M, ctypes.byref(c1), ctypes.byref(c2))
+    buf = _workspace(X.device, nbytes, workspace)
+    _abi.check(lib.tpdq_mlp_shard(
+        _ptr(X), X.stride(0), M, _ptr(P1), ctypes.byref(c1), ctypes.byref(c2), path,
+        _dtype_code(X.dtype), _ptr(y1), _ptr(y2), _ptr(buf), buf.numel(),
+        _stream_handle(X.device)))
+    return y1, y2

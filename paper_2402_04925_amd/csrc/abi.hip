@@ -1,0 +1,334 @@
+// extern "C" entry points of libtpdq: argument validation, workspace layout
+// and dispatch to the gfx950 kernels. Nothing here touches tensor data on the
+// host; every step of the computation runs in the kernels.
+#include <stdarg.h>
+#include <stdio.h>
+
+#include <algorithm>
+#include <string>
+
+#include "tpdq_internal.h"
+
+using namespace tpdq;
+
+namespace {
+
+thread_local std::string g_last_error;
+
+tpdq_status fail(tpdq_status st, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof(buf), fmt, ap);
+  va_end(ap);
+  g_last_error = buf;
+  return st;
+}
+
+tpdq_status hip_fail(hipError_t e, const char* what) {
+  return fail(TPDQ_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+bool aligned(const void* p, size_t a) { return ((uintptr_t)p % a) == 0; }
+
+// Shape and pointer checks of one layer. `need_gidx`: the act-order path
+// reads g_idx; `sorted`: the group of row k is k / G, so G must divide K and
+// num_groups cover K / G.
+tpdq_status check_layer(const tpdq_w4* w, const char* name, bool need_gidx, bool sorted) {
+  if (!w) return fail(TPDQ_ERR_NULL, "%s is NULL", name);
+  if (!w->qweight || !w->scales || !w->qzeros)
+    return fail(TPDQ_ERR_NULL, "%s: qweight, scales and qzeros are required", name);
+  if (need_gidx && !w->g_idx) return fail(TPDQ_ERR_NULL, "%s: g_idx is required", name);
+  if (w->K <= 0 || w->N <= 0 || w->group_size <= 0 || w->num_groups <= 0)
+    return fail(TPDQ_ERR_SHAPE, "%s: K=%d N=%d G=%d num_groups=%d must be positive", name, w->K,
+                w->N, w->group_size, w->num_groups);
+  if (w->K % 8 || w->N % 8 || w->group_size % 8)
+    return fail(TPDQ_ERR_SHAPE, "%s: K=%d, N=%d and G=%d must be multiples of 8", name, w->K, w->N,
+                w->group_size);
+  if (sorted) {
+    if (w->K % w->group_size)
+      return fail(TPDQ_ERR_SHAPE, "%s: sorted rows need G | K (K=%d G=%d)", name, w->K,
+                  w->group_size);
+    if (w->num_groups < w->K / w->group_size)
+      return fail(TPDQ_ERR_SHAPE, "%s: num_groups=%d < K/G=%d", name, w->num_groups,
+                  w->K / w->group_size);
+  }
+  if (w->ld_q < w->N || w->ld_s < w->N || w->ld_z < w->N / 8)
+    return fail(TPDQ_ERR_SHAPE, "%s: leading dimensions too small (ld_q=%lld ld_s=%lld ld_z=%lld)",
+                name, (long long)w->ld_q, (long long)w->ld_s, (long long)w->ld_z);
+  if (!aligned(w->qweight, 16) || w->ld_q % 4)
+    return fail(TPDQ_ERR_ALIGN, "%s: qweight needs 16-byte alignment and ld_q %% 4 == 0", name);
+  if (!aligned(w->scales, 8) || w->ld_s % 4)
+    return fail(TPDQ_ERR_ALIGN, "%s: scales need 8-byte alignment and ld_s %% 4 == 0", name);
+  if (!aligned(w->qzeros, 4)) return fail(TPDQ_ERR_ALIGN, "%s: qzeros need 4-byte alignment", name);
+  if (need_gidx && !aligned(w->g_idx, 16))
+    return fail(TPDQ_ERR_ALIGN, "%s: g_idx needs 16-byte alignment", name);
+  return TPDQ_OK;
+}
+
+// Workspace layout of the GEMM and MLP calls:
+//   [counters][split-K partials][gathered activations]
+struct GemmWs {
+  size_t counters = 0, partials = 0, xperm = 0, total = 0;
+};
+
+GemmWs gemm_ws(int M, const tpdq_w4* a, const tpdq_w4* b, bool gather, int Kgather) {
+  const int mc = std::min(M, kDecodeMaxM);
+  int ncol = (a->N + kDecodeCols - 1) / kDecodeCols;
+  size_t part = 0;
+  const int sa = decode_splits(mc, a->K, a->N);
+  if (sa > 1) part = (size_t)sa * mc * a->N * 4;
+  if (b) {
+    ncol = std::max(ncol, (b->N + kDecodeCols - 1) / kDecodeCols);
+    const int sb = decode_splits(mc, b->K, b->N);
+    if (sb > 1) part = std::max(part, (size_t)sb * mc * b->N * 4);
+  }
+  GemmWs w;
+  w.counters = 0;
+  w.partials = align_up((size_t)ncol * 4);
+  w.xperm = w.partials + align_up(part);
+  w.total = w.xperm + (gather ? align_up((size_t)M * Kgather * 2) : 0);
+  return w;
+}
+
+// One GEMM through the decode kernels, M cut into launches of <= 64 rows.
+tpdq_status run_gemm(const uint16_t* X, int64_t ldx, int M, const tpdq_w4* w, tpdq_path path,
+                     uint16_t* Y, int64_t ldy, char* ws, const GemmWs& lay, hipStream_t st) {
+  for (int m0 = 0; m0 < M; m0 += kDecodeMaxM) {
+    const int mc = std::min(kDecodeMaxM, M - m0);
+    GemmArgs a;
+    a.X = X + (int64_t)m0 * ldx;
+    a.ldx = ldx;
+    a.M = mc;
+    a.qw = (const uint32_t*)w->qweight;
+    a.ldq = w->ld_q;
+    a.sc = (const uint16_t*)w->scales;
+    a.lds = w->ld_s;
+    a.qz = (const uint32_t*)w->qzeros;
+    a.ldz = w->ld_z;
+    a.g_idx = w->g_idx;
+    a.K = w->K;
+    a.N = w->N;
+    a.G = w->group_size;
+    a.num_groups = w->num_groups;
+    a.Y = Y + (int64_t)m0 * ldy;
+    a.ldy = ldy;
+    a.splits = decode_splits(mc, w->K, w->N);
+    a.partials = (float*)(ws + lay.partials);
+    a.counters = (uint32_t*)(ws + lay.counters);
+    hipError_t e;
+    if (path == TPDQ_PATH_ORDERED && w->group_size % 32 == 0)
+      e = launch_decode_ordered(a, st);
+    else
+      e = launch_decode_rowmeta(a, path == TPDQ_PATH_ACTORDER, st);
+    if (e != hipSuccess) return hip_fail(e, "decode GEMM launch");
+  }
+  return TPDQ_OK;
+}
+
+tpdq_status check_common(int32_t M, tpdq_path path, tpdq_dtype dtype) {
+  if (M < 1) return fail(TPDQ_ERR_SHAPE, "M=%d must be >= 1", M);
+  if (path != TPDQ_PATH_ACTORDER && path != TPDQ_PATH_ORDERED)
+    return fail(TPDQ_ERR_SHAPE, "unknown path %d", (int)path);
+  if (dtype == TPDQ_BF16) return fail(TPDQ_ERR_UNSUPPORTED, "bf16 activations are not built yet");
+  if (dtype != TPDQ_FP16) return fail(TPDQ_ERR_SHAPE, "unknown dtype %d", (int)dtype);
+  return TPDQ_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* tpdq_version(void) { return "0.1.0"; }
+
+const char* tpdq_status_string(tpdq_status s) {
+  switch (s) {
+    case TPDQ_OK: return "ok";
+    case TPDQ_ERR_NULL: return "null pointer";
+    case TPDQ_ERR_SHAPE: return "invalid shape";
+    case TPDQ_ERR_ALIGN: return "misaligned pointer or leading dimension";
+    case TPDQ_ERR_GIDX: return "invalid g_idx";
+    case TPDQ_ERR_WORKSPACE: return "workspace too small";
+    case TPDQ_ERR_UNSUPPORTED: return "unsupported";
+    case TPDQ_ERR_HIP: return "HIP error";
+  }
+  return "unknown status";
+}
+
+const char* tpdq_last_error(void) { return g_last_error.c_str(); }
+
+size_t tpdq_workspace_bytes(int op, int32_t M, const tpdq_w4* a, const tpdq_w4* b) {
+  if (!a || a->K <= 0 || a->N <= 0 || a->group_size <= 0) return 0;
+  if (op == 0) {
+    size_t n = 256 + align_up((size_t)a->num_groups * 4);
+    if (b) n += align_up((size_t)b->num_groups * 4);
+    return n;
+  }
+  if (M < 1) return 0;
+  if (op == 1) return gemm_ws(M, a, nullptr, true, a->K).total;
+  if (op == 2) {
+    if (!b) return 0;
+    return gemm_ws(M, a, b, true, a->K).total;
+  }
+  return 0;
+}
+
+tpdq_status tpdq_reorder(const tpdq_w4* w1, const tpdq_w4* w2, int32_t* P1, int32_t* g1_sorted,
+                         int32_t* P2, int32_t* g2_sorted, int32_t* qweight1_out,
+                         void* scales1_out, int32_t* qzeros1_out, int32_t* qweight2_out,
+                         tpdq_dtype dtype, void* workspace, size_t ws_bytes, void* stream) {
+  tpdq_status st = check_layer(w1, "w1", true, true);
+  if (st != TPDQ_OK) return st;
+  if (dtype != TPDQ_FP16 && dtype != TPDQ_BF16) return fail(TPDQ_ERR_SHAPE, "unknown dtype");
+  if (w1->num_groups != w1->K / w1->group_size)
+    return fail(TPDQ_ERR_SHAPE, "w1: a global act-order layer has num_groups == K/G");
+  if (!P1 || !g1_sorted || !qweight1_out || !scales1_out || !qzeros1_out)
+    return fail(TPDQ_ERR_NULL, "P1, g1_sorted, qweight1_out, scales1_out, qzeros1_out are required");
+  if (w2) {
+    st = check_layer(w2, "w2", true, true);
+    if (st != TPDQ_OK) return st;
+    if (w2->K != w1->N) return fail(TPDQ_ERR_SHAPE, "w2->K=%d != w1->N=%d", w2->K, w1->N);
+    if (w2->num_groups != w2->K / w2->group_size)
+      return fail(TPDQ_ERR_SHAPE, "w2: a global act-order layer has num_groups == K/G");
+    if (!P2 || !g2_sorted || !qweight2_out)
+      return fail(TPDQ_ERR_NULL, "P2, g2_sorted and qweight2_out are required with w2");
+  } else if (P2 || g2_sorted || qweight2_out) {
+    return fail(TPDQ_ERR_SHAPE, "P2, g2_sorted and qweight2_out must be NULL without w2");
+  }
+  const size_t need = tpdq_workspace_bytes(0, 0, w1, w2);
+  if (!workspace || ws_bytes < need)
+    return fail(TPDQ_ERR_WORKSPACE, "reorder needs %zu workspace bytes, got %zu", need, ws_bytes);
+  if (!aligned(workspace, 16)) return fail(TPDQ_ERR_ALIGN, "workspace needs 16-byte alignment");
+
+  hipStream_t s = (hipStream_t)stream;
+  char* ws = (char*)workspace;
+  uint32_t* flags = (uint32_t*)ws;  // [0] w1, [1] w2
+  uint32_t* counts1 = (uint32_t*)(ws + 256);
+  uint32_t* counts2 = (uint32_t*)(ws + 256 + align_up((size_t)w1->num_groups * 4));
+  const size_t nwords = need / 4;
+  hipError_t e = launch_fill_u32((uint32_t*)ws, nwords, 0u, s);
+  if (e != hipSuccess) return hip_fail(e, "workspace clear");
+
+  ReorderLayer L1{w1->g_idx, w1->K, w1->group_size, w1->num_groups, P1, g1_sorted};
+  ReorderLayer L2{};
+  e = launch_gidx_validate(L1, counts1, flags + 0, s);
+  if (e != hipSuccess) return hip_fail(e, "g_idx validation launch");
+  if (w2) {
+    L2 = ReorderLayer{w2->g_idx, w2->K, w2->group_size, w2->num_groups, P2, g2_sorted};
+    e = launch_gidx_validate(L2, counts2, flags + 1, s);
+    if (e != hipSuccess) return hip_fail(e, "g_idx validation launch");
+  }
+  uint32_t hflags[2] = {0, 0};
+  e = hipMemcpyAsync(hflags, flags, sizeof(hflags), hipMemcpyDeviceToHost, s);
+  if (e == hipSuccess) e = hipStreamSynchronize(s);
+  if (e != hipSuccess) return hip_fail(e, "g_idx validation readback");
+  for (int l = 0; l < 2; ++l) {
+    if (hflags[l] & 1u)
+      return fail(TPDQ_ERR_GIDX, "w%d: a g_idx value is outside [0, K/G)", l + 1);
+    if (hflags[l] & 2u)
+      return fail(TPDQ_ERR_GIDX, "w%d: a group does not hold exactly G rows", l + 1);
+  }
+
+  e = launch_gidx_rank(L1, s);
+  if (e == hipSuccess && w2) e = launch_gidx_rank(L2, s);
+  if (e != hipSuccess) return hip_fail(e, "argsort launch");
+
+  const int32_t* pcol = w2 ? P2 : nullptr;
+  const int ng1 = w1->num_groups;
+  e = launch_permute_qweight((const uint32_t*)w1->qweight, w1->ld_q, w1->K, w1->N, P1, pcol,
+                             (uint32_t*)qweight1_out, s);
+  if (e == hipSuccess)
+    e = launch_permute_scales((const uint16_t*)w1->scales, w1->ld_s, ng1, w1->N, pcol,
+                              (uint16_t*)scales1_out, s);
+  if (e == hipSuccess)
+    e = launch_permute_qzeros((const uint32_t*)w1->qzeros, w1->ld_z, ng1, w1->N, pcol,
+                              (uint32_t*)qzeros1_out, s);
+  if (e == hipSuccess && w2)
+    e = launch_permute_qweight((const uint32_t*)w2->qweight, w2->ld_q, w2->K, w2->N, P2, nullptr,
+                               (uint32_t*)qweight2_out, s);
+  if (e != hipSuccess) return hip_fail(e, "permute launch");
+  return TPDQ_OK;
+}
+
+tpdq_status tpdq_w4a16_gemm(const void* X, int64_t ldx, int32_t M, const int32_t* x_perm,
+                            const tpdq_w4* w, tpdq_path path, tpdq_dtype dtype, void* Y,
+                            int64_t ldy, void* workspace, size_t ws_bytes, void* stream) {
+  tpdq_status st = check_common(M, path, dtype);
+  if (st != TPDQ_OK) return st;
+  st = check_layer(w, "w", path == TPDQ_PATH_ACTORDER, path == TPDQ_PATH_ORDERED);
+  if (st != TPDQ_OK) return st;
+  if (!X || !Y) return fail(TPDQ_ERR_NULL, "X and Y are required");
+  if (ldx < w->K || ldy < w->N)
+    return fail(TPDQ_ERR_SHAPE, "ldx=%lld < K=%d or ldy=%lld < N=%d", (long long)ldx, w->K,
+                (long long)ldy, w->N);
+  if (x_perm) {
+    if (!aligned(X, 2)) return fail(TPDQ_ERR_ALIGN, "X needs 2-byte alignment");
+  } else if (!aligned(X, 16) || ldx % 8) {
+    return fail(TPDQ_ERR_ALIGN, "X needs 16-byte alignment and ldx %% 8 == 0");
+  }
+  if (!aligned(Y, 8) || ldy % 4) return fail(TPDQ_ERR_ALIGN, "Y needs 8-byte alignment, ldy %% 4 == 0");
+  const GemmWs lay = gemm_ws(M, w, nullptr, x_perm != nullptr, w->K);
+  if (!workspace || ws_bytes < lay.total)
+    return fail(TPDQ_ERR_WORKSPACE, "GEMM needs %zu workspace bytes, got %zu", lay.total, ws_bytes);
+  if (!aligned(workspace, 16)) return fail(TPDQ_ERR_ALIGN, "workspace needs 16-byte alignment");
+
+  hipStream_t s = (hipStream_t)stream;
+  char* ws = (char*)workspace;
+  const uint16_t* Xin = (const uint16_t*)X;
+  int64_t ldin = ldx;
+  if (x_perm) {
+    uint16_t* Xp = (uint16_t*)(ws + lay.xperm);
+    hipError_t e = launch_gather_cols(Xin, ldx, M, w->K, x_perm, Xp, s);
+    if (e != hipSuccess) return hip_fail(e, "activation gather launch");
+    Xin = Xp;
+    ldin = w->K;
+  }
+  return run_gemm(Xin, ldin, M, w, path, (uint16_t*)Y, ldy, ws, lay, s);
+}
+
+tpdq_status tpdq_mlp_shard(const void* X, int64_t ldx, int32_t M, const int32_t* P1,
+                           const tpdq_w4* w1, const tpdq_w4* w2, tpdq_path path, tpdq_dtype dtype,
+                           void* Y1, void* Y2_partial, void* workspace, size_t ws_bytes,
+                           void* stream) {
+  tpdq_status st = check_common(M, path, dtype);
+  if (st != TPDQ_OK) return st;
+  const bool act = path == TPDQ_PATH_ACTORDER;
+  st = check_layer(w1, "w1", act, !act);
+  if (st != TPDQ_OK) return st;
+  st = check_layer(w2, "w2", act, !act);
+  if (st != TPDQ_OK) return st;
+  if (w2->K != w1->N) return fail(TPDQ_ERR_SHAPE, "w2->K=%d != w1->N=%d", w2->K, w1->N);
+  if (!X || !Y1 || !Y2_partial) return fail(TPDQ_ERR_NULL, "X, Y1 and Y2_partial are required");
+  if (act && P1) return fail(TPDQ_ERR_SHAPE, "the act-order path takes no P1");
+  if (!act && !P1) return fail(TPDQ_ERR_NULL, "the ordered path needs P1");
+  if (ldx < w1->K) return fail(TPDQ_ERR_SHAPE, "ldx=%lld < K1=%d", (long long)ldx, w1->K);
+  if (act) {
+    if (!aligned(X, 16) || ldx % 8)
+      return fail(TPDQ_ERR_ALIGN, "X needs 16-byte alignment and ldx %% 8 == 0");
+  } else if (!aligned(X, 2)) {
+    return fail(TPDQ_ERR_ALIGN, "X needs 2-byte alignment");
+  }
+  if (!aligned(Y1, 16) || !aligned(Y2_partial, 8))
+    return fail(TPDQ_ERR_ALIGN, "Y1 needs 16-byte and Y2_partial 8-byte alignment");
+  const GemmWs lay = gemm_ws(M, w1, w2, !act, w1->K);
+  if (!workspace || ws_bytes < lay.total)
+    return fail(TPDQ_ERR_WORKSPACE, "MLP needs %zu workspace bytes, got %zu", lay.total, ws_bytes);
+  if (!aligned(workspace, 16)) return fail(TPDQ_ERR_ALIGN, "workspace needs 16-byte alignment");
+
+  hipStream_t s = (hipStream_t)stream;
+  char* ws = (char*)workspace;
+  const uint16_t* Xin = (const uint16_t*)X;
+  int64_t ldin = ldx;
+  if (!act) {
+    uint16_t* Xp = (uint16_t*)(ws + lay.xperm);
+    hipError_t e = launch_gather_cols(Xin, ldx, M, w1->K, P1, Xp, s);
+    if (e != hipSuccess) return hip_fail(e, "activation gather launch");
+    Xin = Xp;
+    ldin = w1->K;
+  }
+  st = run_gemm(Xin, ldin, M, w1, path, (uint16_t*)Y1, w1->N, ws, lay, s);
+  if (st != TPDQ_OK) return st;
+  return run_gemm((const uint16_t*)Y1, w1->N, M, w2, path, (uint16_t*)Y2_partial, w2->N, ws, lay, s);
+}
+
+}  // extern "C"

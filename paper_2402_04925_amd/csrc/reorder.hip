@@ -1,0 +1,185 @@
+// Offline reorder on gfx950: Alg. 1 (P = argsort(g_idx), g_opt = g_idx[P])
+// and the permutations of the packed weights and their metadata (section 2.2:
+// W1[P1, P2], W2[P2]).
+//
+// The sort exploits what the method guarantees and the host validates first:
+// every group holds exactly G rows, so the sorted position of row i is
+//   g_idx[i] * G + #{ j < i : g_idx[j] == g_idx[i] }
+// (ascending groups, ties by ascending row: the stable order). One workgroup
+// per group sweeps g_idx in row order and ranks the group's members with
+// wave ballots, so the result does not depend on scheduling.
+#include "tpdq_internal.h"
+
+namespace tpdq {
+namespace {
+
+__global__ void k_fill_u32(uint32_t* p, size_t n, uint32_t v) {
+  for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
+       i += (size_t)gridDim.x * blockDim.x)
+    p[i] = v;
+}
+
+// flag bit 0: a g_idx value out of [0, num_groups); bit 1: a group whose
+// count differs from G (set by k_check_counts).
+__global__ void k_count_groups(const int32_t* __restrict__ g_idx, int K, int num_groups,
+                               uint32_t* __restrict__ counts, uint32_t* __restrict__ flag) {
+  for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < K; i += gridDim.x * blockDim.x) {
+    const uint32_t g = (uint32_t)g_idx[i];
+    if (g >= (uint32_t)num_groups)
+      atomicOr(flag, 1u);
+    else
+      atomicAdd(counts + g, 1u);
+  }
+}
+
+__global__ void k_check_counts(const uint32_t* __restrict__ counts, int num_groups, int G,
+                               uint32_t* __restrict__ flag) {
+  for (int g = blockIdx.x * blockDim.x + threadIdx.x; g < num_groups; g += gridDim.x * blockDim.x)
+    if (counts[g] != (uint32_t)G) atomicOr(flag, 2u);
+}
+
+// One workgroup (256 threads = 4 waves) per group g.
+__global__ __launch_bounds__(256) void k_rank_group(const int32_t* __restrict__ g_idx, int K, int G,
+                                                    int32_t* __restrict__ P,
+                                                    int32_t* __restrict__ g_sorted) {
+  __shared__ int wave_count[4];
+  const int g = blockIdx.x;
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  int base = 0;  // members of group g already placed (rows before this chunk)
+  for (int c0 = 0; c0 < K; c0 += 256) {
+    const int i = c0 + threadIdx.x;
+    const bool hit = i < K && g_idx[i] == g;
+    const unsigned long long m = __ballot(hit);
+    const int below = __popcll(m & ((1ull << lane) - 1ull));
+    if (lane == 0) wave_count[wave] = __popcll(m);
+    __syncthreads();
+    int before = base;
+    for (int w = 0; w < wave; ++w) before += wave_count[w];
+    const int total = wave_count[0] + wave_count[1] + wave_count[2] + wave_count[3];
+    __syncthreads();
+    if (hit) {
+      const int r = before + below;
+      if (r < G) {
+        P[(int64_t)g * G + r] = i;
+        g_sorted[(int64_t)g * G + r] = g;
+      }
+    }
+    base += total;
+  }
+}
+
+// dst[r][c] (packed rows) = src rows P_row[8r..8r+7] of column P_col[c]:
+// nibble t of dst word [r][c] = nibble (i & 7) of src word [i >> 3][cs],
+// i = P_row[8r + t], cs = P_col ? P_col[c] : c.
+__global__ void k_permute_qweight(const uint32_t* __restrict__ src, int64_t ld_src, int K, int N,
+                                  const int32_t* __restrict__ Prow, const int32_t* __restrict__ Pcol,
+                                  uint32_t* __restrict__ dst) {
+  const int64_t words = (int64_t)(K / 8) * N;
+  const uint32_t kmax = (uint32_t)(K - 1), nmax = (uint32_t)(N - 1);
+  for (int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; idx < words;
+       idx += (int64_t)gridDim.x * blockDim.x) {
+    const int r = (int)(idx / N);
+    const int c = (int)(idx - (int64_t)r * N);
+    const uint32_t cs = Pcol ? min((uint32_t)Pcol[c], nmax) : (uint32_t)c;
+    uint32_t out = 0;
+#pragma unroll
+    for (int t = 0; t < 8; ++t) {
+      const uint32_t i = min((uint32_t)Prow[8 * r + t], kmax);
+      const uint32_t w = src[(int64_t)(i >> 3) * ld_src + cs];
+      out |= ((w >> (4 * (i & 7))) & 0xFu) << (4 * t);
+    }
+    dst[idx] = out;
+  }
+}
+
+// dst[g][c] = src[g][P_col[c]] (2-byte elements; fp16 or bf16 bits).
+__global__ void k_permute_scales(const uint16_t* __restrict__ src, int64_t ld_src, int ng, int N,
+                                 const int32_t* __restrict__ Pcol, uint16_t* __restrict__ dst) {
+  const int64_t total = (int64_t)ng * N;
+  const uint32_t nmax = (uint32_t)(N - 1);
+  for (int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; idx < total;
+       idx += (int64_t)gridDim.x * blockDim.x) {
+    const int g = (int)(idx / N);
+    const int c = (int)(idx - (int64_t)g * N);
+    const uint32_t cs = Pcol ? min((uint32_t)Pcol[c], nmax) : (uint32_t)c;
+    dst[idx] = src[(int64_t)g * ld_src + cs];
+  }
+}
+
+// Zero codes packed along N: nibble t of dst word [g][cw] = zero of column
+// P_col[8 cw + t] of group g.
+__global__ void k_permute_qzeros(const uint32_t* __restrict__ src, int64_t ld_src, int ng, int N,
+                                 const int32_t* __restrict__ Pcol, uint32_t* __restrict__ dst) {
+  const int nw = N / 8;
+  const int64_t total = (int64_t)ng * nw;
+  const uint32_t nmax = (uint32_t)(N - 1);
+  for (int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; idx < total;
+       idx += (int64_t)gridDim.x * blockDim.x) {
+    const int g = (int)(idx / nw);
+    const int cw = (int)(idx - (int64_t)g * nw);
+    uint32_t out = 0;
+#pragma unroll
+    for (int t = 0; t < 8; ++t) {
+      const uint32_t c = Pcol ? min((uint32_t)Pcol[8 * cw + t], nmax) : (uint32_t)(8 * cw + t);
+      const uint32_t w = src[(int64_t)g * ld_src + (c >> 3)];
+      out |= ((w >> (4 * (c & 7))) & 0xFu) << (4 * t);
+    }
+    dst[idx] = out;
+  }
+}
+
+int grid_for(int64_t n) {
+  int64_t b = (n + 255) / 256;
+  if (b > 8192) b = 8192;
+  if (b < 1) b = 1;
+  return (int)b;
+}
+
+}  // namespace
+
+hipError_t launch_fill_u32(uint32_t* p, size_t n, uint32_t v, hipStream_t s) {
+  hipLaunchKernelGGL(k_fill_u32, dim3(grid_for((int64_t)n)), dim3(256), 0, s, p, n, v);
+  return hipGetLastError();
+}
+
+hipError_t launch_gidx_validate(const ReorderLayer& L, uint32_t* counts, uint32_t* flag,
+                                hipStream_t s) {
+  hipLaunchKernelGGL(k_count_groups, dim3(grid_for(L.K)), dim3(256), 0, s, L.g_idx, L.K,
+                     L.num_groups, counts, flag);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(k_check_counts, dim3(grid_for(L.num_groups)), dim3(256), 0, s, counts,
+                     L.num_groups, L.G, flag);
+  return hipGetLastError();
+}
+
+hipError_t launch_gidx_rank(const ReorderLayer& L, hipStream_t s) {
+  hipLaunchKernelGGL(k_rank_group, dim3(L.num_groups), dim3(256), 0, s, L.g_idx, L.K, L.G, L.P,
+                     L.g_sorted);
+  return hipGetLastError();
+}
+
+hipError_t launch_permute_qweight(const uint32_t* src, int64_t ld_src, int K, int N,
+                                  const int32_t* Prow, const int32_t* Pcol, uint32_t* dst,
+                                  hipStream_t s) {
+  hipLaunchKernelGGL(k_permute_qweight, dim3(grid_for((int64_t)(K / 8) * N)), dim3(256), 0, s, src,
+                     ld_src, K, N, Prow, Pcol, dst);
+  return hipGetLastError();
+}
+
+hipError_t launch_permute_scales(const uint16_t* src, int64_t ld_src, int ng, int N,
+                                 const int32_t* Pcol, uint16_t* dst, hipStream_t s) {
+  hipLaunchKernelGGL(k_permute_scales, dim3(grid_for((int64_t)ng * N)), dim3(256), 0, s, src,
+                     ld_src, ng, N, Pcol, dst);
+  return hipGetLastError();
+}
+
+hipError_t launch_permute_qzeros(const uint32_t* src, int64_t ld_src, int ng, int N,
+                                 const int32_t* Pcol, uint32_t* dst, hipStream_t s) {
+  hipLaunchKernelGGL(k_permute_qzeros, dim3(grid_for((int64_t)ng * (N / 8))), dim3(256), 0, s, src,
+                     ld_src, ng, N, Pcol, dst);
+  return hipGetLastError();
+}
+
+}  // namespace tpdq

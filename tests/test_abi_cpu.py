@@ -1,0 +1,136 @@
+"""Host-side checks of the C ABI: the library loads, exports every entry point
+the header declares, and rejects malformed calls before any device work.
+No call here reaches a kernel launch (no GPU is needed)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2402_04925_amd import _abi
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "tpdq.h")
+
+
+def declared_functions():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(tpdq_[a-z0-9_]+)\s*\(", src)))
+
+
+# The validation tests pass well-aligned but bogus device addresses; they must
+# never get near a GPU, where a validation bug would turn into a launch.
+NO_GPU = not os.path.exists("/dev/kfd")
+needs_no_gpu = pytest.mark.skipif(not NO_GPU, reason="fake device pointers only where no GPU exists")
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(_abi.LIB_PATH):
+        from paper_2402_04925_amd import build
+        build.build()
+    return _abi.lib()
+
+
+def test_exports_every_declared_symbol(lib):
+    names = declared_functions()
+    assert set(names) == set(_abi.EXPORTED), names
+    for n in names:
+        assert hasattr(lib, n), n
+
+
+def test_status_strings(lib):
+    for s in range(8):
+        assert lib.tpdq_status_string(s)
+    assert lib.tpdq_version().decode().count(".") == 2
+
+
+def fake_layer(K=256, N=128, G=32, ng=None, base=1 << 20, gidx=True):
+    # plausible, well-aligned but never dereferenced addresses
+    return _abi.W4(qweight=base, ld_q=N, scales=base + (1 << 16), ld_s=N,
+                   qzeros=base + (2 << 16), ld_z=N // 8, g_idx=(base + (3 << 16)) if gidx else None,
+                   K=K, N=N, group_size=G, num_groups=ng if ng is not None else K // G)
+
+
+def gemm(lib, w, M=4, X=1 << 24, ldx=None, Y=1 << 25, ldy=None, path=_abi.PATH_ORDERED, ws=None,
+         ws_bytes=0, dtype=_abi.FP16, perm=None):
+    return lib.tpdq_w4a16_gemm(X, ldx if ldx is not None else w.K, M, perm,
+                               ctypes.byref(w) if w is not None else None, path, dtype, Y,
+                               ldy if ldy is not None else w.N, ws, ws_bytes, None)
+
+
+@needs_no_gpu
+def test_gemm_validation(lib):
+    w = fake_layer()
+    assert gemm(lib, None, ldx=256, ldy=128) == _abi.ERR_NULL
+    assert gemm(lib, w, X=None) == _abi.ERR_NULL
+    assert gemm(lib, w, M=0) == _abi.ERR_SHAPE
+    assert gemm(lib, fake_layer(K=260), ldx=264) == _abi.ERR_SHAPE          # K % 8
+    assert gemm(lib, fake_layer(N=100), ldy=100) == _abi.ERR_SHAPE          # N % 8
+    assert gemm(lib, fake_layer(G=12)) == _abi.ERR_SHAPE                    # G % 8
+    assert gemm(lib, fake_layer(K=264, G=16, ng=17), ldx=264) == _abi.ERR_SHAPE  # sorted needs G | K
+    assert gemm(lib, w, ldx=128) == _abi.ERR_SHAPE                          # ldx < K
+    assert gemm(lib, w, X=(1 << 24) + 2) == _abi.ERR_ALIGN                  # X 16-B
+    assert gemm(lib, w, ldx=260) == _abi.ERR_ALIGN                          # ldx % 8
+    assert gemm(lib, w, Y=(1 << 25) + 4) == _abi.ERR_ALIGN                  # Y 8-B
+    bad = fake_layer()
+    bad.qweight += 4
+    assert gemm(lib, bad) == _abi.ERR_ALIGN
+    assert gemm(lib, w, path=_abi.PATH_ACTORDER, ws=None) == _abi.ERR_WORKSPACE
+    nog = fake_layer(gidx=False)
+    assert gemm(lib, nog, path=_abi.PATH_ACTORDER) == _abi.ERR_NULL          # act-order needs g_idx
+    assert gemm(lib, w, dtype=_abi.BF16) == _abi.ERR_UNSUPPORTED
+    assert gemm(lib, w, path=7) == _abi.ERR_SHAPE
+    need = lib.tpdq_workspace_bytes(_abi.OP_GEMM, 4, ctypes.byref(w), None)
+    assert need > 0
+    # the query covers the gathered-activation buffer, so ask with a gather
+    assert gemm(lib, w, perm=1 << 27, ws=1 << 26, ws_bytes=need - 1) == _abi.ERR_WORKSPACE
+    assert b"workspace" in lib.tpdq_last_error()
+
+
+@needs_no_gpu
+def test_mlp_validation(lib):
+    w1 = fake_layer(K=256, N=512)
+    w2 = fake_layer(K=512, N=128, base=1 << 22)
+    w2bad = fake_layer(K=256, N=128, base=1 << 22)
+    f = lambda a, b, P1=1 << 27, path=_abi.PATH_ORDERED, ws=None, nb=0: lib.tpdq_mlp_shard(
+        1 << 24, 256, 4, P1, ctypes.byref(a), ctypes.byref(b), path, _abi.FP16, 1 << 25, 1 << 26,
+        ws, nb, None)
+    assert f(w1, w2bad) == _abi.ERR_SHAPE                                    # K2 != N1
+    assert f(w1, w2, P1=None) == _abi.ERR_NULL                                # ordered needs P1
+    assert f(w1, w2, path=_abi.PATH_ACTORDER) == _abi.ERR_SHAPE               # act-order takes no P1
+    assert f(w1, w2) == _abi.ERR_WORKSPACE
+
+
+@needs_no_gpu
+def test_reorder_validation(lib):
+    w1 = fake_layer(K=256, N=512)
+    w2 = fake_layer(K=512, N=128, base=1 << 22)
+    p = 1 << 27
+    args = lambda a, b, P2=None, ws=None, nb=0: (
+        ctypes.byref(a), ctypes.byref(b) if b is not None else None, p, p, P2, P2 and p, p, p, p,
+        P2 and p, _abi.FP16, ws, nb, None)
+    assert lib.tpdq_reorder(*args(w1, None, P2=p)) == _abi.ERR_SHAPE         # P2 without w2
+    assert lib.tpdq_reorder(*args(w1, w2)) == _abi.ERR_NULL                   # w2 without P2
+    nog = fake_layer(K=256, N=512, gidx=False)
+    assert lib.tpdq_reorder(*args(nog, None)) == _abi.ERR_NULL
+    shard = fake_layer(K=256, N=512, ng=64)
+    assert lib.tpdq_reorder(*args(shard, None)) == _abi.ERR_SHAPE            # not a global layer
+    assert lib.tpdq_reorder(*args(w1, w2, P2=p)) == _abi.ERR_WORKSPACE
+
+
+def test_workspace_sizes(lib):
+    w1 = fake_layer(K=8192, N=3584, G=128)
+    w2 = fake_layer(K=3584, N=8192, G=128, base=1 << 22)
+    for M in (1, 4, 16, 64, 2048):
+        g = lib.tpdq_workspace_bytes(_abi.OP_GEMM, M, ctypes.byref(w1), None)
+        m = lib.tpdq_workspace_bytes(_abi.OP_MLP, M, ctypes.byref(w1), ctypes.byref(w2))
+        assert g > 0 and m >= g
+        assert m % 256 == 0
+        # the gathered activations must fit
+        assert m >= M * 8192 * 2
+    r = lib.tpdq_workspace_bytes(_abi.OP_REORDER, 0, ctypes.byref(w1), ctypes.byref(w2))
+    assert r >= 4 * (64 + 28)
+    assert lib.tpdq_workspace_bytes(_abi.OP_MLP, 4, ctypes.byref(w1), None) == 0
+    assert lib.tpdq_workspace_bytes(_abi.OP_GEMM, 0, ctypes.byref(w1), None) == 0

@@ -1,0 +1,161 @@
+"""GPU W4A16 GEMM (act-order and ordered paths) against the oracle."""
+import numpy as np
+import pytest
+
+from oracle import tpdq_oracle as o
+from paper_2402_04925_amd import inputs
+from tests.gpu_util import (TOL_FP16, layer_to_dev, log, np_of, sample_cols, to_dev, torch_dev,
+                            workload_layers)
+
+pytestmark = pytest.mark.gpu
+
+SHAPES = [  # K, N, G: config-0 size, ragged N and K, several tiles, small G (row-metadata kernel)
+    (256, 128, 32), (288, 200, 32), (1024, 520, 128), (128, 72, 8), (192, 64, 64), (40, 24, 8),
+    (2048, 1032, 128),
+]
+MS = [1, 4, 16, 17, 64, 65]
+
+
+def _d(layer):
+    return dict(qweight=layer.qweight, scales=layer.scales, qzeros=layer.qzeros)
+
+
+@pytest.mark.parametrize("K,N,G", SHAPES)
+@pytest.mark.parametrize("M", MS)
+def test_gemm_actorder(K, N, G, M):
+    import torch
+    import paper_2402_04925_amd as tpdq
+    dev = torch_dev()
+    log(f"gemm actorder K={K} N={N} G={G} M={M}")
+    w1, _ = inputs.make_custom(K, N, 0, G, seed=K + N + G)
+    X = inputs.random_activations(M, K, np.random.default_rng(M))
+    Y = tpdq.w4a16_gemm(to_dev(X, dev), layer_to_dev(w1, dev), tpdq.PATH_ACTORDER)
+    torch.cuda.synchronize()
+    ref = o.w4a16_gemm(X, w1.qweight, w1.scales, w1.qzeros, w1.g_idx)
+    assert o.rel_err(np_of(Y), ref) <= TOL_FP16
+
+
+@pytest.mark.parametrize("K,N,G", SHAPES)
+@pytest.mark.parametrize("M", MS)
+def test_gemm_ordered(K, N, G, M):
+    """Sorted rows from the GPU reorder, the activation gather X[:, P] in the
+    call; equal to the act-order product by the reorder invariant."""
+    import torch
+    import paper_2402_04925_amd as tpdq
+    dev = torch_dev()
+    log(f"gemm ordered K={K} N={N} G={G} M={M}")
+    w1, _ = inputs.make_custom(K, N, 0, G, seed=K + N + G)
+    X = inputs.random_activations(M, K, np.random.default_rng(M))
+    P, gs, _, _, wo, _ = tpdq.reorder(layer_to_dev(w1, dev))
+    Xd = to_dev(X, dev)
+    Y = tpdq.w4a16_gemm(Xd, wo, tpdq.PATH_ORDERED, x_perm=P)
+    torch.cuda.synchronize()
+    ref = o.w4a16_gemm(X, w1.qweight, w1.scales, w1.qzeros, w1.g_idx)
+    assert o.rel_err(np_of(Y), ref) <= TOL_FP16
+    # without the gather: X multiplies the sorted rows directly
+    Y2 = tpdq.w4a16_gemm(Xd, wo, tpdq.PATH_ORDERED)
+    torch.cuda.synchronize()
+    eP, eg = o.reorder(w1.g_idx)
+    ws = o.permute_rows(_d(w1), eP)
+    ref2 = o.w4a16_gemm(X, ws["qweight"], ws["scales"], ws["qzeros"], eg)
+    assert o.rel_err(np_of(Y2), ref2) <= TOL_FP16
+
+
+def test_gemm_deterministic():
+    import torch
+    import paper_2402_04925_amd as tpdq
+    dev = torch_dev()
+    w1, _ = inputs.make_custom(4096, 1024, 0, 128, seed=3)
+    X = to_dev(inputs.random_activations(16, 4096, np.random.default_rng(3)), dev)
+    dw = layer_to_dev(w1, dev)
+    P, _, _, _, wo, _ = tpdq.reorder(dw)
+    for path, w, perm in ((tpdq.PATH_ACTORDER, dw, None), (tpdq.PATH_ORDERED, wo, P)):
+        a = tpdq.w4a16_gemm(X, w, path, x_perm=perm).clone()
+        b = tpdq.w4a16_gemm(X, w, path, x_perm=perm).clone()
+        torch.cuda.synchronize()
+        assert torch.equal(a.view(torch.int16), b.view(torch.int16))
+
+
+def test_gemm_zero_codes_special_case():
+    """q == z everywhere -> Y == 0 exactly; G = K (one group)."""
+    import torch
+    import paper_2402_04925_amd as tpdq
+    dev = torch_dev()
+    K, N = 256, 64
+    z = np.random.default_rng(1).integers(0, 16, size=(1, N))
+    qz = o.pack_cols(z)
+    qw = o.pack_rows(np.repeat(z, K, axis=0))
+    s = inputs.random_scales((1, N), np.random.default_rng(2))
+    g = np.zeros(K, dtype=np.int32)
+    w = tpdq.QuantWeight.from_tensors(to_dev(qw, dev), to_dev(s, dev), to_dev(qz, dev), to_dev(g, dev), K)
+    X = to_dev(inputs.random_activations(4, K, np.random.default_rng(3)), dev)
+    for path in (tpdq.PATH_ACTORDER, tpdq.PATH_ORDERED):
+        Y = tpdq.w4a16_gemm(X, w, path)
+        torch.cuda.synchronize()
+        assert np.all(np_of(Y) == 0)
+
+
+def test_gemm_clamps_out_of_range_gidx():
+    """Act-order g_idx values outside [0, num_groups) are clamped in the kernel
+    (no fault); the result equals the oracle with the clamped g_idx."""
+    import torch
+    import paper_2402_04925_amd as tpdq
+    dev = torch_dev()
+    w1, _ = inputs.make_custom(256, 64, 0, 32, seed=5)
+    g = w1.g_idx.copy()
+    g[3], g[100] = 1000, -7
+    w1.g_idx = g
+    X = inputs.random_activations(4, 256, np.random.default_rng(5))
+    Y = tpdq.w4a16_gemm(to_dev(X, dev), layer_to_dev(w1, dev), tpdq.PATH_ACTORDER)
+    torch.cuda.synchronize()
+    gc = np.where(g < 0, 7, g).clip(0, 7)
+    ref = o.w4a16_gemm(X, w1.qweight, w1.scales, w1.qzeros, gc)
+    assert o.rel_err(np_of(Y), ref) <= TOL_FP16
+
+
+@pytest.mark.parametrize("name,which,M", [
+    ("llama70b_tp8", 1, 1), ("llama70b_tp8", 1, 16), ("llama70b_tp8", 2, 4), ("llama70b_tp8", 2, 64),
+    ("granite20b_tp4", 1, 8), ("granite20b_tp4", 2, 16), ("llama70b_tp1", 1, 16), ("llama70b_tp1", 2, 1),
+])
+def test_gemm_full_size_shards(name, which, M):
+    """Rank 0's shard of the global layer at the paper's sizes (act-order:
+    W2's row shard keeps global g_idx values and all metadata), both paths,
+    on sampled output columns."""
+    import torch
+    import paper_2402_04925_amd as tpdq
+    dev = torch_dev()
+    w = inputs.WORKLOADS[name]
+    log(f"gemm full {name} W{which} M={M}")
+    w1, w2 = workload_layers(name)
+    L = w1 if which == 1 else w2
+    K = L.K // (1 if which == 1 else w.tp)
+    X = inputs.random_activations(M, K, np.random.default_rng(M))
+    Xd = to_dev(X, dev)
+    dl = layer_to_dev(L, dev)
+    rng = np.random.default_rng(1)
+    if which == 1:
+        sh = dl.column_shard(0, w.tp)
+        ncols = L.N // w.tp
+        cols = sample_cols(ncols, rng)
+        ref = o.w4a16_gemm(X, L.qweight, L.scales, L.qzeros, L.g_idx, cols=cols)
+    else:
+        sh = dl.row_shard(0, w.tp, sorted_rows=False)
+        cols = sample_cols(L.N, rng)
+        ref = o.w4a16_gemm(X, L.qweight[:K // 8], L.scales, L.qzeros, L.g_idx[:K], cols=cols)
+    Y = tpdq.w4a16_gemm(Xd, sh, tpdq.PATH_ACTORDER)
+    torch.cuda.synchronize()
+    assert o.rel_err(np_of(Y)[:, cols], ref) <= TOL_FP16
+    # ordered: the reordered global layer, same shard position
+    P, gs, _, _, wo, _ = tpdq.reorder(dl)
+    eP, eg = o.reorder(L.g_idx)
+    if which == 1:
+        sho = wo.column_shard(0, w.tp)
+        Yo = tpdq.w4a16_gemm(Xd, sho, tpdq.PATH_ORDERED, x_perm=P)
+        refo = ref   # X[:, P] @ W[P] has the same terms as X @ W
+    else:
+        sho = wo.row_shard(0, w.tp, sorted_rows=True)
+        Yo = tpdq.w4a16_gemm(Xd, sho, tpdq.PATH_ORDERED)
+        Wd = o.dequant(L.qweight, L.scales, L.qzeros, L.g_idx, cols=cols)[eP[:K]]
+        refo = o.to_fp16(o.matmul(X, Wd))
+    torch.cuda.synchronize()
+    assert o.rel_err(np_of(Yo)[:, cols], refo) <= TOL_FP16

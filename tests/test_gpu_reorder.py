@@ -1,0 +1,120 @@
+"""GPU reorder (Alg. 1 and the TP-aware fold) against the oracle: bit-exact
+permutations, sorted g_idx and every packed code."""
+import numpy as np
+import pytest
+
+from oracle import tpdq_oracle as o
+from paper_2402_04925_amd import inputs
+from tests.gpu_util import layer_to_dev, log, np_of, torch_dev
+
+pytestmark = pytest.mark.gpu
+
+
+def _d(layer):
+    return dict(qweight=layer.qweight, scales=layer.scales, qzeros=layer.qzeros)
+
+
+@pytest.mark.parametrize("K1,N1,N2,G,seed", [
+    (256, 512, 128, 32, 1), (64, 128, 64, 8, 2), (512, 256, 200, 64, 3), (384, 640, 72, 128, 4),
+    (256, 256, 128, 256, 5),
+])
+def test_reorder_pair_exact(K1, N1, N2, G, seed):
+    import torch
+    import paper_2402_04925_amd as tpdq
+    dev = torch_dev()
+    log(f"reorder pair K1={K1} N1={N1} N2={N2} G={G}")
+    w1, w2 = inputs.make_custom(K1, N1, N2, G, seed)
+    P1, g1, P2, g2, w1o, w2o = tpdq.reorder(layer_to_dev(w1, dev), layer_to_dev(w2, dev))
+    torch.cuda.synchronize()
+    eP1, eg1 = o.reorder(w1.g_idx)
+    eP2, eg2 = o.reorder(w2.g_idx)
+    f1, f2 = o.fold(_d(w1), _d(w2), eP1, eP2)
+    assert np.array_equal(np_of(P1), eP1) and np.array_equal(np_of(g1), eg1)
+    assert np.array_equal(np_of(P2), eP2) and np.array_equal(np_of(g2), eg2)
+    assert np.array_equal(np_of(w1o.qweight), f1["qweight"])
+    assert np.array_equal(np_of(w1o.scales), f1["scales"])
+    assert np.array_equal(np_of(w1o.qzeros), f1["qzeros"])
+    assert np.array_equal(np_of(w2o.qweight), f2["qweight"])
+
+
+@pytest.mark.parametrize("K,N,G,seed", [(256, 128, 32, 7), (1024, 96, 128, 8), (40, 16, 8, 9)])
+def test_reorder_single_exact(K, N, G, seed):
+    import torch
+    import paper_2402_04925_amd as tpdq
+    dev = torch_dev()
+    log(f"reorder single K={K} N={N} G={G}")
+    w1, _ = inputs.make_custom(K, N, 0, G, seed)
+    P1, g1, P2, g2, w1o, w2o = tpdq.reorder(layer_to_dev(w1, dev))
+    torch.cuda.synchronize()
+    assert P2 is None and w2o is None
+    eP, eg = o.reorder(w1.g_idx)
+    e = o.permute_rows(_d(w1), eP)
+    assert np.array_equal(np_of(P1), eP) and np.array_equal(np_of(g1), eg)
+    assert np.array_equal(np_of(w1o.qweight), e["qweight"])
+    assert np.array_equal(np_of(w1o.scales), w1.scales)
+    assert np.array_equal(np_of(w1o.qzeros), w1.qzeros)
+
+
+def test_reorder_identity_phi():
+    """phi = identity: P = identity and the weights come back unchanged."""
+    import torch
+    import paper_2402_04925_amd as tpdq
+    dev = torch_dev()
+    w1, w2 = inputs.make_custom(256, 256, 64, 32, 11, identity_phi=True)
+    P1, g1, P2, g2, w1o, w2o = tpdq.reorder(layer_to_dev(w1, dev), layer_to_dev(w2, dev))
+    torch.cuda.synchronize()
+    assert np.array_equal(np_of(P1), np.arange(256)) and np.array_equal(np_of(P2), np.arange(256))
+    assert np.array_equal(np_of(w1o.qweight), w1.qweight)
+    assert np.array_equal(np_of(w2o.qweight), w2.qweight)
+
+
+@pytest.mark.parametrize("kind", ["count", "range", "negative"])
+def test_reorder_rejects_bad_gidx(kind):
+    import paper_2402_04925_amd as tpdq
+    dev = torch_dev()
+    w1, _ = inputs.make_custom(128, 64, 0, 32, 12)
+    g = w1.g_idx.copy()
+    if kind == "count":
+        g[np.flatnonzero(g == 0)[0]] = 1     # group 0 short, group 1 long
+    elif kind == "range":
+        g[5] = 4
+    else:
+        g[5] = -3
+    w1.g_idx = g
+    with pytest.raises(tpdq.TpdqError) as ei:
+        tpdq.reorder(layer_to_dev(w1, dev))
+    assert ei.value.status == 4
+
+
+@pytest.mark.parametrize("name", ["granite20b_tp4", "llama70b_tp8"])
+def test_reorder_full_size(name):
+    """Global layers of the paper's MLP problem sizes: P and g_idx compared in
+    full, packed codes and metadata on sampled rows and columns."""
+    import torch
+    import paper_2402_04925_amd as tpdq
+    dev = torch_dev()
+    w = inputs.WORKLOADS[name]
+    log(f"reorder full {name}")
+    w1, w2 = inputs.make_workload(w)
+    P1, g1, P2, g2, w1o, w2o = tpdq.reorder(layer_to_dev(w1, dev), layer_to_dev(w2, dev))
+    torch.cuda.synchronize()
+    eP1, eg1 = o.reorder(w1.g_idx)
+    eP2, eg2 = o.reorder(w2.g_idx)
+    assert np.array_equal(np_of(P1), eP1) and np.array_equal(np_of(g1), eg1)
+    assert np.array_equal(np_of(P2), eP2) and np.array_equal(np_of(g2), eg2)
+    rng = np.random.default_rng(0)
+    rows1 = np.unique(np.concatenate([np.arange(16), w.K1 - 1 - np.arange(16), rng.choice(w.K1, 64)]))
+    cols1 = np.unique(np.concatenate([np.arange(16), w.N1 - 1 - np.arange(16), rng.choice(w.N1, 64)]))
+    got1 = o.unpack_rows(np_of(w1o.qweight[torch.from_numpy(np.unique(rows1 // 8)).to(dev)]))
+    rows_w = np.unique(rows1 // 8)
+    exp1 = o.fold_sample(w1.qweight, eP1, eP2, np.concatenate([8 * r + np.arange(8) for r in rows_w]), cols1)
+    assert np.array_equal(got1[:, cols1], exp1)
+    es1, ez1 = o.fold_meta(w1.scales, w1.qzeros, eP2)
+    assert np.array_equal(np_of(w1o.scales), es1)
+    assert np.array_equal(np_of(w1o.qzeros), ez1)
+    rows2 = np.unique(np.concatenate([np.arange(16), w.K2 - 1 - np.arange(16), rng.choice(w.K2, 64)]))
+    rows_w2 = np.unique(rows2 // 8)
+    got2 = o.unpack_rows(np_of(w2o.qweight[torch.from_numpy(rows_w2).to(dev)]))
+    cols2 = np.arange(w.N2)
+    exp2 = o.fold_sample(w2.qweight, eP2, None, np.concatenate([8 * r + np.arange(8) for r in rows_w2]), cols2)
+    assert np.array_equal(got2, exp2)
