@@ -120,16 +120,17 @@ class Setup:
         def dense(q, with_g):
             return tpdq.QuantWeight(q.qweight.contiguous(), q.scales.contiguous(), q.qzeros.contiguous(),
                                     q.g_idx.contiguous() if with_g and q.g_idx is not None else None,
-                                    q.K, q.N, q.G, q.num_groups)
+                                    q.K, q.N, q.G, q.num_groups, q.layout)
 
-        base = [dense(ord1, False), dense(ord2, False), dense(act1, True), dense(act2, True)]
+        a1, a2 = dense(act1, True), dense(act2, True)
+        base = [dense(ord1, False), dense(ord2, False), a1, a2, tpdq.pack_tiled(a1), tpdq.pack_tiled(a2)]
         per = sum(t.qweight.numel() * 4 + t.scales.numel() * 2 + t.qzeros.numel() * 4 for t in base[:2])
         self.R = max(2, -(-min_bytes // per))
         self.reps = [base]
         for _ in range(self.R - 1):
             self.reps.append([tpdq.QuantWeight(q.qweight.clone(), q.scales.clone(), q.qzeros.clone(),
                                                q.g_idx.clone() if q.g_idx is not None else None,
-                                               q.K, q.N, q.G, q.num_groups) for q in base])
+                                               q.K, q.N, q.G, q.num_groups, q.layout) for q in base])
         torch.cuda.synchronize()
         del d1, d2, w1o, w2o
         eprint(f"[bench] {self.R} weight replicas of {per / 1e6:.1f} MB (ordered pair)")
@@ -235,8 +236,11 @@ def main():
         xg = X[:, st.P1.long()].contiguous()   # X[:, P1] for the single-GEMM timings
         ws = tpdq.Workspace(dev)
 
-        def mk_mlp(rep, path):
-            w1, w2 = (rep[0], rep[1]) if path == tpdq.PATH_ORDERED else (rep[2], rep[3])
+        PAIRS = {"ordered": (0, 1), "actorder": (2, 3), "actorder_global": (2, 3), "actorder_tiled": (4, 5)}
+
+        def mk_mlp(rep, pname, path):
+            i1, i2 = PAIRS[pname]
+            w1, w2 = rep[i1], rep[i2]
             c1, c2 = w1.c_struct(), w2.c_struct()
             nb = lib.tpdq_workspace_bytes(tpdq.OP_MLP, M, ctypes.byref(c1), ctypes.byref(c2))
             buf = ws.get(nb)
@@ -250,8 +254,8 @@ def main():
                     torch.cuda.current_stream(dev).cuda_stream))
             return call
 
-        def mk_gemm(rep, which, path):
-            w = rep[which] if path == tpdq.PATH_ORDERED else rep[2 + which]
+        def mk_gemm(rep, which, pname, path):
+            w = rep[PAIRS[pname][which]]
             c = w.c_struct()
             nb = lib.tpdq_workspace_bytes(tpdq.OP_GEMM, M, ctypes.byref(c), None)
             buf = ws.get(nb)
@@ -266,10 +270,15 @@ def main():
             return call
 
         r = {}
-        for pname, path in (("ordered", tpdq.PATH_ORDERED), ("actorder", tpdq.PATH_ACTORDER)):
-            ms, _ = capture_and_time([mk_mlp(rep, path) for rep in st.reps], args.steps, args.warmup, dev)
-            g1, _ = capture_and_time([mk_gemm(rep, 0, path) for rep in st.reps], args.steps, args.warmup, dev)
-            g2, _ = capture_and_time([mk_gemm(rep, 1, path) for rep in st.reps], args.steps, args.warmup, dev)
+        for pname, path in (("ordered", tpdq.PATH_ORDERED), ("actorder", tpdq.PATH_ACTORDER),
+                            ("actorder_global", tpdq.PATH_ACTORDER_GLOBAL),
+                            ("actorder_tiled", tpdq.PATH_ACTORDER)):
+            ms, _ = capture_and_time([mk_mlp(rep, pname, path) for rep in st.reps], args.steps,
+                                     args.warmup, dev)
+            g1, _ = capture_and_time([mk_gemm(rep, 0, pname, path) for rep in st.reps], args.steps,
+                                     args.warmup, dev)
+            g2, _ = capture_and_time([mk_gemm(rep, 1, pname, path) for rep in st.reps], args.steps,
+                                     args.warmup, dev)
             r[pname] = dict(mlp_us=ms * 1e3, gemm1_us=g1 * 1e3, gemm2_us=g2 * 1e3)
             eprint(f"[bench] M={M} {pname}: mlp {ms*1e3:.2f} us, gemm1 {g1*1e3:.2f} us, gemm2 {g2*1e3:.2f} us")
         ng2_act = wl.K2 // wl.G
@@ -306,6 +315,14 @@ def main():
             ordered_mlp_us=round(rr["ordered"]["mlp_us"], 3),
             actorder_mlp_us=round(rr["actorder"]["mlp_us"], 3),
             speedup_ordered_vs_actorder=round(rr["actorder"]["mlp_us"] / rr["ordered"]["mlp_us"], 3),
+            actorder_global_mlp_us=round(rr["actorder_global"]["mlp_us"], 3),
+            speedup_ordered_vs_actorder_global=round(rr["actorder_global"]["mlp_us"] / rr["ordered"]["mlp_us"], 3),
+            actorder_global_gemm_us=[round(rr["actorder_global"]["gemm1_us"], 3),
+                                     round(rr["actorder_global"]["gemm2_us"], 3)],
+            actorder_tiled_mlp_us=round(rr["actorder_tiled"]["mlp_us"], 3),
+            speedup_ordered_vs_actorder_tiled=round(rr["actorder_tiled"]["mlp_us"] / rr["ordered"]["mlp_us"], 3),
+            actorder_tiled_gemm_us=[round(rr["actorder_tiled"]["gemm1_us"], 3),
+                                    round(rr["actorder_tiled"]["gemm2_us"], 3)],
             ordered_gemm_us=[round(rr["ordered"]["gemm1_us"], 3), round(rr["ordered"]["gemm2_us"], 3)],
             actorder_gemm_us=[round(rr["actorder"]["gemm1_us"], 3), round(rr["actorder"]["gemm2_us"], 3)],
             ordered_mlp_gbs=round(bb["mlp"] / (rr["ordered"]["mlp_us"] * 1e-6) / 1e9, 1),

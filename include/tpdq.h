@@ -60,20 +60,40 @@ typedef enum {
 
 typedef enum { TPDQ_FP16 = 0, TPDQ_BF16 = 1 } tpdq_dtype;
 
+/* Storage order of qweight.
+ * TPDQ_LAYOUT_GPTQ: int32 [K/8][ld_q], word [r][n] = rows 8r..8r+7 of column n.
+ * TPDQ_LAYOUT_TILED: the same words regrouped so that one wavefront of the
+ *   decode GEMM reads 1 KB contiguous per load: int32 [ceil(N/16)][ld_q] with
+ *   ld_q >= ceil(K/128)*256; for 16-column tile t, 128-row block b, lane
+ *   l = 16*kq + j (0 <= j < 16, 0 <= kq < 4) and step u (0 <= u < 4):
+ *     tiled[t][256*b + 4*l + u] = gptq[4*(4*b + u) + kq][16*t + j]
+ *   Words of rows at or beyond K (padding of the last block) are zero. A row
+ *   shard starting at a multiple of 128 rows is the view qweight + 256*(k0/128)
+ *   with the same ld_q; a column shard starting at a multiple of 16 columns is
+ *   qweight + ld_q*(c0/16). Produced by tpdq_reorder or tpdq_pack_tiled. */
+typedef enum { TPDQ_LAYOUT_GPTQ = 0, TPDQ_LAYOUT_TILED = 1 } tpdq_layout;
+
 typedef enum {
   /* Per-row metadata through g_idx (Eq. 3; the naive load of Fig. 1). The
-     scale and zero of row k are those of group g_idx[k]. */
+     scale and zero of row k are those of group g_idx[k]; every row looks its
+     metadata up separately and the weight is dequantized per element. The
+     metadata of a 16-column tile (all num_groups groups) is staged in LDS. */
   TPDQ_PATH_ACTORDER = 0,
   /* Rows sorted by group (Alg. 1; the optimized load of Fig. 2): the group of
      local row k is floor(k / G); g_idx is ignored and may be NULL. */
-  TPDQ_PATH_ORDERED = 1
+  TPDQ_PATH_ORDERED = 1,
+  /* As TPDQ_PATH_ACTORDER, but every row fetches its scale and zero from
+     global memory (Fig. 1 as drawn, no staging): the baseline for counting
+     redundant metadata fetches. */
+  TPDQ_PATH_ACTORDER_GLOBAL = 2
 } tpdq_path;
 
 /* One quantized layer, or a shard of one given as views (pointer offsets and
  * leading dimensions). K = input features (rows), N = output features.
  * num_groups is the number of metadata rows: K/G for a whole or sorted layer;
  * an act-order row-parallel shard keeps the global metadata and global g_idx
- * values, so there num_groups = K_global/G exceeds K/G.
+ * values, so there num_groups = K_global/G exceeds K/G. layout is a
+ * tpdq_layout (scales, qzeros and g_idx are always as described above).
  * Alignment: qweight 16 B and ld_q % 4 == 0; scales 8 B and ld_s % 4 == 0;
  * qzeros 4 B; g_idx 16 B. */
 typedef struct tpdq_w4 {
@@ -88,6 +108,7 @@ typedef struct tpdq_w4 {
   int32_t N;
   int32_t group_size;  /* G, a multiple of 8 */
   int32_t num_groups;
+  int32_t layout;      /* tpdq_layout of qweight */
 } tpdq_w4;
 
 /*
@@ -107,9 +128,10 @@ typedef struct tpdq_w4 {
  *
  * Requirements: every g_idx value in [0, K/G) and every group holding exactly
  * G rows (what Eq. 3 gives for a permutation phi with G | K); K%G == 0,
- * G%8 == 0, N%8 == 0. Outputs are dense: qweight1_out int32 [K1/8][N1],
- * scales1_out [K1/G][N1] (the dtype of w1->scales), qzeros1_out int32
- * [K1/G][N1/8], qweight2_out int32 [K2/8][N2], P and g_sorted int32 [K].
+ * G%8 == 0, N%8 == 0; both inputs in TPDQ_LAYOUT_GPTQ. Outputs are dense:
+ * qweight1_out and qweight2_out in out_layout (GPTQ: int32 [K/8][N]; TILED:
+ * int32 [ceil(N/16)][ceil(K/128)*256]), scales1_out [K1/G][N1] (the dtype of
+ * w1->scales), qzeros1_out int32 [K1/G][N1/8], P and g_sorted int32 [K].
  * P2, g2_sorted and qweight2_out must be NULL when w2 is NULL.
  *
  * Workspace: at least tpdq_workspace_bytes(0, 0, w1, w2) bytes, any content.
@@ -121,8 +143,18 @@ typedef struct tpdq_w4 {
 tpdq_status tpdq_reorder(const tpdq_w4* w1, const tpdq_w4* w2,
                          int32_t* P1, int32_t* g1_sorted, int32_t* P2, int32_t* g2_sorted,
                          int32_t* qweight1_out, void* scales1_out, int32_t* qzeros1_out,
-                         int32_t* qweight2_out, tpdq_dtype dtype,
+                         int32_t* qweight2_out, tpdq_dtype dtype, tpdq_layout out_layout,
                          void* workspace, size_t ws_bytes, void* stream);
+
+/*
+ * tpdq_pack_tiled - copy w->qweight (TPDQ_LAYOUT_GPTQ, K x N) into
+ * TPDQ_LAYOUT_TILED with ld_q = ceil(K/128)*256: out is int32
+ * [ceil(N/16)][ceil(K/128)*256], device, caller-owned. Offline; asynchronous
+ * on `stream`. Used to give act-order weights the same storage order as the
+ * reordered ones, so that the two GEMM paths differ only in their metadata
+ * access (section 2.1, Fig. 1 vs Fig. 2).
+ */
+tpdq_status tpdq_pack_tiled(const tpdq_w4* w, int32_t* qweight_out, void* stream);
 
 /*
  * tpdq_w4a16_gemm - Y = X' @ deq(W), fp32 accumulation, result rounded to
@@ -130,16 +162,17 @@ tpdq_status tpdq_reorder(const tpdq_w4* w1, const tpdq_w4* w2,
  *
  * X  [M][ldx] activations (K columns used); X' = X, or X[:, x_perm] when
  *    x_perm (int32 [K], device) is given: column j of X' is column x_perm[j]
- *    of X (the X[:, P1] gather of Alg. 2 and Alg. 3). Alignment 16 B and
- *    ldx % 8 == 0 when x_perm is NULL; 2 B otherwise.
- * w  the layer; path selects the metadata load (see tpdq_path).
- *    TPDQ_PATH_ACTORDER needs w->g_idx; values outside [0, num_groups) are
+ *    of X (the X[:, P1] gather of Alg. 2 and Alg. 3); x_perm values outside
+ *    [0, K) are clamped. Alignment 16 B and ldx % 8 == 0 when x_perm is NULL;
+ *    2 B otherwise.
+ * w  the layer; path selects the metadata load (see tpdq_path). The
+ *    act-order paths need w->g_idx; values outside [0, num_groups) are
  *    clamped into range (no fault; such rows give unspecified results).
  * Y  [M][ldy] output, 8 B aligned, ldy % 4 == 0, ldy >= N.
- * Workspace: at least tpdq_workspace_bytes(1, M, w, NULL) bytes, zero-filled
- * before its first use with this library; every call leaves its counter words
- * zero again when it completes. Calls that overlap in time must not share a
- * workspace. Deterministic: the same inputs give bit-identical outputs.
+ * Workspace: at least tpdq_workspace_bytes(1, M, w, NULL) bytes, any content
+ * (it holds the gathered X' when the gather cannot be done on chip). Calls
+ * that overlap in time must not share a workspace. Deterministic: the same
+ * inputs give bit-identical outputs.
  */
 tpdq_status tpdq_w4a16_gemm(const void* X, int64_t ldx, int32_t M, const int32_t* x_perm,
                             const tpdq_w4* w, tpdq_path path, tpdq_dtype dtype,
@@ -153,14 +186,14 @@ tpdq_status tpdq_w4a16_gemm(const void* X, int64_t ldx, int32_t M, const int32_t
  *   w2 its row shard of W2[P2] (sorted rows, so local groups are floor(k/G));
  *   Y1 = X[:, P1] @ deq(w1), Y2_partial = Y1 @ deq(w2). No permute or gather
  *   of Y1 happens between the GEMMs. P1 (int32 [K1], global) is required.
- * TPDQ_PATH_ACTORDER: w1 is the rank's column shard of W1 with its g_idx, w2
- *   the row shard of W2 with its rows' global g_idx values and the full
- *   metadata (num_groups = K2_global/G); P1 must be NULL.
+ * TPDQ_PATH_ACTORDER / TPDQ_PATH_ACTORDER_GLOBAL: w1 is the rank's column
+ *   shard of W1 with its g_idx, w2 the row shard of W2 with its rows' global
+ *   g_idx values and the full metadata (num_groups = K2_global/G); P1 must be
+ *   NULL.
  * Requirements: w2->K == w1->N. X [M][ldx] with w1->K columns used.
  * Y1 [M][w1->N] and Y2_partial [M][w2->N], dense, written in the activation
  * dtype; Y2_partial is this rank's summand of the AllReduce(SUM) of Alg. 3.
- * Workspace: tpdq_workspace_bytes(2, M, w1, w2) bytes, zero-filled before
- * first use, as for tpdq_w4a16_gemm.
+ * Workspace: tpdq_workspace_bytes(2, M, w1, w2) bytes, any content.
  */
 tpdq_status tpdq_mlp_shard(const void* X, int64_t ldx, int32_t M, const int32_t* P1,
                            const tpdq_w4* w1, const tpdq_w4* w2, tpdq_path path,

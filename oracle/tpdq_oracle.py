@@ -77,6 +77,38 @@ def pack_cols(z: np.ndarray) -> np.ndarray:
     return w.view(np.int32)
 
 
+def tiled_ld(K: int) -> int:
+    return (K + 127) // 128 * 256
+
+
+def untile(qt: np.ndarray, K: int, N: int) -> np.ndarray:
+    """GPTQ words [K/8][N] of a qweight stored in the tiled order: for tile t
+    (16 columns), block b (128 rows), lane l = 16 kq + j and step u,
+    tiled[t][256 b + 4 l + u] is GPTQ word [4 (4 b + u) + kq][16 t + j]."""
+    qt = np.asarray(qt).view(np.uint32)
+    r = np.arange(K // 8)[:, None]
+    c = np.arange(N)[None, :]
+    s, kq = r // 4, r % 4
+    b, u = s // 4, s % 4
+    t, jj = c // 16, c % 16
+    return qt[t, 256 * b + 4 * (16 * kq + jj) + u].view(np.int32)
+
+
+def tile(qw: np.ndarray) -> np.ndarray:
+    """Inverse of untile, with zero padding past K and N."""
+    qw = np.asarray(qw).view(np.uint32)
+    kw, N = qw.shape
+    K = kw * 8
+    out = np.zeros(((N + 15) // 16, tiled_ld(K)), dtype=np.uint32)
+    r = np.arange(kw)[:, None]
+    c = np.arange(N)[None, :]
+    s, kq = r // 4, r % 4
+    b, u = s // 4, s % 4
+    t, jj = c // 16, c % 16
+    out[t, 256 * b + 4 * (16 * kq + jj) + u] = qw
+    return out.view(np.int32)
+
+
 # ----------------------------------------------------------------------------
 # Group index arrays (section 1.1, Eq. 1-3) and the reorder (section 2.1, Alg. 1)
 # ----------------------------------------------------------------------------

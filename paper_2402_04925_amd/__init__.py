@@ -12,12 +12,13 @@ import dataclasses
 from typing import Optional
 
 from . import _abi
-from ._abi import (BF16, FP16, OP_GEMM, OP_MLP, OP_REORDER, PATH_ACTORDER, PATH_ORDERED,
-                   TpdqError)
+from ._abi import (BF16, FP16, LAYOUT_GPTQ, LAYOUT_TILED, OP_GEMM, OP_MLP, OP_REORDER,
+                   PATH_ACTORDER, PATH_ACTORDER_GLOBAL, PATH_ORDERED, TpdqError)
 
 __all__ = [
-    "QuantWeight", "reorder", "w4a16_gemm", "mlp_shard", "workspace_bytes", "Workspace",
-    "TpdqError", "PATH_ACTORDER", "PATH_ORDERED", "FP16", "BF16", "version",
+    "QuantWeight", "reorder", "pack_tiled", "w4a16_gemm", "mlp_shard", "workspace_bytes", "Workspace",
+    "LAYOUT_GPTQ", "LAYOUT_TILED", "tiled_ld",
+    "TpdqError", "PATH_ACTORDER", "PATH_ORDERED", "PATH_ACTORDER_GLOBAL", "FP16", "BF16", "version",
 ]
 
 
@@ -48,12 +49,19 @@ def _dtype_code(dt) -> int:
     raise TypeError(f"activations and scales must be float16 or bfloat16, got {dt}")
 
 
+def tiled_ld(K: int) -> int:
+    """Words per 16-column tile of a dense tiled qweight with K rows."""
+    return (K + 127) // 128 * 256
+
+
 @dataclasses.dataclass
 class QuantWeight:
     """A quantized layer (or a shard of one as views) in device memory.
 
-    qweight int32 [K/8][>=N], scales fp16 [num_groups][>=N],
-    qzeros int32 [num_groups][>=N/8], g_idx int32 [K] or None.
+    qweight int32: GPTQ layout [K/8][>=N], or tiled layout
+    [ceil(N/16)][>=tiled_ld(K)] (see include/tpdq.h); scales fp16
+    [num_groups][>=N]; qzeros int32 [num_groups][>=N/8]; g_idx int32 [K] or
+    None.
     """
     qweight: object
     scales: object
@@ -63,13 +71,15 @@ class QuantWeight:
     N: int
     G: int
     num_groups: int
+    layout: int = LAYOUT_GPTQ
 
     @classmethod
     def from_tensors(cls, qweight, scales, qzeros, g_idx, G: int, num_groups: Optional[int] = None):
+        """A GPTQ-layout layer: K and N follow from qweight's shape."""
         K = qweight.shape[0] * 8
         N = qweight.shape[1]
         ng = scales.shape[0] if num_groups is None else num_groups
-        return cls(qweight, scales, qzeros, g_idx, K, N, G, ng)
+        return cls(qweight, scales, qzeros, g_idx, K, N, G, ng, LAYOUT_GPTQ)
 
     def c_struct(self) -> _abi.W4:
         for name in ("qweight", "scales", "qzeros"):
@@ -83,7 +93,7 @@ class QuantWeight:
             scales=_ptr(self.scales), ld_s=self.scales.stride(0),
             qzeros=_ptr(self.qzeros), ld_z=self.qzeros.stride(0),
             g_idx=_ptr(self.g_idx), K=self.K, N=self.N, group_size=self.G,
-            num_groups=self.num_groups)
+            num_groups=self.num_groups, layout=self.layout)
 
     @property
     def device(self):
@@ -93,9 +103,14 @@ class QuantWeight:
         """Megatron column-parallel shard (views): columns [rank*N/tp, ...)."""
         n = self.N // tp
         c0 = rank * n
-        return QuantWeight(self.qweight[:, c0:c0 + n], self.scales[:, c0:c0 + n],
-                           self.qzeros[:, c0 // 8:(c0 + n) // 8], self.g_idx, self.K, n, self.G,
-                           self.num_groups)
+        if self.layout == LAYOUT_TILED:
+            if c0 % 16 or n % 16:
+                raise ValueError("a tiled column shard must start and end on 16-column tiles")
+            qw = self.qweight[c0 // 16:(c0 + n) // 16]
+        else:
+            qw = self.qweight[:, c0:c0 + n]
+        return QuantWeight(qw, self.scales[:, c0:c0 + n], self.qzeros[:, c0 // 8:(c0 + n) // 8],
+                           self.g_idx, self.K, n, self.G, self.num_groups, self.layout)
 
     def row_shard(self, rank: int, tp: int, sorted_rows: bool) -> "QuantWeight":
         """Megatron row-parallel shard (views): rows [rank*K/tp, ...).
@@ -104,20 +119,24 @@ class QuantWeight:
         keep the global g_idx values of their rows and all the metadata."""
         k = self.K // tp
         r0 = rank * k
-        qw = self.qweight[r0 // 8:(r0 + k) // 8]
+        if self.layout == LAYOUT_TILED:
+            if r0 % 128:
+                raise ValueError("a tiled row shard must start on a 128-row block")
+            qw = self.qweight[:, (r0 // 128) * 256:]
+        else:
+            qw = self.qweight[r0 // 8:(r0 + k) // 8]
         g = None if self.g_idx is None else self.g_idx[r0:r0 + k]
         if sorted_rows:
             g0, ng = r0 // self.G, k // self.G
             return QuantWeight(qw, self.scales[g0:g0 + ng], self.qzeros[g0:g0 + ng], g, k, self.N,
-                               self.G, ng)
-        return QuantWeight(qw, self.scales, self.qzeros, g, k, self.N, self.G, self.num_groups)
+                               self.G, ng, self.layout)
+        return QuantWeight(qw, self.scales, self.qzeros, g, k, self.N, self.G, self.num_groups,
+                           self.layout)
 
 
 class Workspace:
-    """Zero-initialised device scratch for the library calls, grown on demand.
-
-    The kernels leave their counter words at zero, so one workspace can serve
-    any number of calls issued one after another on one stream."""
+    """Device scratch for the library calls, grown on demand. One workspace
+    serves any number of calls issued one after another on one stream."""
 
     def __init__(self, device=None):
         self.device = device
@@ -127,7 +146,7 @@ class Workspace:
         torch = _torch()
         if self.buf is None or self.buf.numel() < nbytes:
             n = max(nbytes, 1 << 20)
-            self.buf = torch.zeros(n, dtype=torch.uint8, device=self.device)
+            self.buf = torch.empty(n, dtype=torch.uint8, device=self.device)
         return self.buf
 
 
@@ -150,25 +169,32 @@ def workspace_bytes(op: int, M: int, a: QuantWeight, b: Optional[QuantWeight] = 
                                           ctypes.byref(cb) if cb is not None else None)
 
 
-def reorder(w1: QuantWeight, w2: Optional[QuantWeight] = None, workspace: Optional[Workspace] = None):
+def reorder(w1: QuantWeight, w2: Optional[QuantWeight] = None, workspace: Optional[Workspace] = None,
+            layout: int = LAYOUT_TILED):
     """Alg. 1 on w1 (and w2) plus the TP-aware fold W1[P1, P2], W2[P2].
 
     Returns (P1, g1_sorted, P2, g2_sorted, w1_out, w2_out); P2, g2_sorted and
-    w2_out are None without w2. w1_out/w2_out are sorted-row QuantWeights
-    (their g_idx is the sorted g_idx)."""
+    w2_out are None without w2. w1_out/w2_out are sorted-row QuantWeights in
+    `layout` (their g_idx is the sorted g_idx)."""
     torch = _torch()
     dev = w1.device
     i32 = dict(dtype=torch.int32, device=dev)
+
+    def qbuf(K, N):
+        if layout == LAYOUT_TILED:
+            return torch.empty((N + 15) // 16, tiled_ld(K), **i32)
+        return torch.empty(K // 8, N, **i32)
+
     P1 = torch.empty(w1.K, **i32)
     g1 = torch.empty(w1.K, **i32)
-    q1 = torch.empty(w1.K // 8, w1.N, **i32)
+    q1 = qbuf(w1.K, w1.N)
     s1 = torch.empty(w1.num_groups, w1.N, dtype=w1.scales.dtype, device=dev)
     z1 = torch.empty(w1.num_groups, w1.N // 8, **i32)
     P2 = g2 = q2 = None
     if w2 is not None:
         P2 = torch.empty(w2.K, **i32)
         g2 = torch.empty(w2.K, **i32)
-        q2 = torch.empty(w2.K // 8, w2.N, **i32)
+        q2 = qbuf(w2.K, w2.N)
     c1 = w1.c_struct()
     c2 = w2.c_struct() if w2 is not None else None
     lib = _abi.lib()
@@ -178,12 +204,21 @@ def reorder(w1: QuantWeight, w2: Optional[QuantWeight] = None, workspace: Option
     _abi.check(lib.tpdq_reorder(
         ctypes.byref(c1), ctypes.byref(c2) if c2 is not None else None,
         _ptr(P1), _ptr(g1), _ptr(P2), _ptr(g2), _ptr(q1), _ptr(s1), _ptr(z1), _ptr(q2),
-        _dtype_code(w1.scales.dtype), _ptr(buf), buf.numel(), _stream_handle(dev)))
-    w1o = QuantWeight(q1, s1, z1, g1, w1.K, w1.N, w1.G, w1.num_groups)
+        _dtype_code(w1.scales.dtype), layout, _ptr(buf), buf.numel(), _stream_handle(dev)))
+    w1o = QuantWeight(q1, s1, z1, g1, w1.K, w1.N, w1.G, w1.num_groups, layout)
     w2o = None
     if w2 is not None:
-        w2o = QuantWeight(q2, w2.scales, w2.qzeros, g2, w2.K, w2.N, w2.G, w2.num_groups)
+        w2o = QuantWeight(q2, w2.scales, w2.qzeros, g2, w2.K, w2.N, w2.G, w2.num_groups, layout)
     return P1, g1, P2, g2, w1o, w2o
+
+
+def pack_tiled(w: QuantWeight) -> QuantWeight:
+    """The same layer with qweight in the tiled layout (metadata shared)."""
+    torch = _torch()
+    out = torch.empty((w.N + 15) // 16, tiled_ld(w.K), dtype=torch.int32, device=w.device)
+    c = w.c_struct()
+    _abi.check(_abi.lib().tpdq_pack_tiled(ctypes.byref(c), _ptr(out), _stream_handle(w.device)))
+    return QuantWeight(out, w.scales, w.qzeros, w.g_idx, w.K, w.N, w.G, w.num_groups, LAYOUT_TILED)
 
 
 def w4a16_gemm(X, w: QuantWeight, path: int, x_perm=None, out=None,

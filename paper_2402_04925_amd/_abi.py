@@ -9,11 +9,12 @@ LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libtpdq.so"
 
 OK, ERR_NULL, ERR_SHAPE, ERR_ALIGN, ERR_GIDX, ERR_WORKSPACE, ERR_UNSUPPORTED, ERR_HIP = range(8)
 FP16, BF16 = 0, 1
-PATH_ACTORDER, PATH_ORDERED = 0, 1
+PATH_ACTORDER, PATH_ORDERED, PATH_ACTORDER_GLOBAL = 0, 1, 2
 OP_REORDER, OP_GEMM, OP_MLP = 0, 1, 2
+LAYOUT_GPTQ, LAYOUT_TILED = 0, 1
 
 EXPORTED = (
-    "tpdq_reorder", "tpdq_w4a16_gemm", "tpdq_mlp_shard", "tpdq_workspace_bytes",
+    "tpdq_reorder", "tpdq_pack_tiled", "tpdq_w4a16_gemm", "tpdq_mlp_shard", "tpdq_workspace_bytes",
     "tpdq_status_string", "tpdq_last_error", "tpdq_version",
 )
 
@@ -27,6 +28,7 @@ class W4(ctypes.Structure):
         ("g_idx", ctypes.c_void_p),
         ("K", ctypes.c_int32), ("N", ctypes.c_int32),
         ("group_size", ctypes.c_int32), ("num_groups", ctypes.c_int32),
+        ("layout", ctypes.c_int32),
     ]
 
 
@@ -37,8 +39,11 @@ _lib = None
 def _declare(lib):
     vp, i32, i64, sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_size_t
     pw = ctypes.POINTER(W4)
-    lib.tpdq_reorder.argtypes = [pw, pw, vp, vp, vp, vp, vp, vp, vp, vp, ctypes.c_int, vp, sz, vp]
+    lib.tpdq_reorder.argtypes = [pw, pw, vp, vp, vp, vp, vp, vp, vp, vp, ctypes.c_int, ctypes.c_int,
+                                 vp, sz, vp]
     lib.tpdq_reorder.restype = ctypes.c_int
+    lib.tpdq_pack_tiled.argtypes = [pw, vp, vp]
+    lib.tpdq_pack_tiled.restype = ctypes.c_int
     lib.tpdq_w4a16_gemm.argtypes = [vp, i64, i32, vp, pw, ctypes.c_int, ctypes.c_int, vp, i64, vp,
                                     sz, vp]
     lib.tpdq_w4a16_gemm.restype = ctypes.c_int

@@ -53,7 +53,10 @@ tpdq_status check_layer(const tpdq_w4* w, const char* name, bool need_gidx, bool
       return fail(TPDQ_ERR_SHAPE, "%s: num_groups=%d < K/G=%d", name, w->num_groups,
                   w->K / w->group_size);
   }
-  if (w->ld_q < w->N || w->ld_s < w->N || w->ld_z < w->N / 8)
+  if (w->layout != TPDQ_LAYOUT_GPTQ && w->layout != TPDQ_LAYOUT_TILED)
+    return fail(TPDQ_ERR_SHAPE, "%s: unknown layout %d", name, w->layout);
+  const int64_t ldq_min = w->layout == TPDQ_LAYOUT_TILED ? tiled_ld(w->K) : (int64_t)w->N;
+  if (w->ld_q < ldq_min || w->ld_s < w->N || w->ld_z < w->N / 8)
     return fail(TPDQ_ERR_SHAPE, "%s: leading dimensions too small (ld_q=%lld ld_s=%lld ld_z=%lld)",
                 name, (long long)w->ld_q, (long long)w->ld_s, (long long)w->ld_z);
   if (!aligned(w->qweight, 16) || w->ld_q % 4)
@@ -66,69 +69,79 @@ tpdq_status check_layer(const tpdq_w4* w, const char* name, bool need_gidx, bool
   return TPDQ_OK;
 }
 
-// Workspace layout of the GEMM and MLP calls:
-//   [counters][split-K partials][gathered activations]
-struct GemmWs {
-  size_t counters = 0, partials = 0, xperm = 0, total = 0;
-};
+// Workspace of the GEMM and MLP calls: only the gathered activations, when
+// the gather X[:, perm] cannot be done inside the GEMM's LDS.
+size_t gather_ws_bytes(int M, int K) { return align_up((size_t)M * K * 2); }
 
-GemmWs gemm_ws(int M, const tpdq_w4* a, const tpdq_w4* b, bool gather, int Kgather) {
-  const int mc = std::min(M, kDecodeMaxM);
-  int ncol = (a->N + kDecodeCols - 1) / kDecodeCols;
-  size_t part = 0;
-  const int sa = decode_splits(mc, a->K, a->N);
-  if (sa > 1) part = (size_t)sa * mc * a->N * 4;
-  if (b) {
-    ncol = std::max(ncol, (b->N + kDecodeCols - 1) / kDecodeCols);
-    const int sb = decode_splits(mc, b->K, b->N);
-    if (sb > 1) part = std::max(part, (size_t)sb * mc * b->N * 4);
-  }
-  GemmWs w;
-  w.counters = 0;
-  w.partials = align_up((size_t)ncol * 4);
-  w.xperm = w.partials + align_up(part);
-  w.total = w.xperm + (gather ? align_up((size_t)M * Kgather * 2) : 0);
-  return w;
+int meta_mode(tpdq_path path) {
+  if (path == TPDQ_PATH_ORDERED) return kMetaGroup;
+  if (path == TPDQ_PATH_ACTORDER_GLOBAL) return kMetaRowGlobal;
+  return kMetaRowLds;
 }
 
 // One GEMM through the decode kernels, M cut into launches of <= 64 rows.
-tpdq_status run_gemm(const uint16_t* X, int64_t ldx, int M, const tpdq_w4* w, tpdq_path path,
-                     uint16_t* Y, int64_t ldy, char* ws, const GemmWs& lay, hipStream_t st) {
+// perm != NULL: the operand is X[:, perm]; it is gathered inside the kernel
+// when it fits in LDS, else into the workspace first (already in operand
+// order).
+tpdq_status run_gemm(const uint16_t* X, int64_t ldx, int M, const int32_t* perm, const tpdq_w4* w,
+                     tpdq_path path, uint16_t* Y, int64_t ldy, char* ws, hipStream_t st) {
+  const int meta = meta_mode(path);
+  const int32_t* gidx = path == TPDQ_PATH_ORDERED ? nullptr : w->g_idx;
   for (int m0 = 0; m0 < M; m0 += kDecodeMaxM) {
     const int mc = std::min(kDecodeMaxM, M - m0);
-    GemmArgs a;
-    a.X = X + (int64_t)m0 * ldx;
-    a.ldx = ldx;
+    const uint16_t* Xc = X + (int64_t)m0 * ldx;
+    int64_t ldc = ldx;
+    DecodePlan plan;
+    int operand = kOperandPlain;
+    bool ok;
+    if (perm) {
+      operand = kOperandGather;
+      ok = plan_decode(mc, w->K, w->N, w->group_size, w->num_groups, w->layout, meta, operand, &plan);
+      if (!ok) {
+        uint16_t* Xp = (uint16_t*)ws;
+        hipError_t e = launch_gather_prep(Xc, ldx, mc, w->K, perm, Xp, st);
+        if (e != hipSuccess) return hip_fail(e, "activation gather launch");
+        Xc = Xp;
+        ldc = w->K;
+        operand = kOperandPrepared;
+        ok = plan_decode(mc, w->K, w->N, w->group_size, w->num_groups, w->layout, meta, operand,
+                         &plan);
+      }
+    } else {
+      ok = plan_decode(mc, w->K, w->N, w->group_size, w->num_groups, w->layout, meta, operand, &plan);
+    }
+    if (!ok)
+      return fail(TPDQ_ERR_UNSUPPORTED, "no decode kernel for M=%d K=%d N=%d G=%d", mc, w->K, w->N,
+                  w->group_size);
+    GemmArgs a{};
+    a.X = Xc;
+    a.ldx = ldc;
     a.M = mc;
+    a.perm = operand == kOperandGather ? perm : nullptr;
     a.qw = (const uint32_t*)w->qweight;
     a.ldq = w->ld_q;
     a.sc = (const uint16_t*)w->scales;
     a.lds = w->ld_s;
     a.qz = (const uint32_t*)w->qzeros;
     a.ldz = w->ld_z;
-    a.g_idx = w->g_idx;
+    a.g_idx = gidx;
     a.K = w->K;
     a.N = w->N;
     a.G = w->group_size;
     a.num_groups = w->num_groups;
     a.Y = Y + (int64_t)m0 * ldy;
     a.ldy = ldy;
-    a.splits = decode_splits(mc, w->K, w->N);
-    a.partials = (float*)(ws + lay.partials);
-    a.counters = (uint32_t*)(ws + lay.counters);
-    hipError_t e;
-    if (path == TPDQ_PATH_ORDERED && w->group_size % 32 == 0)
-      e = launch_decode_ordered(a, st);
-    else
-      e = launch_decode_rowmeta(a, path == TPDQ_PATH_ACTORDER, st);
+    hipError_t e = launch_decode(a, plan, st);
     if (e != hipSuccess) return hip_fail(e, "decode GEMM launch");
   }
   return TPDQ_OK;
 }
 
+bool is_actorder(tpdq_path p) { return p == TPDQ_PATH_ACTORDER || p == TPDQ_PATH_ACTORDER_GLOBAL; }
+
 tpdq_status check_common(int32_t M, tpdq_path path, tpdq_dtype dtype) {
   if (M < 1) return fail(TPDQ_ERR_SHAPE, "M=%d must be >= 1", M);
-  if (path != TPDQ_PATH_ACTORDER && path != TPDQ_PATH_ORDERED)
+  if (path != TPDQ_PATH_ACTORDER && path != TPDQ_PATH_ORDERED && path != TPDQ_PATH_ACTORDER_GLOBAL)
     return fail(TPDQ_ERR_SHAPE, "unknown path %d", (int)path);
   if (dtype == TPDQ_BF16) return fail(TPDQ_ERR_UNSUPPORTED, "bf16 activations are not built yet");
   if (dtype != TPDQ_FP16) return fail(TPDQ_ERR_SHAPE, "unknown dtype %d", (int)dtype);
@@ -165,10 +178,10 @@ size_t tpdq_workspace_bytes(int op, int32_t M, const tpdq_w4* a, const tpdq_w4* 
     return n;
   }
   if (M < 1) return 0;
-  if (op == 1) return gemm_ws(M, a, nullptr, true, a->K).total;
+  if (op == 1) return gather_ws_bytes(std::min(M, (int32_t)kDecodeMaxM), a->K);
   if (op == 2) {
     if (!b) return 0;
-    return gemm_ws(M, a, b, true, a->K).total;
+    return gather_ws_bytes(std::min(M, (int32_t)kDecodeMaxM), a->K);
   }
   return 0;
 }
@@ -176,9 +189,14 @@ size_t tpdq_workspace_bytes(int op, int32_t M, const tpdq_w4* a, const tpdq_w4* 
 tpdq_status tpdq_reorder(const tpdq_w4* w1, const tpdq_w4* w2, int32_t* P1, int32_t* g1_sorted,
                          int32_t* P2, int32_t* g2_sorted, int32_t* qweight1_out,
                          void* scales1_out, int32_t* qzeros1_out, int32_t* qweight2_out,
-                         tpdq_dtype dtype, void* workspace, size_t ws_bytes, void* stream) {
+                         tpdq_dtype dtype, tpdq_layout out_layout, void* workspace,
+                         size_t ws_bytes, void* stream) {
   tpdq_status st = check_layer(w1, "w1", true, true);
   if (st != TPDQ_OK) return st;
+  if (w1->layout != TPDQ_LAYOUT_GPTQ || (w2 && w2->layout != TPDQ_LAYOUT_GPTQ))
+    return fail(TPDQ_ERR_SHAPE, "reorder takes GPTQ-layout inputs");
+  if (out_layout != TPDQ_LAYOUT_GPTQ && out_layout != TPDQ_LAYOUT_TILED)
+    return fail(TPDQ_ERR_SHAPE, "unknown output layout %d", (int)out_layout);
   if (dtype != TPDQ_FP16 && dtype != TPDQ_BF16) return fail(TPDQ_ERR_SHAPE, "unknown dtype");
   if (w1->num_groups != w1->K / w1->group_size)
     return fail(TPDQ_ERR_SHAPE, "w1: a global act-order layer has num_groups == K/G");
@@ -236,7 +254,7 @@ tpdq_status tpdq_reorder(const tpdq_w4* w1, const tpdq_w4* w2, int32_t* P1, int3
   const int32_t* pcol = w2 ? P2 : nullptr;
   const int ng1 = w1->num_groups;
   e = launch_permute_qweight((const uint32_t*)w1->qweight, w1->ld_q, w1->K, w1->N, P1, pcol,
-                             (uint32_t*)qweight1_out, s);
+                             (uint32_t*)qweight1_out, out_layout, s);
   if (e == hipSuccess)
     e = launch_permute_scales((const uint16_t*)w1->scales, w1->ld_s, ng1, w1->N, pcol,
                               (uint16_t*)scales1_out, s);
@@ -245,8 +263,23 @@ tpdq_status tpdq_reorder(const tpdq_w4* w1, const tpdq_w4* w2, int32_t* P1, int3
                               (uint32_t*)qzeros1_out, s);
   if (e == hipSuccess && w2)
     e = launch_permute_qweight((const uint32_t*)w2->qweight, w2->ld_q, w2->K, w2->N, P2, nullptr,
-                               (uint32_t*)qweight2_out, s);
+                               (uint32_t*)qweight2_out, out_layout, s);
   if (e != hipSuccess) return hip_fail(e, "permute launch");
+  return TPDQ_OK;
+}
+
+tpdq_status tpdq_pack_tiled(const tpdq_w4* w, int32_t* qweight_out, void* stream) {
+  if (!w) return fail(TPDQ_ERR_NULL, "w is NULL");
+  if (!w->qweight || !qweight_out) return fail(TPDQ_ERR_NULL, "qweight and qweight_out are required");
+  if (w->layout != TPDQ_LAYOUT_GPTQ) return fail(TPDQ_ERR_SHAPE, "input must be GPTQ layout");
+  if (w->K <= 0 || w->N <= 0 || w->K % 8 || w->N % 8)
+    return fail(TPDQ_ERR_SHAPE, "K=%d and N=%d must be positive multiples of 8", w->K, w->N);
+  if (w->ld_q < w->N) return fail(TPDQ_ERR_SHAPE, "ld_q=%lld < N=%d", (long long)w->ld_q, w->N);
+  if (!aligned(qweight_out, 16)) return fail(TPDQ_ERR_ALIGN, "qweight_out needs 16-byte alignment");
+  hipError_t e = launch_permute_qweight((const uint32_t*)w->qweight, w->ld_q, w->K, w->N, nullptr,
+                                        nullptr, (uint32_t*)qweight_out, TPDQ_LAYOUT_TILED,
+                                        (hipStream_t)stream);
+  if (e != hipSuccess) return hip_fail(e, "pack launch");
   return TPDQ_OK;
 }
 
@@ -255,7 +288,7 @@ tpdq_status tpdq_w4a16_gemm(const void* X, int64_t ldx, int32_t M, const int32_t
                             int64_t ldy, void* workspace, size_t ws_bytes, void* stream) {
   tpdq_status st = check_common(M, path, dtype);
   if (st != TPDQ_OK) return st;
-  st = check_layer(w, "w", path == TPDQ_PATH_ACTORDER, path == TPDQ_PATH_ORDERED);
+  st = check_layer(w, "w", is_actorder(path), path == TPDQ_PATH_ORDERED);
   if (st != TPDQ_OK) return st;
   if (!X || !Y) return fail(TPDQ_ERR_NULL, "X and Y are required");
   if (ldx < w->K || ldy < w->N)
@@ -267,23 +300,13 @@ tpdq_status tpdq_w4a16_gemm(const void* X, int64_t ldx, int32_t M, const int32_t
     return fail(TPDQ_ERR_ALIGN, "X needs 16-byte alignment and ldx %% 8 == 0");
   }
   if (!aligned(Y, 8) || ldy % 4) return fail(TPDQ_ERR_ALIGN, "Y needs 8-byte alignment, ldy %% 4 == 0");
-  const GemmWs lay = gemm_ws(M, w, nullptr, x_perm != nullptr, w->K);
-  if (!workspace || ws_bytes < lay.total)
-    return fail(TPDQ_ERR_WORKSPACE, "GEMM needs %zu workspace bytes, got %zu", lay.total, ws_bytes);
-  if (!aligned(workspace, 16)) return fail(TPDQ_ERR_ALIGN, "workspace needs 16-byte alignment");
-
-  hipStream_t s = (hipStream_t)stream;
-  char* ws = (char*)workspace;
-  const uint16_t* Xin = (const uint16_t*)X;
-  int64_t ldin = ldx;
-  if (x_perm) {
-    uint16_t* Xp = (uint16_t*)(ws + lay.xperm);
-    hipError_t e = launch_gather_cols(Xin, ldx, M, w->K, x_perm, Xp, s);
-    if (e != hipSuccess) return hip_fail(e, "activation gather launch");
-    Xin = Xp;
-    ldin = w->K;
-  }
-  return run_gemm(Xin, ldin, M, w, path, (uint16_t*)Y, ldy, ws, lay, s);
+  const size_t need = tpdq_workspace_bytes(1, M, w, nullptr);
+  if (x_perm && (!workspace || ws_bytes < need))
+    return fail(TPDQ_ERR_WORKSPACE, "GEMM needs %zu workspace bytes, got %zu", need, ws_bytes);
+  if (workspace && !aligned(workspace, 16))
+    return fail(TPDQ_ERR_ALIGN, "workspace needs 16-byte alignment");
+  return run_gemm((const uint16_t*)X, ldx, M, x_perm, w, path, (uint16_t*)Y, ldy, (char*)workspace,
+                  (hipStream_t)stream);
 }
 
 tpdq_status tpdq_mlp_shard(const void* X, int64_t ldx, int32_t M, const int32_t* P1,
@@ -292,14 +315,14 @@ tpdq_status tpdq_mlp_shard(const void* X, int64_t ldx, int32_t M, const int32_t*
                            void* stream) {
   tpdq_status st = check_common(M, path, dtype);
   if (st != TPDQ_OK) return st;
-  const bool act = path == TPDQ_PATH_ACTORDER;
+  const bool act = is_actorder(path);
   st = check_layer(w1, "w1", act, !act);
   if (st != TPDQ_OK) return st;
   st = check_layer(w2, "w2", act, !act);
   if (st != TPDQ_OK) return st;
   if (w2->K != w1->N) return fail(TPDQ_ERR_SHAPE, "w2->K=%d != w1->N=%d", w2->K, w1->N);
   if (!X || !Y1 || !Y2_partial) return fail(TPDQ_ERR_NULL, "X, Y1 and Y2_partial are required");
-  if (act && P1) return fail(TPDQ_ERR_SHAPE, "the act-order path takes no P1");
+  if (act && P1) return fail(TPDQ_ERR_SHAPE, "the act-order paths take no P1");
   if (!act && !P1) return fail(TPDQ_ERR_NULL, "the ordered path needs P1");
   if (ldx < w1->K) return fail(TPDQ_ERR_SHAPE, "ldx=%lld < K1=%d", (long long)ldx, w1->K);
   if (act) {
@@ -310,25 +333,18 @@ tpdq_status tpdq_mlp_shard(const void* X, int64_t ldx, int32_t M, const int32_t*
   }
   if (!aligned(Y1, 16) || !aligned(Y2_partial, 8))
     return fail(TPDQ_ERR_ALIGN, "Y1 needs 16-byte and Y2_partial 8-byte alignment");
-  const GemmWs lay = gemm_ws(M, w1, w2, !act, w1->K);
-  if (!workspace || ws_bytes < lay.total)
-    return fail(TPDQ_ERR_WORKSPACE, "MLP needs %zu workspace bytes, got %zu", lay.total, ws_bytes);
-  if (!aligned(workspace, 16)) return fail(TPDQ_ERR_ALIGN, "workspace needs 16-byte alignment");
+  const size_t need = tpdq_workspace_bytes(2, M, w1, w2);
+  if (!act && (!workspace || ws_bytes < need))
+    return fail(TPDQ_ERR_WORKSPACE, "MLP needs %zu workspace bytes, got %zu", need, ws_bytes);
+  if (workspace && !aligned(workspace, 16))
+    return fail(TPDQ_ERR_ALIGN, "workspace needs 16-byte alignment");
 
   hipStream_t s = (hipStream_t)stream;
   char* ws = (char*)workspace;
-  const uint16_t* Xin = (const uint16_t*)X;
-  int64_t ldin = ldx;
-  if (!act) {
-    uint16_t* Xp = (uint16_t*)(ws + lay.xperm);
-    hipError_t e = launch_gather_cols(Xin, ldx, M, w1->K, P1, Xp, s);
-    if (e != hipSuccess) return hip_fail(e, "activation gather launch");
-    Xin = Xp;
-    ldin = w1->K;
-  }
-  st = run_gemm(Xin, ldin, M, w1, path, (uint16_t*)Y1, w1->N, ws, lay, s);
+  st = run_gemm((const uint16_t*)X, ldx, M, act ? nullptr : P1, w1, path, (uint16_t*)Y1, w1->N, ws, s);
   if (st != TPDQ_OK) return st;
-  return run_gemm((const uint16_t*)Y1, w1->N, M, w2, path, (uint16_t*)Y2_partial, w2->N, ws, lay, s);
+  return run_gemm((const uint16_t*)Y1, w1->N, M, nullptr, w2, path, (uint16_t*)Y2_partial, w2->N, ws,
+                  s);
 }
 
 }  // extern "C"

@@ -69,27 +69,64 @@ __global__ __launch_bounds__(256) void k_rank_group(const int32_t* __restrict__ 
   }
 }
 
-// dst[r][c] (packed rows) = src rows P_row[8r..8r+7] of column P_col[c]:
-// nibble t of dst word [r][c] = nibble (i & 7) of src word [i >> 3][cs],
-// i = P_row[8r + t], cs = P_col ? P_col[c] : c.
+// One output word: rows P_row[8r .. 8r+7] of source column cs; nibble t of
+// the result = nibble (i & 7) of src word [i >> 3][cs], i = P_row[8r + t].
+__device__ __forceinline__ uint32_t gather_word(const uint32_t* __restrict__ src, int64_t ld_src,
+                                                int K, const int32_t* __restrict__ Prow, int r,
+                                                uint32_t cs) {
+  if (!Prow) return src[(int64_t)r * ld_src + cs];
+  const uint32_t kmax = (uint32_t)(K - 1);
+  uint32_t out = 0;
+#pragma unroll
+  for (int t = 0; t < 8; ++t) {
+    const uint32_t i = min((uint32_t)Prow[8 * r + t], kmax);
+    const uint32_t w = src[(int64_t)(i >> 3) * ld_src + cs];
+    out |= ((w >> (4 * (i & 7))) & 0xFu) << (4 * t);
+  }
+  return out;
+}
+
+// GPTQ-layout output: dst[r][c] = W[P_row, P_col] word.
 __global__ void k_permute_qweight(const uint32_t* __restrict__ src, int64_t ld_src, int K, int N,
                                   const int32_t* __restrict__ Prow, const int32_t* __restrict__ Pcol,
                                   uint32_t* __restrict__ dst) {
   const int64_t words = (int64_t)(K / 8) * N;
-  const uint32_t kmax = (uint32_t)(K - 1), nmax = (uint32_t)(N - 1);
+  const uint32_t nmax = (uint32_t)(N - 1);
   for (int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; idx < words;
        idx += (int64_t)gridDim.x * blockDim.x) {
     const int r = (int)(idx / N);
     const int c = (int)(idx - (int64_t)r * N);
     const uint32_t cs = Pcol ? min((uint32_t)Pcol[c], nmax) : (uint32_t)c;
-    uint32_t out = 0;
-#pragma unroll
-    for (int t = 0; t < 8; ++t) {
-      const uint32_t i = min((uint32_t)Prow[8 * r + t], kmax);
-      const uint32_t w = src[(int64_t)(i >> 3) * ld_src + cs];
-      out |= ((w >> (4 * (i & 7))) & 0xFu) << (4 * t);
+    dst[idx] = gather_word(src, ld_src, K, Prow, r, cs);
+  }
+}
+
+// Tiled output: dst[t][256 b + 4 l + u] = word [4 (4 b + u) + kq][16 t + j],
+// l = 16 kq + j; words past K or N are zero.
+__global__ void k_permute_qweight_tiled(const uint32_t* __restrict__ src, int64_t ld_src, int K,
+                                        int N, const int32_t* __restrict__ Prow,
+                                        const int32_t* __restrict__ Pcol,
+                                        uint32_t* __restrict__ dst) {
+  const int64_t ld = tiled_ld(K);
+  const int ntiles = (N + 15) / 16;
+  const int64_t words = (int64_t)ntiles * ld;
+  const uint32_t nmax = (uint32_t)(N - 1);
+  const int kw = K / 8;
+  for (int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; idx < words;
+       idx += (int64_t)gridDim.x * blockDim.x) {
+    const int t = (int)(idx / ld);
+    const int o = (int)(idx - (int64_t)t * ld);
+    const int b = o >> 8;
+    const int l = (o >> 2) & 63;
+    const int u = o & 3;
+    const int r = 4 * (4 * b + u) + (l >> 4);
+    const int c = 16 * t + (l & 15);
+    uint32_t v = 0u;
+    if (r < kw && c < N) {
+      const uint32_t cs = Pcol ? min((uint32_t)Pcol[c], nmax) : (uint32_t)c;
+      v = gather_word(src, ld_src, K, Prow, r, cs);
     }
-    dst[idx] = out;
+    dst[idx] = v;
   }
 }
 
@@ -162,9 +199,15 @@ hipError_t launch_gidx_rank(const ReorderLayer& L, hipStream_t s) {
 
 hipError_t launch_permute_qweight(const uint32_t* src, int64_t ld_src, int K, int N,
                                   const int32_t* Prow, const int32_t* Pcol, uint32_t* dst,
-                                  hipStream_t s) {
-  hipLaunchKernelGGL(k_permute_qweight, dim3(grid_for((int64_t)(K / 8) * N)), dim3(256), 0, s, src,
-                     ld_src, K, N, Prow, Pcol, dst);
+                                  int dst_layout, hipStream_t s) {
+  if (dst_layout == TPDQ_LAYOUT_TILED) {
+    const int64_t words = (int64_t)((N + 15) / 16) * tiled_ld(K);
+    hipLaunchKernelGGL(k_permute_qweight_tiled, dim3(grid_for(words)), dim3(256), 0, s, src, ld_src,
+                       K, N, Prow, Pcol, dst);
+  } else {
+    hipLaunchKernelGGL(k_permute_qweight, dim3(grid_for((int64_t)(K / 8) * N)), dim3(256), 0, s,
+                       src, ld_src, K, N, Prow, Pcol, dst);
+  }
   return hipGetLastError();
 }
 

@@ -15,46 +15,77 @@ namespace tpdq {
 constexpr size_t kWsAlign = 256;
 inline size_t align_up(size_t x, size_t a = kWsAlign) { return (x + a - 1) / a * a; }
 
-// Columns covered by one decode workgroup (4 waves share one column tile and
-// split its K range); each lane owns 4 consecutive columns.
-constexpr int kDecodeCols = 64;
-constexpr int kDecodeWaves = 4;
-// Rows of the MFMA tile (v_mfma_f32_16x16x32_f16) and the largest M handled
-// by one decode launch (4 row tiles).
+// Decode GEMM geometry: a workgroup owns 16 output columns over the whole K
+// range (no cross-workgroup reduction); its waves split K; one MFMA tile has
+// 16 rows of M; one launch handles up to 4 row tiles.
+constexpr int kTileN = 16;
 constexpr int kTileM = 16;
 constexpr int kDecodeMaxM = 64;
+// Largest LDS a decode workgroup may use (gfx950 has 160 KB per CU).
+constexpr size_t kLdsMax = 160 * 1024;
 
-// One GEMM launch as the decode kernels see it (device pointers).
+// How a decode kernel obtains each row's scale and zero.
+enum MetaMode {
+  kMetaGroup = 0,      // sorted rows: one (scale, zero) per 32-row step, staged in LDS
+  kMetaRowGlobal = 1,  // per row through g_idx, read from global memory (Fig. 1 as drawn)
+  kMetaRowLds = 2,     // per row through g_idx, tile metadata staged in LDS
+};
+// Where the A operand (activations) comes from.
+enum AMode {
+  kAGlobal = 0,        // 16-byte fragment loads from global memory, permuted in registers
+  kALds = 1,           // whole X staged in LDS in operand order
+  kALdsGather = 2,     // X[:, perm] gathered into LDS in operand order
+  kAGlobalPrep = 3,    // 16-byte fragment loads of an operand already in operand order
+};
+// What the caller hands the GEMM as its activations.
+enum Operand {
+  kOperandPlain = 0,     // X row-major
+  kOperandGather = 1,    // X row-major, used as X[:, perm]
+  kOperandPrepared = 2,  // X[:, perm] already gathered and in operand order (k_gather_prep)
+};
+
+// One decode launch (device pointers).
 struct GemmArgs {
-  const uint16_t* X;      // [M][ldx] fp16/bf16 bits
+  const uint16_t* X;      // [M][ldx] fp16 bits
   int64_t ldx;
   int M;
-  const uint32_t* qw;     // [K/8][ldq]
+  const int32_t* perm;    // kALdsGather: column j of the operand is column perm[j] of X
+  const uint32_t* qw;     // GPTQ: [K/8][ldq]; tiled: [ceil(N/16)][ldq]
   int64_t ldq;
   const uint16_t* sc;     // [num_groups][lds]
   int64_t lds;
   const uint32_t* qz;     // [num_groups][ldz]
   int64_t ldz;
-  const int32_t* g_idx;   // [K] (act-order only)
+  const int32_t* g_idx;   // [K] (per-row metadata modes)
   int K, N, G, num_groups;
   uint16_t* Y;            // [M][ldy]
   int64_t ldy;
-  float* partials;        // [splits][M][N] fp32, when splits > 1
-  uint32_t* counters;     // [ceil(N/64)], zero on entry and on exit
-  int splits;
+  int meta_rows;          // metadata rows staged in LDS
+  int lds_x_off;          // byte offset of the staged X in LDS
 };
 
-// Split-K factor the decode launch uses for this shape (one place, so the
-// workspace query and the launch agree).
-int decode_splits(int M, int K, int N);
-// Workspace bytes for one decode GEMM (counters + partials), M <= 64.
-size_t decode_ws_bytes(int M, int K, int N);
+// Host-side plan of one decode launch.
+struct DecodePlan {
+  int layout;   // tpdq_layout of qweight
+  int meta;     // MetaMode
+  int amode;    // AMode
+  int nw;       // waves per workgroup
+  int mt;       // row tiles (1, 2, 4)
+  int spg;      // 32-row steps per group (kMetaGroup)
+  int meta_rows;
+  size_t lds_bytes;
+  int lds_x_off;
+};
 
-// Launchers (device code in gemm_decode.hip). They return hipSuccess or the
-// launch error.
-hipError_t launch_decode_ordered(const GemmArgs& a, hipStream_t s);
-hipError_t launch_decode_rowmeta(const GemmArgs& a, bool actorder, hipStream_t s);
-hipError_t launch_gather_cols(const uint16_t* X, int64_t ldx, int M, int K, const int32_t* perm,
+// meta_pref: kMetaGroup for sorted rows (needs G % 32 == 0), otherwise a
+// per-row mode; operand: an Operand. Returns false when no decode kernel
+// covers the request (for kOperandGather: the gather does not fit in LDS, the
+// caller then runs launch_gather_prep and plans with kOperandPrepared).
+bool plan_decode(int M, int K, int N, int G, int num_groups, int layout, int meta_pref, int operand,
+                 DecodePlan* p);
+hipError_t launch_decode(const GemmArgs& a, const DecodePlan& p, hipStream_t s);
+// Xp [M][K] = X[:, perm] (perm may be NULL), each octet in operand order.
+hipError_t launch_gather_prep(const uint16_t* X, int64_t ldx, int M, int K, const int32_t* perm,
                               uint16_t* Xp, hipStream_t s);
 
 // Reorder (device code in reorder.hip).
@@ -67,9 +98,13 @@ struct ReorderLayer {
 hipError_t launch_fill_u32(uint32_t* p, size_t n, uint32_t v, hipStream_t s);
 hipError_t launch_gidx_validate(const ReorderLayer& L, uint32_t* counts, uint32_t* flag, hipStream_t s);
 hipError_t launch_gidx_rank(const ReorderLayer& L, hipStream_t s);
+// dst = src[Prow, Pcol] (either permutation may be NULL = identity), src in
+// GPTQ layout, dst dense in dst_layout.
 hipError_t launch_permute_qweight(const uint32_t* src, int64_t ld_src, int K, int N,
                                   const int32_t* Prow, const int32_t* Pcol, uint32_t* dst,
-                                  hipStream_t s);
+                                  int dst_layout, hipStream_t s);
+// words per 16-column tile of a dense tiled qweight with K rows
+__host__ __device__ inline int64_t tiled_ld(int K) { return (int64_t)((K + 127) / 128) * 256; }
 hipError_t launch_permute_scales(const uint16_t* src, int64_t ld_src, int ng, int N,
                                  const int32_t* Pcol, uint16_t* dst, hipStream_t s);
 hipError_t launch_permute_qzeros(const uint32_t* src, int64_t ld_src, int ng, int N,

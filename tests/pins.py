@@ -356,10 +356,39 @@ def pin_distinct_groups(o, seed=13):
     assert np.all(o.distinct_groups_per_tile(gs, T) == 1)
 
 
+def pin_tiled_layout(o):
+    """The tiled storage order on a value-equals-address example: with
+    GPTQ word [r][c] = 16 r + c (K = 256, N = 32), the word a lane finds at
+    tiled[t][256 b + 4 l + u] must be the one for row 4 (4 b + u) + l // 16
+    and column 16 t + l % 16, worked out here by walking the lanes; and the
+    round trip is the identity for a ragged shape (padding is zero)."""
+    K, N = 256, 32
+    qw = (16 * np.arange(K // 8)[:, None] + np.arange(N)[None, :]).astype(np.int32)
+    qt = o.tile(qw)
+    assert qt.shape == (2, 512)
+    for t in range(2):
+        for b in range(2):
+            for lane in range(64):
+                for u in range(4):
+                    row = 4 * (4 * b + u) + lane // 16
+                    colm = 16 * t + lane % 16
+                    assert qt[t, 256 * b + 4 * lane + u] == 16 * row + colm
+    assert np.array_equal(o.untile(qt, K, N), qw)
+    w1, _ = inputs.make_custom(160, 24, 0, 32, 14)          # K % 128 != 0, N % 16 != 0
+    qt2 = o.tile(w1.qweight)
+    assert qt2.shape == (2, 512)
+    assert np.array_equal(o.untile(qt2, 160, 24), w1.qweight)
+    used = np.zeros(qt2.shape, bool)
+    r = np.arange(20)[:, None]
+    c = np.arange(24)[None, :]
+    used[c // 16, 256 * ((r // 4) // 4) + 4 * (16 * (r % 4) + c % 16) + (r // 4) % 4] = True
+    assert np.all(qt2.view(np.uint32)[~used] == 0)
+
+
 ALL_PINS = [
     pin_unpack_bruteforce, pin_pack_roundtrip, pin_golden_gemm_codes, pin_worked_reorder,
     pin_reorder_closed_form, pin_identity_phi, pin_check_groups, pin_golden_gemm,
     pin_gemm_bruteforce, pin_one_hot_rows, pin_special_cases, pin_ordered_equals_actorder,
     pin_tp_aware_mlp, pin_actorder_shard_mlp, pin_alg2_equals_alg3, pin_fold_elementwise,
-    pin_distinct_groups,
+    pin_distinct_groups, pin_tiled_layout,
 ]

@@ -77,11 +77,12 @@ def test_gemm_validation(lib):
     bad = fake_layer()
     bad.qweight += 4
     assert gemm(lib, bad) == _abi.ERR_ALIGN
-    assert gemm(lib, w, path=_abi.PATH_ACTORDER, ws=None) == _abi.ERR_WORKSPACE
+    assert gemm(lib, w, perm=1 << 27, ws=None) == _abi.ERR_WORKSPACE        # a gather needs workspace
     nog = fake_layer(gidx=False)
     assert gemm(lib, nog, path=_abi.PATH_ACTORDER) == _abi.ERR_NULL          # act-order needs g_idx
     assert gemm(lib, w, dtype=_abi.BF16) == _abi.ERR_UNSUPPORTED
     assert gemm(lib, w, path=7) == _abi.ERR_SHAPE
+    assert gemm(lib, nog, path=_abi.PATH_ACTORDER_GLOBAL) == _abi.ERR_NULL
     need = lib.tpdq_workspace_bytes(_abi.OP_GEMM, 4, ctypes.byref(w), None)
     assert need > 0
     # the query covers the gathered-activation buffer, so ask with a gather
@@ -108,9 +109,9 @@ def test_reorder_validation(lib):
     w1 = fake_layer(K=256, N=512)
     w2 = fake_layer(K=512, N=128, base=1 << 22)
     p = 1 << 27
-    args = lambda a, b, P2=None, ws=None, nb=0: (
+    args = lambda a, b, P2=None, ws=None, nb=0, lay=_abi.LAYOUT_TILED: (
         ctypes.byref(a), ctypes.byref(b) if b is not None else None, p, p, P2, P2 and p, p, p, p,
-        P2 and p, _abi.FP16, ws, nb, None)
+        P2 and p, _abi.FP16, lay, ws, nb, None)
     assert lib.tpdq_reorder(*args(w1, None, P2=p)) == _abi.ERR_SHAPE         # P2 without w2
     assert lib.tpdq_reorder(*args(w1, w2)) == _abi.ERR_NULL                   # w2 without P2
     nog = fake_layer(K=256, N=512, gidx=False)
@@ -118,6 +119,28 @@ def test_reorder_validation(lib):
     shard = fake_layer(K=256, N=512, ng=64)
     assert lib.tpdq_reorder(*args(shard, None)) == _abi.ERR_SHAPE            # not a global layer
     assert lib.tpdq_reorder(*args(w1, w2, P2=p)) == _abi.ERR_WORKSPACE
+    assert lib.tpdq_reorder(*args(w1, w2, P2=p, lay=5)) == _abi.ERR_SHAPE    # unknown layout
+    tiled_in = fake_layer(K=256, N=512)
+    tiled_in.layout = _abi.LAYOUT_TILED
+    tiled_in.ld_q = 512
+    assert lib.tpdq_reorder(*args(tiled_in, None)) == _abi.ERR_SHAPE         # inputs are GPTQ
+
+
+@needs_no_gpu
+def test_tiled_layout_validation(lib):
+    w = fake_layer(K=256, N=64)
+    w.layout = _abi.LAYOUT_TILED
+    w.ld_q = 256            # < ceil(256/128)*256 = 512
+    assert gemm(lib, w, perm=1 << 27) == _abi.ERR_SHAPE
+    w.layout = 3
+    w.ld_q = 512
+    assert gemm(lib, w, perm=1 << 27) == _abi.ERR_SHAPE
+    g = fake_layer(K=256, N=64)
+    assert lib.tpdq_pack_tiled(ctypes.byref(g), None, None) == _abi.ERR_NULL
+    g.layout = _abi.LAYOUT_TILED
+    assert lib.tpdq_pack_tiled(ctypes.byref(g), 1 << 27, None) == _abi.ERR_SHAPE
+    g = fake_layer(K=256, N=60)
+    assert lib.tpdq_pack_tiled(ctypes.byref(g), 1 << 27, None) == _abi.ERR_SHAPE
 
 
 def test_workspace_sizes(lib):
@@ -128,8 +151,8 @@ def test_workspace_sizes(lib):
         m = lib.tpdq_workspace_bytes(_abi.OP_MLP, M, ctypes.byref(w1), ctypes.byref(w2))
         assert g > 0 and m >= g
         assert m % 256 == 0
-        # the gathered activations must fit
-        assert m >= M * 8192 * 2
+        # the gathered activations of one launch (at most 64 rows) must fit
+        assert m >= min(M, 64) * 8192 * 2
     r = lib.tpdq_workspace_bytes(_abi.OP_REORDER, 0, ctypes.byref(w1), ctypes.byref(w2))
     assert r >= 4 * (64 + 28)
     assert lib.tpdq_workspace_bytes(_abi.OP_MLP, 4, ctypes.byref(w1), None) == 0

@@ -9,9 +9,10 @@ from tests.gpu_util import (TOL_FP16, layer_to_dev, log, np_of, sample_cols, to_
 
 pytestmark = pytest.mark.gpu
 
-SHAPES = [  # K, N, G: config-0 size, ragged N and K, several tiles, small G (row-metadata kernel)
+SHAPES = [  # K, N, G: config-0 size, ragged N and K, several tiles, small G (row-metadata kernel),
+    # groups of 256 rows that span two 128-row blocks, split between waves
     (256, 128, 32), (288, 200, 32), (1024, 520, 128), (128, 72, 8), (192, 64, 64), (40, 24, 8),
-    (2048, 1032, 128),
+    (2048, 1032, 128), (768, 48, 256), (2304, 96, 256),
 ]
 MS = [1, 4, 16, 17, 64, 65]
 
@@ -22,14 +23,19 @@ def _d(layer):
 
 @pytest.mark.parametrize("K,N,G", SHAPES)
 @pytest.mark.parametrize("M", MS)
-def test_gemm_actorder(K, N, G, M):
+@pytest.mark.parametrize("variant", ["lds", "global", "lds-tiled"])
+def test_gemm_actorder(K, N, G, M, variant):
     import torch
     import paper_2402_04925_amd as tpdq
     dev = torch_dev()
-    log(f"gemm actorder K={K} N={N} G={G} M={M}")
+    path = tpdq.PATH_ACTORDER_GLOBAL if variant == "global" else tpdq.PATH_ACTORDER
+    log(f"gemm actorder-{variant} K={K} N={N} G={G} M={M}")
     w1, _ = inputs.make_custom(K, N, 0, G, seed=K + N + G)
     X = inputs.random_activations(M, K, np.random.default_rng(M))
-    Y = tpdq.w4a16_gemm(to_dev(X, dev), layer_to_dev(w1, dev), tpdq.PATH_ACTORDER)
+    dw = layer_to_dev(w1, dev)
+    if variant == "lds-tiled":
+        dw = tpdq.pack_tiled(dw)
+    Y = tpdq.w4a16_gemm(to_dev(X, dev), dw, path)
     torch.cuda.synchronize()
     ref = o.w4a16_gemm(X, w1.qweight, w1.scales, w1.qzeros, w1.g_idx)
     assert o.rel_err(np_of(Y), ref) <= TOL_FP16
@@ -37,16 +43,18 @@ def test_gemm_actorder(K, N, G, M):
 
 @pytest.mark.parametrize("K,N,G", SHAPES)
 @pytest.mark.parametrize("M", MS)
-def test_gemm_ordered(K, N, G, M):
+@pytest.mark.parametrize("layout", ["tiled", "gptq"])
+def test_gemm_ordered(K, N, G, M, layout):
     """Sorted rows from the GPU reorder, the activation gather X[:, P] in the
     call; equal to the act-order product by the reorder invariant."""
     import torch
     import paper_2402_04925_amd as tpdq
     dev = torch_dev()
-    log(f"gemm ordered K={K} N={N} G={G} M={M}")
+    log(f"gemm ordered K={K} N={N} G={G} M={M} {layout}")
     w1, _ = inputs.make_custom(K, N, 0, G, seed=K + N + G)
     X = inputs.random_activations(M, K, np.random.default_rng(M))
-    P, gs, _, _, wo, _ = tpdq.reorder(layer_to_dev(w1, dev))
+    lay = tpdq.LAYOUT_TILED if layout == "tiled" else tpdq.LAYOUT_GPTQ
+    P, gs, _, _, wo, _ = tpdq.reorder(layer_to_dev(w1, dev), layout=lay)
     Xd = to_dev(X, dev)
     Y = tpdq.w4a16_gemm(Xd, wo, tpdq.PATH_ORDERED, x_perm=P)
     torch.cuda.synchronize()
@@ -145,6 +153,12 @@ def test_gemm_full_size_shards(name, which, M):
     Y = tpdq.w4a16_gemm(Xd, sh, tpdq.PATH_ACTORDER)
     torch.cuda.synchronize()
     assert o.rel_err(np_of(Y)[:, cols], ref) <= TOL_FP16
+    # act-order on the tiled storage order
+    dlt = tpdq.pack_tiled(dl)
+    sht = dlt.column_shard(0, w.tp) if which == 1 else dlt.row_shard(0, w.tp, sorted_rows=False)
+    Yt = tpdq.w4a16_gemm(Xd, sht, tpdq.PATH_ACTORDER)
+    torch.cuda.synchronize()
+    assert o.rel_err(np_of(Yt)[:, cols], ref) <= TOL_FP16
     # ordered: the reordered global layer, same shard position
     P, gs, _, _, wo, _ = tpdq.reorder(dl)
     eP, eg = o.reorder(L.g_idx)
@@ -159,3 +173,27 @@ def test_gemm_full_size_shards(name, which, M):
         refo = o.to_fp16(o.matmul(X, Wd))
     torch.cuda.synchronize()
     assert o.rel_err(np_of(Yo)[:, cols], refo) <= TOL_FP16
+
+
+def test_gemm_interleaved_shapes_share_workspace():
+    """Calls of different shapes and paths, one after another on one stream and
+    one workspace, each equal to its own oracle result."""
+    import torch
+    import paper_2402_04925_amd as tpdq
+    dev = torch_dev()
+    ws = tpdq.Workspace(dev)
+    cases = [(256, 64, 32, 3), (2048, 3584, 128, 16), (512, 1032, 64, 1), (2048, 512, 128, 40)]
+    outs = []
+    for K, N, G, M in cases * 2:
+        w1, _ = inputs.make_custom(K, N, 0, G, seed=K + N)
+        X = inputs.random_activations(M, K, np.random.default_rng(K))
+        dw = layer_to_dev(w1, dev)
+        P, _, _, _, wo, _ = tpdq.reorder(dw, workspace=ws)
+        Yo = tpdq.w4a16_gemm(to_dev(X, dev), wo, tpdq.PATH_ORDERED, x_perm=P, workspace=ws)
+        Ya = tpdq.w4a16_gemm(to_dev(X, dev), dw, tpdq.PATH_ACTORDER, workspace=ws)
+        outs.append((X, w1, Yo, Ya))
+    torch.cuda.synchronize()
+    for X, w1, Yo, Ya in outs:
+        ref = o.w4a16_gemm(X, w1.qweight, w1.scales, w1.qzeros, w1.g_idx)
+        assert o.rel_err(np_of(Yo), ref) <= TOL_FP16
+        assert o.rel_err(np_of(Ya), ref) <= TOL_FP16

@@ -14,12 +14,12 @@ def _l(layer):
     return (layer.qweight, layer.scales, layer.qzeros, layer.g_idx)
 
 
-def _run_rank(tpdq, X, d1, d2, P1, w1o, w2o, rank, tp, ordered):
+def _run_rank(tpdq, X, d1, d2, P1, w1o, w2o, rank, tp, ordered, path=None):
     if ordered:
         return tpdq.mlp_shard(X, w1o.column_shard(rank, tp), w2o.row_shard(rank, tp, True),
                               tpdq.PATH_ORDERED, P1=P1)
     return tpdq.mlp_shard(X, d1.column_shard(rank, tp), d2.row_shard(rank, tp, False),
-                          tpdq.PATH_ACTORDER)
+                          tpdq.PATH_ACTORDER if path is None else path)
 
 
 @pytest.mark.parametrize("tp", [1, 2, 4])
@@ -72,9 +72,16 @@ def test_mlp_full_size(name, M):
     eP2, _ = o.reorder(w2.g_idx)
     cols = sample_cols(w.N2, np.random.default_rng(M))
     Xd = to_dev(X, dev)
-    for ordered in (False, True):
-        y1, y2 = _run_rank(tpdq, Xd, d1, d2, P1, w1o, w2o, 0, w.tp, ordered)
+    t1, t2 = tpdq.pack_tiled(d1), tpdq.pack_tiled(d2)
+    e_act = o.mlp_rank_from_global(X, _l(w1), _l(w2), 0, w.tp, False, P2=eP2, cols2=cols)
+    e_ord = o.mlp_rank_from_global(X, _l(w1), _l(w2), 0, w.tp, True, P2=eP2, cols2=cols)
+    for name, ordered, a1, a2, path in (
+            ("actorder", False, d1, d2, tpdq.PATH_ACTORDER),
+            ("actorder-global", False, d1, d2, tpdq.PATH_ACTORDER_GLOBAL),
+            ("actorder-tiled", False, t1, t2, tpdq.PATH_ACTORDER),
+            ("ordered", True, d1, d2, None)):
+        y1, y2 = _run_rank(tpdq, Xd, a1, a2, P1, w1o, w2o, 0, w.tp, ordered, path)
         torch.cuda.synchronize()
-        e1, e2 = o.mlp_rank_from_global(X, _l(w1), _l(w2), 0, w.tp, ordered, P2=eP2, cols2=cols)
-        assert o.rel_err(np_of(y1), e1) <= TOL_FP16, ordered
-        assert o.rel_err(np_of(y2)[:, cols], e2) <= TOL_FP16, ordered
+        e1, e2 = e_ord if ordered else e_act
+        assert o.rel_err(np_of(y1), e1) <= TOL_FP16, name
+        assert o.rel_err(np_of(y2)[:, cols], e2) <= TOL_FP16, name

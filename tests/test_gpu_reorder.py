@@ -14,27 +14,50 @@ def _d(layer):
     return dict(qweight=layer.qweight, scales=layer.scales, qzeros=layer.qzeros)
 
 
+def words_of(w):
+    """GPTQ words of a device QuantWeight, whatever its layout."""
+    import paper_2402_04925_amd as tpdq
+    q = np_of(w.qweight)
+    return o.untile(q, w.K, w.N) if w.layout == tpdq.LAYOUT_TILED else q
+
+
 @pytest.mark.parametrize("K1,N1,N2,G,seed", [
     (256, 512, 128, 32, 1), (64, 128, 64, 8, 2), (512, 256, 200, 64, 3), (384, 640, 72, 128, 4),
-    (256, 256, 128, 256, 5),
+    (256, 256, 128, 256, 5), (160, 32, 40, 32, 6),
 ])
-def test_reorder_pair_exact(K1, N1, N2, G, seed):
+@pytest.mark.parametrize("layout", ["gptq", "tiled"])
+def test_reorder_pair_exact(K1, N1, N2, G, seed, layout):
     import torch
     import paper_2402_04925_amd as tpdq
     dev = torch_dev()
-    log(f"reorder pair K1={K1} N1={N1} N2={N2} G={G}")
+    lay = tpdq.LAYOUT_TILED if layout == "tiled" else tpdq.LAYOUT_GPTQ
+    log(f"reorder pair K1={K1} N1={N1} N2={N2} G={G} {layout}")
     w1, w2 = inputs.make_custom(K1, N1, N2, G, seed)
-    P1, g1, P2, g2, w1o, w2o = tpdq.reorder(layer_to_dev(w1, dev), layer_to_dev(w2, dev))
+    P1, g1, P2, g2, w1o, w2o = tpdq.reorder(layer_to_dev(w1, dev), layer_to_dev(w2, dev), layout=lay)
     torch.cuda.synchronize()
     eP1, eg1 = o.reorder(w1.g_idx)
     eP2, eg2 = o.reorder(w2.g_idx)
     f1, f2 = o.fold(_d(w1), _d(w2), eP1, eP2)
     assert np.array_equal(np_of(P1), eP1) and np.array_equal(np_of(g1), eg1)
     assert np.array_equal(np_of(P2), eP2) and np.array_equal(np_of(g2), eg2)
-    assert np.array_equal(np_of(w1o.qweight), f1["qweight"])
+    assert np.array_equal(words_of(w1o), f1["qweight"])
     assert np.array_equal(np_of(w1o.scales), f1["scales"])
     assert np.array_equal(np_of(w1o.qzeros), f1["qzeros"])
-    assert np.array_equal(np_of(w2o.qweight), f2["qweight"])
+    assert np.array_equal(words_of(w2o), f2["qweight"])
+    if layout == "tiled":   # the padding past K and N is zero
+        assert np.array_equal(np_of(w1o.qweight), o.tile(f1["qweight"]))
+        assert np.array_equal(np_of(w2o.qweight), o.tile(f2["qweight"]))
+
+
+@pytest.mark.parametrize("K,N,seed", [(256, 64, 1), (160, 24, 2), (1024, 1000, 3)])
+def test_pack_tiled_exact(K, N, seed):
+    import torch
+    import paper_2402_04925_amd as tpdq
+    dev = torch_dev()
+    w1, _ = inputs.make_custom(K, N, 0, 32, seed)
+    wt = tpdq.pack_tiled(layer_to_dev(w1, dev))
+    torch.cuda.synchronize()
+    assert np.array_equal(np_of(wt.qweight), o.tile(w1.qweight))
 
 
 @pytest.mark.parametrize("K,N,G,seed", [(256, 128, 32, 7), (1024, 96, 128, 8), (40, 16, 8, 9)])
@@ -44,7 +67,7 @@ def test_reorder_single_exact(K, N, G, seed):
     dev = torch_dev()
     log(f"reorder single K={K} N={N} G={G}")
     w1, _ = inputs.make_custom(K, N, 0, G, seed)
-    P1, g1, P2, g2, w1o, w2o = tpdq.reorder(layer_to_dev(w1, dev))
+    P1, g1, P2, g2, w1o, w2o = tpdq.reorder(layer_to_dev(w1, dev), layout=tpdq.LAYOUT_GPTQ)
     torch.cuda.synchronize()
     assert P2 is None and w2o is None
     eP, eg = o.reorder(w1.g_idx)
@@ -61,7 +84,8 @@ def test_reorder_identity_phi():
     import paper_2402_04925_amd as tpdq
     dev = torch_dev()
     w1, w2 = inputs.make_custom(256, 256, 64, 32, 11, identity_phi=True)
-    P1, g1, P2, g2, w1o, w2o = tpdq.reorder(layer_to_dev(w1, dev), layer_to_dev(w2, dev))
+    P1, g1, P2, g2, w1o, w2o = tpdq.reorder(layer_to_dev(w1, dev), layer_to_dev(w2, dev),
+                                            layout=tpdq.LAYOUT_GPTQ)
     torch.cuda.synchronize()
     assert np.array_equal(np_of(P1), np.arange(256)) and np.array_equal(np_of(P2), np.arange(256))
     assert np.array_equal(np_of(w1o.qweight), w1.qweight)
@@ -96,7 +120,8 @@ def test_reorder_full_size(name):
     w = inputs.WORKLOADS[name]
     log(f"reorder full {name}")
     w1, w2 = inputs.make_workload(w)
-    P1, g1, P2, g2, w1o, w2o = tpdq.reorder(layer_to_dev(w1, dev), layer_to_dev(w2, dev))
+    d1, d2 = layer_to_dev(w1, dev), layer_to_dev(w2, dev)
+    P1, g1, P2, g2, w1o, w2o = tpdq.reorder(d1, d2, layout=tpdq.LAYOUT_GPTQ)
     torch.cuda.synchronize()
     eP1, eg1 = o.reorder(w1.g_idx)
     eP2, eg2 = o.reorder(w2.g_idx)
@@ -118,3 +143,15 @@ def test_reorder_full_size(name):
     cols2 = np.arange(w.N2)
     exp2 = o.fold_sample(w2.qweight, eP2, None, np.concatenate([8 * r + np.arange(8) for r in rows_w2]), cols2)
     assert np.array_equal(got2, exp2)
+
+    # tiled output: sampled 16-column tiles, all rows
+    _, _, _, _, w1t, w2t = tpdq.reorder(d1, d2, layout=tpdq.LAYOUT_TILED)
+    torch.cuda.synchronize()
+    for t in (0, 7, w.N1 // 16 - 1):
+        got = o.untile(np_of(w1t.qweight[t:t + 1]), w.K1, 16)
+        exp = o.fold_sample(w1.qweight, eP1, eP2, np.arange(w.K1), np.arange(16 * t, 16 * t + 16))
+        assert np.array_equal(o.unpack_rows(got), exp), t
+    for t in (0, w.N2 // 16 - 1):
+        got = o.untile(np_of(w2t.qweight[t:t + 1]), w.K2, 16)
+        exp = o.fold_sample(w2.qweight, eP2, None, np.arange(w.K2), np.arange(16 * t, 16 * t + 16))
+        assert np.array_equal(o.unpack_rows(got), exp), t
