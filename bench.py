@@ -195,6 +195,119 @@ def cpu_baseline(wl, M, L1, L2, budget_s=20.0):
                        f"ordered, float64 dequant + GEMM), median")
 
 
+class Calls:
+    """Library calls of one batch size M on the rank-0 shards: the MLP shard
+    and each GEMM on its own, for every path, one closure per weight replica."""
+
+    PAIRS = {"ordered": (0, 1), "actorder": (2, 3), "actorder_global": (2, 3), "actorder_tiled": (4, 5)}
+
+    def __init__(self, st, M, dev):
+        import torch
+        import paper_2402_04925_amd as tpdq
+        from paper_2402_04925_amd import inputs
+        wl = st.wl
+        self.st, self.M, self.dev = st, M, dev
+        self.tpdq = tpdq
+        self.lib = tpdq._abi.lib()
+        self.X = torch.from_numpy(inputs.make_x(wl, M)).to(dev)
+        self.y1 = torch.empty(M, wl.N1 // wl.tp, dtype=torch.float16, device=dev)
+        self.y2 = torch.empty(M, wl.N2, dtype=torch.float16, device=dev)
+        self.xg = self.X[:, st.P1.long()].contiguous()   # X[:, P1] for the single-GEMM timings
+        self.ws = tpdq.Workspace(dev)
+        self.paths = {"ordered": tpdq.PATH_ORDERED, "actorder": tpdq.PATH_ACTORDER,
+                      "actorder_global": tpdq.PATH_ACTORDER_GLOBAL,
+                      "actorder_tiled": tpdq.PATH_ACTORDER}
+
+    def _stream(self):
+        import torch
+        return torch.cuda.current_stream(self.dev).cuda_stream
+
+    def mlp(self, rep, pname):
+        import ctypes
+        tpdq, lib, M = self.tpdq, self.lib, self.M
+        path = self.paths[pname]
+        i1, i2 = self.PAIRS[pname]
+        c1, c2 = rep[i1].c_struct(), rep[i2].c_struct()
+        nb = lib.tpdq_workspace_bytes(tpdq.OP_MLP, M, ctypes.byref(c1), ctypes.byref(c2))
+        buf = self.ws.get(nb)
+        P1 = self.st.P1.data_ptr() if path == tpdq.PATH_ORDERED else None
+        X, y1, y2 = self.X, self.y1, self.y2
+
+        def call():
+            tpdq._abi.check(lib.tpdq_mlp_shard(
+                X.data_ptr(), X.stride(0), M, P1, ctypes.byref(c1), ctypes.byref(c2), path,
+                tpdq.FP16, y1.data_ptr(), y2.data_ptr(), buf.data_ptr(), buf.numel(), self._stream()))
+        return call
+
+    def gemm(self, rep, which, pname):
+        import ctypes
+        tpdq, lib, M = self.tpdq, self.lib, self.M
+        path = self.paths[pname]
+        c = rep[self.PAIRS[pname][which]].c_struct()
+        nb = lib.tpdq_workspace_bytes(tpdq.OP_GEMM, M, ctypes.byref(c), None)
+        buf = self.ws.get(nb)
+        xin = (self.xg if path == tpdq.PATH_ORDERED else self.X) if which == 0 else self.y1
+        out = self.y1 if which == 0 else self.y2
+
+        def call():
+            tpdq._abi.check(lib.tpdq_w4a16_gemm(
+                xin.data_ptr(), xin.stride(0), M, None, ctypes.byref(c), path, tpdq.FP16,
+                out.data_ptr(), out.stride(0), buf.data_ptr(), buf.numel(), self._stream()))
+        return call
+
+
+COPY_BYTES = 1 << 30
+
+
+def copy_ceiling(dev, reps=10):
+    """Plain device copy (torch's copy kernel) of 1 GiB: read + write GB/s.
+    Context for the roofline fraction; also the calibration kernel of the HBM
+    traffic counters."""
+    import torch
+    src = torch.empty(COPY_BYTES // 2, dtype=torch.float16, device=dev).fill_(1.0)
+    dst = torch.empty_like(src)
+    dst.copy_(src)
+    torch.cuda.synchronize()
+    cur = torch.cuda.current_stream(dev)
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    e0.record(cur)
+    for _ in range(reps):
+        dst.copy_(src)
+    e1.record(cur)
+    torch.cuda.synchronize()
+    sec = e0.elapsed_time(e1) / 1e3 / reps
+    del src, dst
+    return 2 * COPY_BYTES / sec / 1e9
+
+
+def profile_run(st, Ms, launches, dev):
+    """Eager launches for rocprofv3 (kernel trace or counters): every path's
+    GEMM1 and GEMM2 and the ordered MLP shard at each M, `launches` times
+    each over the rotating replicas, then the 1 GiB copy kernel."""
+    import torch
+    for M in Ms:
+        c = Calls(st, M, dev)
+        for pname in ("ordered", "actorder", "actorder_global", "actorder_tiled"):
+            for which in (0, 1):
+                fns = [c.gemm(rep, which, pname) for rep in st.reps]
+                for i in range(launches):
+                    fns[i % len(fns)]()
+                torch.cuda.synchronize()
+                eprint(f"[profile] M={M} {pname} gemm{which + 1}: {launches} launches")
+        fns = [c.mlp(rep, "ordered") for rep in st.reps]
+        for i in range(launches):
+            fns[i % len(fns)]()
+        torch.cuda.synchronize()
+        eprint(f"[profile] M={M} ordered mlp: {launches} launches")
+    src = torch.empty(COPY_BYTES // 2, dtype=torch.float16, device=dev).fill_(1.0)
+    dst = torch.empty_like(src)
+    for _ in range(launches):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    eprint(f"[profile] copy of {COPY_BYTES} bytes: {launches} launches")
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -204,6 +317,8 @@ def main():
     ap.add_argument("--M", type=int, default=16)
     ap.add_argument("--sweep", default="1,4,16", help="extra batch sizes reported alongside")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--profile-run", action="store_true",
+                    help="eager launches for rocprofv3 (kernel trace or counters); no JSON")
     args = ap.parse_args()
 
     if args.gpus != 1:
@@ -213,7 +328,6 @@ def main():
         sys.exit(2)
 
     import torch
-    import paper_2402_04925_amd as tpdq
     from paper_2402_04925_amd import inputs
 
     if not torch.cuda.is_available():
@@ -222,65 +336,26 @@ def main():
     dev = torch.device("cuda:0")
     wl = inputs.WORKLOADS[args.workload]
     st = Setup(wl, dev)
-    lib = tpdq._abi.lib()
-    import ctypes
+    Ms = sorted(set([args.M] + [int(m) for m in args.sweep.split(",") if m]))
+    if args.profile_run:
+        profile_run(st, Ms, args.steps, dev)
+        return
 
     results = {}
-    Ms = sorted(set([args.M] + [int(m) for m in args.sweep.split(",") if m]))
     for M in Ms:
-        X = torch.from_numpy(inputs.make_x(wl, M)).to(dev)
-        N1 = wl.N1 // wl.tp
-        K2 = wl.K2 // wl.tp
-        y1 = torch.empty(M, N1, dtype=torch.float16, device=dev)
-        y2 = torch.empty(M, wl.N2, dtype=torch.float16, device=dev)
-        xg = X[:, st.P1.long()].contiguous()   # X[:, P1] for the single-GEMM timings
-        ws = tpdq.Workspace(dev)
-
-        PAIRS = {"ordered": (0, 1), "actorder": (2, 3), "actorder_global": (2, 3), "actorder_tiled": (4, 5)}
-
-        def mk_mlp(rep, pname, path):
-            i1, i2 = PAIRS[pname]
-            w1, w2 = rep[i1], rep[i2]
-            c1, c2 = w1.c_struct(), w2.c_struct()
-            nb = lib.tpdq_workspace_bytes(tpdq.OP_MLP, M, ctypes.byref(c1), ctypes.byref(c2))
-            buf = ws.get(nb)
-            P1 = st.P1.data_ptr() if path == tpdq.PATH_ORDERED else None
-            keep = (c1, c2)
-
-            def call():
-                tpdq._abi.check(lib.tpdq_mlp_shard(
-                    X.data_ptr(), X.stride(0), M, P1, ctypes.byref(keep[0]), ctypes.byref(keep[1]),
-                    path, tpdq.FP16, y1.data_ptr(), y2.data_ptr(), buf.data_ptr(), buf.numel(),
-                    torch.cuda.current_stream(dev).cuda_stream))
-            return call
-
-        def mk_gemm(rep, which, pname, path):
-            w = rep[PAIRS[pname][which]]
-            c = w.c_struct()
-            nb = lib.tpdq_workspace_bytes(tpdq.OP_GEMM, M, ctypes.byref(c), None)
-            buf = ws.get(nb)
-            xin = (xg if path == tpdq.PATH_ORDERED else X) if which == 0 else y1
-            out = y1 if which == 0 else y2
-
-            def call():
-                tpdq._abi.check(lib.tpdq_w4a16_gemm(
-                    xin.data_ptr(), xin.stride(0), M, None, ctypes.byref(c), path, tpdq.FP16,
-                    out.data_ptr(), out.stride(0), buf.data_ptr(), buf.numel(),
-                    torch.cuda.current_stream(dev).cuda_stream))
-            return call
-
+        c = Calls(st, M, dev)
         r = {}
-        for pname, path in (("ordered", tpdq.PATH_ORDERED), ("actorder", tpdq.PATH_ACTORDER),
-                            ("actorder_global", tpdq.PATH_ACTORDER_GLOBAL),
-                            ("actorder_tiled", tpdq.PATH_ACTORDER)):
-            ms, _ = capture_and_time([mk_mlp(rep, pname, path) for rep in st.reps], args.steps,
+        for pname in ("ordered", "actorder", "actorder_global", "actorder_tiled"):
+            ms, _ = capture_and_time([c.mlp(rep, pname) for rep in st.reps], args.steps,
                                      args.warmup, dev)
-            g1, _ = capture_and_time([mk_gemm(rep, 0, pname, path) for rep in st.reps], args.steps,
+            g1, _ = capture_and_time([c.gemm(rep, 0, pname) for rep in st.reps], args.steps,
                                      args.warmup, dev)
-            g2, _ = capture_and_time([mk_gemm(rep, 1, pname, path) for rep in st.reps], args.steps,
+            g2, _ = capture_and_time([c.gemm(rep, 1, pname) for rep in st.reps], args.steps,
                                      args.warmup, dev)
             r[pname] = dict(mlp_us=ms * 1e3, gemm1_us=g1 * 1e3, gemm2_us=g2 * 1e3)
             eprint(f"[bench] M={M} {pname}: mlp {ms*1e3:.2f} us, gemm1 {g1*1e3:.2f} us, gemm2 {g2*1e3:.2f} us")
+        N1 = wl.N1 // wl.tp
+        K2 = wl.K2 // wl.tp
         ng2_act = wl.K2 // wl.G
         b1 = gemm_bytes(M, wl.K1, N1, wl.G)
         b2 = gemm_bytes(M, K2, wl.N2, wl.G)
@@ -291,7 +366,10 @@ def main():
         r["bytes"] = dict(gemm1=b1, gemm2=b2, mlp=b_mlp, gemm1_actorder=b1a, gemm2_actorder=b2a)
         r["flops"] = flops
         results[M] = r
+        del c
         torch.cuda.synchronize()
+    copy_gbs = copy_ceiling(dev)
+    eprint(f"[bench] 1 GiB device copy: {copy_gbs:.0f} GB/s (read + write)")
 
     M = args.M
     r = results[M]
@@ -344,7 +422,10 @@ def main():
         hbm_frac=round(b["mlp"] / (mlp_us * 1e-6) / 1e9 / HBM_PEAK_GBS, 4),
         tflops=round(r["flops"] / (mlp_us * 1e-6) / 1e12, 3),
         speedup_vs_actorder=round(r["actorder"]["mlp_us"] / mlp_us, 3),
-        roofline=roof, cpu_baseline=cpu, sweep=sweep,
+        roofline=roof, cpu_baseline=cpu,
+        copy_1gib_gbs=round(copy_gbs, 1),
+        roofline_frac_of_copy=round(achieved / copy_gbs, 4),
+        sweep=sweep,
         paper_context="paper: up to 1.81x (Llama-70B) / 1.78x (Granite-20B) Alg. 3 vs Alg. 2 on "
                       "A100/H100 DGX, multi-GPU, communication included; not comparable",
     )

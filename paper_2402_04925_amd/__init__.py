@@ -122,7 +122,8 @@ class QuantWeight:
         if self.layout == LAYOUT_TILED:
             if r0 % 128:
                 raise ValueError("a tiled row shard must start on a 128-row block")
-            qw = self.qweight[:, (r0 // 128) * 256:]
+            c0 = (r0 // 128) * 256
+            qw = self.qweight[:, c0:min(c0 + tiled_ld(k), self.qweight.shape[1])]
         else:
             qw = self.qweight[r0 // 8:(r0 + k) // 8]
         g = None if self.g_idx is None else self.g_idx[r0:r0 + k]
