@@ -381,7 +381,7 @@ def main():
     traffic = read_traffic(wl.name, M)
     roof = dict(bound="hbm", achieved=round(achieved, 1), peak=HBM_PEAK_GBS, unit="GB/s",
                 frac=round(achieved / HBM_PEAK_GBS, 4), traffic=traffic,
-                kernel="k_decode_ordered (GEMM1 and GEMM2 launches averaged)")
+                kernel="k_ordered (its GEMM1 and GEMM2 launches averaged)")
     cpu = None
     if not args.no_cpu_baseline:
         cpu = cpu_baseline(wl, M, st.L1, st.L2)
