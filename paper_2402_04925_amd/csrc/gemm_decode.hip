@@ -114,6 +114,16 @@ __device__ __forceinline__ u4_t permute_octet(u4_t x) {
   return r;
 }
 
+// s_waitcnt vmcnt(N) alone (expcnt and lgkmcnt at their maxima). Placed
+// where the N most recent vector-memory loads may stay in flight while all
+// older ones must have landed; it also tells the compiler's wait-count pass
+// that the older loads are done on every path.
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt is 6 bits");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (0x7 << 4) | (0xF << 8));
+}
+
 __device__ __forceinline__ f4_t mfma16x16x32(h8_t a, h8_t b, f4_t c) {
   return __builtin_amdgcn_mfma_f32_16x16x32_f16(a, b, c, 0, 0, 0);
 }
@@ -142,6 +152,32 @@ __device__ __forceinline__ int xcd_tile(int b, int nb) {
   return (b % 8) * (nb / 8) + b / 8;
 }
 
+// Buffer loads. A raw buffer resource carries its size: a load past it
+// returns zeros without touching memory. Loads therefore need no branches
+// (every item, valid or not, issues exactly one load, which keeps the wait
+// counts exact), and items past the data cost no traffic.
+constexpr uint32_t kOutOfRange = 0x80000000u;  // an offset past every resource here
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t buffer_rsrc(const void* base, uint32_t bytes) {
+  // stride 0 (raw), 32-bit dwords, range checked against `bytes`
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes,
+                                           0x00020000);
+}
+// kNonTemporal: the cache-policy bit for data read once (the weight stream)
+constexpr int kNonTemporal = 2;
+template <int POLICY = 0>
+__device__ __forceinline__ u4_t buffer_load16(__amdgpu_buffer_rsrc_t r, uint32_t off) {
+  return __builtin_bit_cast(u4_t, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, POLICY));
+}
+template <int POLICY = 0>
+__device__ __forceinline__ uint32_t buffer_load4(__amdgpu_buffer_rsrc_t r, uint32_t off) {
+  return __builtin_amdgcn_raw_buffer_load_b32(r, off, 0, POLICY);
+}
+
+__device__ __forceinline__ uint32_t buffer_load2(__amdgpu_buffer_rsrc_t r, uint32_t off) {
+  return __builtin_amdgcn_raw_buffer_load_b16(r, off, 0, 0);
+}
+
 // ---------------------------------------------------------------------------
 // Staging into LDS. Global loads go to registers before the weight stream is
 // started, so waiting for them never waits for HBM; what does not fit in the
@@ -155,17 +191,20 @@ __device__ __forceinline__ int xcd_tile(int b, int nb) {
 template <int NT, int R, int DECODE>
 struct MetaStage {
   uint32_t s[R], z[R];
+  // Entry idx = 16 g + c: group g, column n0 + c. The loads are branch-free:
+  // group and column are clamped into the tile's metadata (entries past the
+  // last group are never stored; columns past N meet zero weights or are not
+  // written), so the weight loads issued behind them keep their own counts.
+  __device__ __forceinline__ static void fetch(const GemmArgs& a, int n0, int rows, int idx,
+                                               uint32_t& sv, uint32_t& zv) {
+    const int g = min(idx >> 4, rows - 1);
+    const int n = min(n0 + (idx & 15), a.N - 1);
+    sv = a.sc[(int64_t)g * a.lds + n];
+    zv = a.qz[(int64_t)g * a.ldz + (n >> 3)];
+  }
   __device__ __forceinline__ void load(const GemmArgs& a, int n0, int rows, int tid) {
-    const int items = rows * kTileN;
 #pragma unroll
-    for (int i = 0; i < R; ++i) {
-      const int idx = tid + i * NT;
-      const int n = n0 + (idx & 15);
-      const int g = idx >> 4;
-      const bool ok = idx < items && n < a.N;
-      s[i] = ok ? (uint32_t)a.sc[(int64_t)g * a.lds + n] : 0u;
-      z[i] = ok ? a.qz[(int64_t)g * a.ldz + (n >> 3)] : 0u;
-    }
+    for (int i = 0; i < R; ++i) fetch(a, n0, rows, tid + i * NT, s[i], z[i]);
   }
   __device__ __forceinline__ static void put(u4_t* meta, int idx, int n, uint32_t sbits,
                                              uint32_t zw) {
@@ -181,105 +220,122 @@ struct MetaStage {
     }
     meta[idx] = v;
   }
+  // Entries past the last group go to the spare entry meta[items], so every
+  // value loaded in load() is consumed on every path (a value used only
+  // under a branch lets the compiler sink its load behind the weight loads).
   __device__ __forceinline__ void store(const GemmArgs& a, u4_t* meta, int n0, int rows, int tid) {
     const int items = rows * kTileN;
 #pragma unroll
     for (int i = 0; i < R; ++i) {
       const int idx = tid + i * NT;
-      if (idx < items) put(meta, idx, n0 + (idx & 15), s[i], z[i]);
+      put(meta, min(idx, items), n0 + (idx & 15), s[i], z[i]);
     }
     for (int base = tid + R * NT; base < items; base += 4 * NT) {
       uint32_t ss[4], zz[4];
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int idx = base + i * NT;
-        const int n = n0 + (idx & 15);
-        const int g = idx >> 4;
-        const bool ok = idx < items && n < a.N;
-        ss[i] = ok ? (uint32_t)a.sc[(int64_t)g * a.lds + n] : 0u;
-        zz[i] = ok ? a.qz[(int64_t)g * a.ldz + (n >> 3)] : 0u;
-      }
+      for (int i = 0; i < 4; ++i) fetch(a, n0, rows, base + i * NT, ss[i], zz[i]);
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const int idx = base + i * NT;
         if (idx < items) put(meta, idx, n0 + (idx & 15), ss[i], zz[i]);
       }
+      wait_vmcnt<0>();  // no load of this loop outlives it (see wait_vmcnt)
     }
   }
 };
 
 // Activations in operand order: LDS entry (r * M + m) holds row m, rows
 // 8r..8r+7 of the operand, permuted as x0, x4, x1, x5, x2, x6, x3, x7, for
-// r < 16 * ceil(K / 128) (zero past K). With GATHER the operand column k is X
-// column perm[k] (X[:, perm]). One more zero entry follows (see a_addr).
+// r < 16 * ceil(K / 128) (zero past K). One more zero entry follows (see
+// AAddr), then a spare entry. With GATHER the operand column k is X column
+// perm[k] (X[:, perm]): the rows of X are first copied to LDS as they are
+// (at xr, [M][K]) and gathered from there, so no global load waits on
+// another. Global loads are buffer loads: items past the end load zeros
+// at no cost and go to the spare entry.
 template <int NT, bool GATHER>
 struct XStage {
   static constexpr int R = 4;
-  u4_t v[R];   // !GATHER: raw 16-byte rows; GATHER: permutation entries
+  __amdgpu_buffer_rsrc_t rx;
+  u4_t v[R];   // first-pass pieces: item = tid + i * NT, item = m * kw + r
+  u4_t p[2];   // GATHER: permutation entries of octet tid
+  __device__ __forceinline__ u4_t piece(const GemmArgs& a, int item, int kw) const {
+    const int m = item / kw;
+    const int r = item - m * kw;
+    const uint32_t off = item < a.M * kw ? ((uint32_t)m * (uint32_t)a.ldx + (uint32_t)r * 8u) * 2u
+                                         : kOutOfRange;
+    return buffer_load16(rx, off);
+  }
+  // Pass i (items tid + i * NT) is issued only when some item of it exists:
+  // a wave-uniform test, so the vector memory path is not clogged with
+  // out-of-range loads ahead of the weight stream.
   __device__ __forceinline__ void load(const GemmArgs& a, int tid) {
     const int kw = a.K >> 3;
+    rx = buffer_rsrc(a.X, (uint32_t)a.M * (uint32_t)a.ldx * 2u);
 #pragma unroll
-    for (int i = 0; i < R; ++i) {
-      if (GATHER) {
-        // entries of octet r = tid + (i/2)*NT, half i%2
-        const int r = tid + (i >> 1) * NT;
-        v[i] = r < kw ? *(const u4_t*)(a.perm + r * 8 + 4 * (i & 1)) : u4_t{0u, 0u, 0u, 0u};
-      } else {
-        const int m = i;  // rows 0..R-1 of octet tid (first pass)
-        v[i] = (m < a.M && tid < kw) ? *(const u4_t*)(a.X + (int64_t)m * a.ldx + tid * 8)
-                                     : u4_t{0u, 0u, 0u, 0u};
-      }
+    for (int i = 0; i < R; ++i)
+      if (i * NT < a.M * kw) v[i] = piece(a, tid + i * NT, kw);
+    if (GATHER) {
+      const __amdgpu_buffer_rsrc_t rp = buffer_rsrc(a.perm, (uint32_t)a.K * 4u);
+      const uint32_t off = tid < kw ? (uint32_t)tid * 32u : kOutOfRange;
+      p[0] = buffer_load16(rp, off);
+      p[1] = buffer_load16(rp, off + 16u);
     }
   }
-  __device__ __forceinline__ static u4_t gather_octet(const GemmArgs& a, int m, const u4_t& p0,
-                                                      const u4_t& p1) {
-    const uint32_t kmax = (uint32_t)(a.K - 1);
-    const uint16_t* xr = a.X + (int64_t)m * a.ldx;
-    uint32_t x[8];
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      x[e] = xr[min(p0[e], kmax)];
-      x[e + 4] = xr[min(p1[e], kmax)];
+  // operand entry of (m, r) from a piece of X, or (GATHER) the LDS copy;
+  // items past the end go to the spare entry (xs[spare] or xr[items]).
+  __device__ __forceinline__ static void put(u4_t* xs, u4_t* xr, int M, int kw, int items,
+                                             int spare, int item, const u4_t& x) {
+    if (GATHER) {
+      xr[min(item, items)] = x;
+    } else {
+      const int it = min(item, items - 1);
+      const int m = it / kw;
+      const int r = it - m * kw;
+      xs[item < items ? r * M + m : spare] = permute_octet(x);
     }
-    return u4_t{x[0] | (x[1] << 16), x[2] | (x[3] << 16), x[4] | (x[5] << 16), x[6] | (x[7] << 16)};
   }
-  __device__ __forceinline__ void store(const GemmArgs& a, u4_t* xs, int tid) {
+  __device__ __forceinline__ void store(const GemmArgs& a, u4_t* xs, u4_t* xr, int tid) {
     const int kw = a.K >> 3;
     const int M = a.M;
+    const int items = M * kw;
     const int kwp = 16 * ((a.K + 127) >> 7);
+    const int spare = kwp * M + 1;  // after the zero entry
     for (int i = kw * M + tid; i <= kwp * M; i += NT) xs[i] = u4_t{0u, 0u, 0u, 0u};
+#pragma unroll
+    for (int i = 0; i < R; ++i)
+      if (i * NT < items) put(xs, xr, M, kw, items, spare, tid + i * NT, v[i]);
+    for (int base = tid + R * NT; base < items; base += 4 * NT) {
+      u4_t t4[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) t4[i] = piece(a, base + i * NT, kw);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) put(xs, xr, M, kw, items, spare, base + i * NT, t4[i]);
+      wait_vmcnt<0>();  // no load of this loop outlives it (see wait_vmcnt)
+    }
     if (GATHER) {
+      __syncthreads();  // the copy of X is complete
+      const uint16_t* x16 = (const uint16_t*)xr;
+      const uint32_t kmax = (uint32_t)(a.K - 1);
+      for (int r = tid; r < kw; r += NT) {
+        u4_t p0 = p[0], p1 = p[1];
+        if (r != tid) {
+          p0 = *(const u4_t*)(a.perm + r * 8);
+          p1 = *(const u4_t*)(a.perm + r * 8 + 4);
+          wait_vmcnt<0>();
+        }
+        uint32_t c[8];
 #pragma unroll
-      for (int h = 0; h < 2; ++h) {
-        const int r = tid + h * NT;
-        if (r < kw)
-          for (int m = 0; m < M; ++m) xs[r * M + m] = permute_octet(gather_octet(a, m, v[2 * h], v[2 * h + 1]));
-      }
-      for (int r = tid + 2 * NT; r < kw; r += NT) {
-        const u4_t p0 = *(const u4_t*)(a.perm + r * 8);
-        const u4_t p1 = *(const u4_t*)(a.perm + r * 8 + 4);
-        for (int m = 0; m < M; ++m) xs[r * M + m] = permute_octet(gather_octet(a, m, p0, p1));
-      }
-    } else {
-      if (tid < kw) {
-#pragma unroll
-        for (int m = 0; m < R; ++m)
-          if (m < M) xs[tid * M + m] = permute_octet(v[m]);
-      }
-      // the rest: rows >= R of the first pass, then further octets
-      for (int m = 0; m < M; ++m) {
-        for (int base = (m < R ? tid + NT : tid); base < kw; base += 4 * NT) {
-          u4_t t4[4];
-#pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            const int r = base + i * NT;
-            t4[i] = r < kw ? *(const u4_t*)(a.X + (int64_t)m * a.ldx + r * 8) : u4_t{0u, 0u, 0u, 0u};
-          }
-#pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            const int r = base + i * NT;
-            if (r < kw) xs[r * M + m] = permute_octet(t4[i]);
-          }
+        for (int e = 0; e < 4; ++e) {
+          c[e] = min(p0[e], kmax);
+          c[e + 4] = min(p1[e], kmax);
+        }
+        for (int m = 0; m < M; ++m) {
+          const uint16_t* xm = x16 + m * a.K;
+          // x0, x4, x1, x5, x2, x6, x3, x7
+          xs[r * M + m] = u4_t{xm[c[0]] | ((uint32_t)xm[c[4]] << 16),
+                               xm[c[1]] | ((uint32_t)xm[c[5]] << 16),
+                               xm[c[2]] | ((uint32_t)xm[c[6]] << 16),
+                               xm[c[3]] | ((uint32_t)xm[c[7]] << 16)};
         }
       }
     }
@@ -355,6 +411,76 @@ __device__ __forceinline__ void load_a_block(const GemmArgs& a, int j, int kq, i
 
 constexpr bool a_global(int am) { return am == kAGlobal || am == kAGlobalPrep; }
 
+// The weight stream of one 16-column tile: block b (128 rows) for lane
+// (j, kq); word u = rows 32 (4b + u) + 8 kq .. +7 of column n0 + j.
+// Tiled: one 16-byte load per block. GPTQ: four 4-byte loads (rows past K
+// read zeros; columns past N read whatever lies there and are not written).
+template <int LAYOUT>
+struct WeightStream {
+  __amdgpu_buffer_rsrc_t rs;
+  uint32_t lane_off;   // byte offset of the lane's data in block 0
+  uint32_t blk_bytes;  // bytes between consecutive blocks
+  __device__ __forceinline__ WeightStream(const GemmArgs& a, int tile, int lane, int kq, int col,
+                                          int nblk) {
+    if constexpr (LAYOUT == TPDQ_LAYOUT_TILED) {
+      rs = buffer_rsrc(a.qw + (int64_t)tile * a.ldq, (uint32_t)nblk * 1024u);
+      lane_off = (uint32_t)lane * 16u;
+      blk_bytes = 1024u;
+    } else {
+      rs = buffer_rsrc(a.qw, (uint32_t)(a.K >> 3) * (uint32_t)a.ldq * 4u);
+      lane_off = ((uint32_t)kq * (uint32_t)a.ldq + (uint32_t)col) * 4u;
+      blk_bytes = 16u * (uint32_t)a.ldq * 4u;
+    }
+  }
+  // block b if valid, else zeros at no cost
+  __device__ __forceinline__ u4_t fetch(int b, bool valid, int64_t ldq) const {
+    const uint32_t base = valid ? (uint32_t)b * blk_bytes + lane_off : kOutOfRange;
+    if constexpr (LAYOUT == TPDQ_LAYOUT_TILED) {
+      return buffer_load16<kNonTemporal>(rs, base);
+    } else {
+      const uint32_t step = 4u * (uint32_t)ldq * 4u;  // 32 rows = 4 word rows
+      u4_t w;
+#pragma unroll
+      for (int u = 0; u < 4; ++u)
+        w[u] = buffer_load4<kNonTemporal>(rs, valid ? base + u * step : kOutOfRange);
+      return w;
+    }
+  }
+};
+
+// A fragments of block b from global memory: row t*16 + j, rows 8 (4 (4b + u)
+// + kq) .. +7, permuted into operand order unless already (kAGlobalPrep).
+// Rows past M read zeros from the resource bound; columns past K are zeroed.
+template <int MT, int AM>
+struct AStream {
+  __amdgpu_buffer_rsrc_t rs;
+  uint32_t row_off[MT];
+  __device__ __forceinline__ AStream(const GemmArgs& a, int j) {
+    rs = buffer_rsrc(a.X, (uint32_t)a.M * (uint32_t)a.ldx * 2u);
+#pragma unroll
+    for (int t = 0; t < MT; ++t) {
+      const int row = t * kTileM + j;
+      row_off[t] = row < a.M ? (uint32_t)row * (uint32_t)a.ldx * 2u : kOutOfRange;
+    }
+  }
+  __device__ __forceinline__ void fetch(int b, bool valid, int kq, int kw, u4_t (&x)[4][MT]) const {
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int wr = 4 * (4 * b + u) + kq;
+      const bool in_k = valid && wr < kw;
+#pragma unroll
+      for (int t = 0; t < MT; ++t) {
+        const uint32_t off = in_k && row_off[t] != kOutOfRange ? row_off[t] + (uint32_t)wr * 16u
+                                                              : kOutOfRange;
+        const u4_t v = buffer_load16(rs, off);
+        x[u][t] = AM == kAGlobalPrep ? v : permute_octet(v);
+      }
+    }
+  }
+};
+
+
+
 // LDS entry of the A fragment of row tile t at step s for lane (j, kq):
 // base + stride * s, with rows past M pointed at the zero entry (stride 0).
 struct AAddr {
@@ -367,62 +493,115 @@ struct AAddr {
   }
 };
 
+// Scales and zeros of the ordered kernel, per wave and per chunk of 4 blocks
+// (16 steps of 32 rows, groups g0 = 16 c / (4 SPG) onwards). They travel with
+// the weight stream instead of through LDS, so no wave waits for another
+// wave's metadata: lane 16 q + j loads group g0 + 4 n + q (set n < NL) of
+// column n0 + j, decodes it once per chunk, and a lane that opens group g
+// reads it from lane 16 ((g - g0) % 4) + j of set (g - g0) / 4 (ds_bpermute).
+template <int SPG>
+struct ChunkMeta {
+  static constexpr int NL = SPG >= 4 ? 1 : 4 / SPG;
+  __amdgpu_buffer_rsrc_t rs, rz;
+  uint32_t soff, zoff;    // this lane's pair in group row g0 = 0
+  uint32_t sgrp, zgrp;    // bytes per group row
+  uint32_t shift;         // nibble of column n0 + j in its zeros word
+  uint32_t raw_s[NL], raw_z[NL];
+  float s[NL];
+  uint32_t z1024[NL], z64[NL];
+  __device__ __forceinline__ ChunkMeta(const GemmArgs& a, int ng, int col, int q) {
+    rs = buffer_rsrc(a.sc, (uint32_t)ng * (uint32_t)a.lds * 2u);
+    rz = buffer_rsrc(a.qz, (uint32_t)ng * (uint32_t)a.ldz * 4u);
+    sgrp = (uint32_t)a.lds * 2u;
+    zgrp = (uint32_t)a.ldz * 4u;
+    soff = (uint32_t)q * sgrp + (uint32_t)col * 2u;
+    zoff = (uint32_t)q * zgrp + (uint32_t)(col >> 3) * 4u;
+    shift = 4u * (uint32_t)(col & 7);
+  }
+  // the chunk whose first group is g0 (groups past ng load zeros)
+  __device__ __forceinline__ void load(int g0, bool valid, int ng, int q) {
+#pragma unroll
+    for (int n = 0; n < NL; ++n) {
+      const bool ok = valid && g0 + 4 * n + q < ng;
+      const uint32_t g = (uint32_t)(g0 + 4 * n);
+      raw_s[n] = buffer_load2(rs, ok ? soff + g * sgrp : kOutOfRange);
+      raw_z[n] = buffer_load4(rz, ok ? zoff + g * zgrp : kOutOfRange);
+    }
+  }
+  // {scale as fp32, 1024 + z (fp16 x2), 64 + z (fp16 x2)}, see unpack_sub
+  __device__ __forceinline__ void decode() {
+#pragma unroll
+    for (int n = 0; n < NL; ++n) {
+      const uint32_t zc = (raw_z[n] >> shift) & 0xFu;
+      s[n] = half_bits_to_float(raw_s[n]);
+      z1024[n] = (0x6400u | zc) * 0x10001u;
+      z64[n] = (0x5400u | (zc << 4)) * 0x10001u;
+    }
+  }
+  __device__ __forceinline__ void get(int n, int src, float& sv, uint32_t& z1, uint32_t& z2) const {
+    sv = __shfl(s[n], src);
+    z1 = (uint32_t)__shfl((int)z1024[n], src);
+    z2 = (uint32_t)__shfl((int)z64[n], src);
+  }
+};
+
 // ---------------------------------------------------------------------------
 // Ordered kernel: sorted rows, group of row k = k / G, G = 32 * SPG. Each wave
-// owns a run of 128-row blocks; CB blocks of weights are prefetched one chunk
-// ahead. Group boundaries inside a block sit at compile-time positions.
+// owns a run of 128-row blocks and keeps D of them in flight: the loads are
+// issued in the order the blocks are consumed and waited for one block at a
+// time, so the dequant and MFMAs of a block run while later blocks are still
+// arriving. Each chunk's scales and zeros are loaded just before its first
+// block. Block ranges and the loop are wave-uniform (scalar); group
+// boundaries inside a chunk sit at compile-time positions for G <= 128.
 // ---------------------------------------------------------------------------
 template <int MT, int NW, int SPG, int AM, int LAYOUT>
 __global__ __launch_bounds__(NW * 64) void k_ordered(GemmArgs a) {
   extern __shared__ __align__(16) unsigned char smem[];
   constexpr int NT = NW * 64;
   constexpr bool AG = a_global(AM);
-  constexpr int CB = AG ? (MT == 1 ? 2 : 1) : 4;  // blocks per chunk
+  constexpr int D = AG ? (MT == 4 ? 1 : 2) : 4;  // 128-row blocks in flight per wave
   const int tid = threadIdx.x;
   const int lane = tid & 63;
-  const int wave = tid >> 6;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int j = lane & 15;
   const int kq = lane >> 4;
   const int tile = xcd_tile(blockIdx.x, gridDim.x);
   const int n0 = tile * kTileN;
   const int col = n0 + j;
-  const bool col_ok = col < a.N;
   const int kw = a.K >> 3;
   const int ng = a.K / (32 * SPG);
-  const int nsteps = a.K >> 5;  // 32-row steps
   const int nblk = (a.K + 127) >> 7;
   const int b0 = (int)((int64_t)nblk * wave / NW);
   const int b1 = (int)((int64_t)nblk * (wave + 1) / NW);
-  u4_t* meta = (u4_t*)smem;
   u4_t* xs = (u4_t*)(smem + a.lds_x_off);
+  u4_t* xr = (u4_t*)(smem + a.lds_xr_off);
   const int zero_slot = a.M * 16 * nblk;  // the zero entry after the staged X
-  const uint32_t* qcol = a.qw + col;
-  const uint32_t* qtile = a.qw + (int64_t)tile * a.ldq;
-  const bool wok = LAYOUT == TPDQ_LAYOUT_TILED ? true : col_ok;
   const UnpackConsts kc;
 
-  // 1. staging loads (L2-resident) into registers
-  MetaStage<NT, 4, 1> ms;
-  ms.load(a, n0, ng, tid);
+  // 1. loads, in the order they are needed: activations (L2 hits, staged in
+  //    LDS), the first chunk's scales and zeros, the first D weight blocks
   XStage<NT, AM == kALdsGather> xst;
   if constexpr (!AG) xst.load(a, tid);
-
-  // 2. the weight stream: first chunk
-  u4_t wb[CB];
-  u4_t ab[AG ? CB : 1][4][MT];
+  ChunkMeta<SPG> cm(a, ng, col, kq);
+  cm.load((4 * b0) / SPG, b0 < b1, ng, kq);
+  const WeightStream<LAYOUT> wsrc(a, tile, lane, kq, col, nblk);
+  const AStream<MT, AM> asrc(a, j);
+  u4_t wb[D];
+  u4_t ab[AG ? D : 1][4][MT];
 #pragma unroll
-  for (int bi = 0; bi < CB; ++bi) {
-    const bool ok = b0 + bi < b1;
-    wb[bi] = load_block<LAYOUT>(a, qcol, qtile, lane, kq, b0 + bi, ok && wok, kw);
-    if constexpr (AG) load_a_block<MT, AM>(a, j, kq, b0 + bi, ok, kw, ab[bi]);
+  for (int i = 0; i < D; ++i) {
+    wb[i] = wsrc.fetch(b0 + i, b0 + i < b1, a.ldq);
+    if constexpr (AG) asrc.fetch(b0 + i, b0 + i < b1, kq, kw, ab[i]);
   }
 
-  // 3. staged operands to LDS
-  ms.store(a, meta, n0, ng, tid);
-  if constexpr (!AG) xst.store(a, xs, tid);
-  __syncthreads();
+  // 2. activations to LDS; the metadata and weights stay in flight
+  if constexpr (!AG) {
+    xst.store(a, xs, xr, tid);
+    wait_vmcnt<2 * ChunkMeta<SPG>::NL + D * (LAYOUT == TPDQ_LAYOUT_TILED ? 1 : 4)>();
+    __syncthreads();
+  }
 
-  // 4. main loop
+  // 3. main loop
   AAddr aa[MT];
 #pragma unroll
   for (int t = 0; t < MT; ++t) aa[t].init(a.M, j, kq, t, zero_slot);
@@ -435,82 +614,61 @@ __global__ __launch_bounds__(NW * 64) void k_ordered(GemmArgs a) {
   const f4_t fz = {0.f, 0.f, 0.f, 0.f};
   float s_cur = 0.f;
   uint32_t z1024 = 0x64006400u, z64 = 0x54005400u;
-  auto set_group = [&](int g) {
-    const u4_t v = meta[min(g, ng - 1) * kTileN + j];
-    s_cur = as_f32(v.x);
-    z1024 = v.y;
-    z64 = v.z;
-  };
-  // close a group: acc += s * group_acc
-  auto flush = [&]() {
+
+  // block c + i of the chunk starting at block c: 4 steps of 32 rows; a group
+  // opens at its first step (fresh MFMA accumulator, its scale and zeros) and
+  // closes at its last (acc += s * group_acc). Steps past K have zero
+  // activations and groups past the last one zero metadata.
+  auto block = [&](int c, int i, const u4_t& w, const u4_t (&av_g)[4][MT]) {
+    const int b = c + i;
 #pragma unroll
-    for (int t = 0; t < MT; ++t) acc[t] += s_cur * gacc[t];
-  };
-  set_group((4 * b0) / SPG);
-  bool open = false;  // a group has been accumulated and not yet closed
-  for (int c = b0; c < b1; c += CB) {
-    u4_t wn[CB];
-    u4_t an[AG ? CB : 1][4][MT];
-    const bool more = c + CB < b1;
-    if (more) {
+    for (int u = 0; u < 4; ++u) {
+      const int st = 4 * b + u;
+      bool open, close;
+      if constexpr (SPG <= 4) {
+        open = (u % SPG) == 0;
+        close = (u % SPG) == SPG - 1;
+      } else {  // SPG == 8: a group is blocks 2g and 2g + 1
+        open = u == 0 && ((b & 1) == 0 || b == b0);
+        close = u == 3 && ((b & 1) == 1 || b == b1 - 1);
+      }
+      if (open) {
+        if constexpr (SPG <= 4) {
+          const int rel = (4 * i + u) / SPG;  // compile-time once unrolled
+          cm.get(rel >> 2, 16 * (rel & 3) + j, s_cur, z1024, z64);
+        } else {
+          const int rel = st / SPG - (4 * c) / SPG;  // 0..2
+          cm.get(0, 16 * rel + j, s_cur, z1024, z64);
+        }
+      }
+      h8_t av[MT];
 #pragma unroll
-      for (int bi = 0; bi < CB; ++bi) {
-        const bool ok = c + CB + bi < b1;
-        wn[bi] = load_block<LAYOUT>(a, qcol, qtile, lane, kq, c + CB + bi, ok && wok, kw);
-        if constexpr (AG) load_a_block<MT, AM>(a, j, kq, c + CB + bi, ok, kw, an[bi]);
+      for (int t = 0; t < MT; ++t)
+        av[t] = AG ? as_h8(av_g[u][t]) : as_h8(xs[aa[t].base + aa[t].stride * st]);
+      const h8_t bv = unpack_sub(kc, w[u], z1024, z64);
+#pragma unroll
+      for (int t = 0; t < MT; ++t) gacc[t] = mfma16x16x32(av[t], bv, open ? fz : gacc[t]);
+      if (close) {
+#pragma unroll
+        for (int t = 0; t < MT; ++t) acc[t] += s_cur * gacc[t];
       }
     }
+  };
+
+  // Every load is unconditional (a block or group past the run loads zeros
+  // for free), so that each use waits for exactly what it needs: a load
+  // behind a branch makes the wait counts fall back to waiting for all.
+  for (int c = b0; c < b1; c += 4) {
+    cm.decode();
+    cm.load((4 * (c + 4)) / SPG, c + 4 < b1, ng, kq);
 #pragma unroll
-    for (int bi = 0; bi < CB; ++bi) {
-      const int b = c + bi;
-      if (b < b1) {
-        h8_t av[4][MT];
-#pragma unroll
-        for (int t = 0; t < MT; ++t) {
-          const int i0 = aa[t].base + aa[t].stride * (4 * b);
-#pragma unroll
-          for (int u = 0; u < 4; ++u) {
-            if constexpr (AG)
-              av[u][t] = as_h8(ab[bi][u][t]);
-            else
-              av[u][t] = as_h8(xs[i0 + aa[t].stride * u]);
-          }
-        }
-#pragma unroll
-        for (int u = 0; u < 4; ++u) {
-          // K is a multiple of G and so of 32: the steps of a partial last
-          // block past K hold no rows and must not reopen the last group
-          if (4 * b + u >= nsteps) break;
-          bool start;
-          if constexpr (SPG <= 4)
-            start = (u % SPG) == 0;
-          else
-            start = u == 0 && (b % (SPG / 4)) == 0;
-          if (start) {  // a new group begins at this step: close the last one
-            if (open) flush();
-            set_group((4 * b + u) / SPG);
-          }
-          open = true;
-          const h8_t bv = unpack_sub(kc, wb[bi][u], z1024, z64);
-#pragma unroll
-          for (int t = 0; t < MT; ++t) gacc[t] = mfma16x16x32(av[u][t], bv, start ? fz : gacc[t]);
-        }
-      }
-    }
-    if (more) {
-#pragma unroll
-      for (int bi = 0; bi < CB; ++bi) {
-        wb[bi] = wn[bi];
-        if constexpr (AG) {
-#pragma unroll
-          for (int u = 0; u < 4; ++u)
-#pragma unroll
-            for (int t = 0; t < MT; ++t) ab[bi][u][t] = an[bi][u][t];
-        }
-      }
+    for (int i = 0; i < 4; ++i) {
+      const int b = c + i;
+      if (b < b1) block(c, i, wb[i % D], ab[AG ? i % D : 0]);
+      wb[i % D] = wsrc.fetch(b + D, b + D < b1, a.ldq);
+      if constexpr (AG) asrc.fetch(b + D, b + D < b1, kq, kw, ab[i % D]);
     }
   }
-  if (open) flush();
   reduce_store<MT, NW>(a, acc, n0, smem);
 }
 
@@ -564,7 +722,7 @@ __global__ __launch_bounds__(NW * 64) void k_rowmeta(GemmArgs a) {
   if constexpr (AG) load_a_block<MT, AM>(a, j, kq, b0, b0 < b1, kw, ab);
 
   if constexpr (META == kMetaRowLds) ms.store(a, meta, n0, a.meta_rows, tid);
-  if constexpr (!AG) xst.store(a, xs, tid);
+  if constexpr (!AG) xst.store(a, xs, nullptr, tid);
   if constexpr (META == kMetaRowLds || !AG) __syncthreads();
   AAddr aa[MT];
 #pragma unroll
@@ -658,9 +816,13 @@ typedef void (*DecodeKernel)(GemmArgs);
 
 template <int MT, int NW, int SPG, int L>
 DecodeKernel pick_ordered_am(int am) {
+  // A fragments held in registers for two row tiles do not fit 16 waves
+  constexpr bool ag_ok = !(NW == 16 && MT > 1);
   switch (am) {
-    case kAGlobal: return k_ordered<MT, NW, SPG, kAGlobal, L>;
-    case kAGlobalPrep: return k_ordered<MT, NW, SPG, kAGlobalPrep, L>;
+    case kAGlobal: if constexpr (ag_ok) return k_ordered<MT, NW, SPG, kAGlobal, L>; return nullptr;
+    case kAGlobalPrep:
+      if constexpr (ag_ok) return k_ordered<MT, NW, SPG, kAGlobalPrep, L>;
+      return nullptr;
     case kALds: return k_ordered<MT, NW, SPG, kALds, L>;
     case kALdsGather: return k_ordered<MT, NW, SPG, kALdsGather, L>;
   }
@@ -732,40 +894,52 @@ bool plan_decode(int M, int K, int N, int G, int num_groups, int layout, int met
   if (M < 1 || M > kDecodeMaxM) return false;
   const int mt = M <= 16 ? 1 : (M <= 32 ? 2 : 4);
   const int ntiles = (N + kTileN - 1) / kTileN;
-  // waves per workgroup: about 16 resident waves per CU over the grid
+  // waves per workgroup (the per-row kernels): about 16 resident waves per
+  // CU over the grid; the ordered kernel is set below
   int nw = 16;
   if (ntiles > 256) nw = 8;
   if (ntiles > 1024) nw = 4;
+
   int meta = meta_pref;
   const int spg = G / 32;
   if (meta == kMetaGroup &&
       (G % 32 != 0 || K % G != 0 || !(spg == 1 || spg == 2 || spg == 4 || spg == 8)))
     meta = kMetaRowLds;  // sorted rows of another G: per-row groups floor(k / G)
   if ((meta != kMetaGroup || mt == 4) && nw > 8) nw = 8;
-  int meta_rows = 0;
-  if (meta == kMetaGroup) meta_rows = K / G;
-  if (meta == kMetaRowLds) meta_rows = num_groups;
+  // tile metadata in LDS: the per-row act-order kernel only (the ordered
+  // kernel's travels with its weight stream)
+  int meta_rows = meta == kMetaRowLds ? num_groups : 0;
   const size_t red = (size_t)nw * mt * 1024;
-  size_t meta_bytes = align_up((size_t)meta_rows * kTileN * 16, 16);
+  size_t meta_bytes =
+      meta_rows ? align_up(((size_t)meta_rows * kTileN + 1) * 16, 16) : 0;  // + a spare entry
   if (meta_bytes > kLdsMax - red) {
-    if (meta == kMetaGroup) return false;
     meta = kMetaRowGlobal;
     meta_rows = 0;
     meta_bytes = 0;
   }
-  const size_t x_bytes = ((size_t)M * 16 * ((K + 127) / 128) + 1) * 16;  // padded + zero entry
+  // padded X + the zero entry + a spare entry
+  const size_t x_bytes = ((size_t)M * 16 * ((K + 127) / 128) + 2) * 16;
+  const size_t xr_bytes = align_up((size_t)M * K * 2, 16) + 16;  // the gather's copy of X + spare
   // stage X in LDS when it leaves room for two workgroups per CU (or one,
   // when the grid has no more workgroups than CUs)
   const size_t budget = ntiles <= 256 ? kLdsMax : kLdsMax / 2;
   const bool fits = meta_bytes + x_bytes <= budget;
   int am;
   if (operand == kOperandGather) {
-    if (!fits || meta != kMetaGroup) return false;
+    if (meta_bytes + x_bytes + xr_bytes > budget || meta != kMetaGroup) return false;
     am = kALdsGather;
   } else if (operand == kOperandPrepared) {
     am = kAGlobalPrep;
   } else {
     am = fits ? kALds : kAGlobal;
+  }
+  if (a_global(am) && mt > 1 && nw > 8) nw = 8;
+  if (meta == kMetaGroup) {
+    // the ordered kernel streams best with about 8 blocks of 128 rows per
+    // wave and at most 8 waves per workgroup (measured on the Llama-70B
+    // shard shapes); with X read from global memory, 4 waves
+    const int nblk = (K + 127) / 128;
+    nw = (!a_global(am) && nblk >= 48) ? 8 : 4;
   }
   p->layout = layout;
   p->meta = meta;
@@ -775,8 +949,11 @@ bool plan_decode(int M, int K, int N, int G, int num_groups, int layout, int met
   p->spg = spg;
   p->meta_rows = meta_rows;
   p->lds_x_off = (int)meta_bytes;
+  p->lds_xr_off = (int)(meta_bytes + x_bytes);
   size_t need = a_global(am) ? meta_bytes : meta_bytes + x_bytes;  // <= budget when staged
-  if (need < red) need = red;
+  if (am == kALdsGather) need += xr_bytes;
+  const size_t red_final = (size_t)nw * mt * 1024;  // reduce_store's partial tiles
+  if (need < red_final) need = red_final;
   p->lds_bytes = need;
   return pick_kernel(*p) != nullptr;
 }
@@ -787,6 +964,7 @@ hipError_t launch_decode(const GemmArgs& a0, const DecodePlan& p, hipStream_t s)
   GemmArgs a = a0;
   a.meta_rows = p.meta_rows;
   a.lds_x_off = p.lds_x_off;
+  a.lds_xr_off = p.lds_xr_off;
   if (p.lds_bytes > 64 * 1024) {
     hipError_t e = hipFuncSetAttribute((const void*)k, hipFuncAttributeMaxDynamicSharedMemorySize,
                                        (int)kLdsMax);

@@ -62,6 +62,7 @@ struct GemmArgs {
   int64_t ldy;
   int meta_rows;          // metadata rows staged in LDS
   int lds_x_off;          // byte offset of the staged X in LDS
+  int lds_xr_off;         // kALdsGather: byte offset of the LDS copy of X's rows
 };
 
 // Host-side plan of one decode launch.
@@ -75,6 +76,7 @@ struct DecodePlan {
   int meta_rows;
   size_t lds_bytes;
   int lds_x_off;
+  int lds_xr_off;
 };
 
 // meta_pref: kMetaGroup for sorted rows (needs G % 32 == 0), otherwise a
