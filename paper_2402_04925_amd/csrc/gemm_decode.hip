@@ -449,7 +449,9 @@ struct WeightStream {
 };
 
 // A fragments of block b from global memory: row t*16 + j, rows 8 (4 (4b + u)
-// + kq) .. +7, permuted into operand order unless already (kAGlobalPrep).
+// + kq) .. +7, as stored (the consumer permutes them into operand order
+// unless they already are, kAGlobalPrep: permuting at the load would make
+// the load be waited for at once).
 // Rows past M read zeros from the resource bound; columns past K are zeroed.
 template <int MT, int AM>
 struct AStream {
@@ -472,8 +474,7 @@ struct AStream {
       for (int t = 0; t < MT; ++t) {
         const uint32_t off = in_k && row_off[t] != kOutOfRange ? row_off[t] + (uint32_t)wr * 16u
                                                               : kOutOfRange;
-        const u4_t v = buffer_load16(rs, off);
-        x[u][t] = AM == kAGlobalPrep ? v : permute_octet(v);
+        x[u][t] = buffer_load16(rs, off);  // raw: permuted where it is used
       }
     }
   }
@@ -559,7 +560,9 @@ __global__ __launch_bounds__(NW * 64) void k_ordered(GemmArgs a) {
   extern __shared__ __align__(16) unsigned char smem[];
   constexpr int NT = NW * 64;
   constexpr bool AG = a_global(AM);
-  constexpr int D = AG ? (MT == 4 ? 1 : 2) : 4;  // 128-row blocks in flight per wave
+  // 128-row blocks in flight per wave; with A from global memory its
+  // fragments (4 * MT registers of 16 bytes per block) ride along
+  constexpr int D = AG ? (MT == 4 ? 1 : 2) : 4;
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -580,10 +583,14 @@ __global__ __launch_bounds__(NW * 64) void k_ordered(GemmArgs a) {
 
   // 1. loads, in the order they are needed: activations (L2 hits, staged in
   //    LDS), the first chunk's scales and zeros, the first D weight blocks
+  //    (the scheduling barriers keep that issue order: loads complete in
+  //    order, so a load moved behind the weights would be waited for last)
   XStage<NT, AM == kALdsGather> xst;
   if constexpr (!AG) xst.load(a, tid);
+  __builtin_amdgcn_sched_barrier(0);
   ChunkMeta<SPG> cm(a, ng, col, kq);
   cm.load((4 * b0) / SPG, b0 < b1, ng, kq);
+  __builtin_amdgcn_sched_barrier(0);
   const WeightStream<LAYOUT> wsrc(a, tile, lane, kq, col, nblk);
   const AStream<MT, AM> asrc(a, j);
   u4_t wb[D];
@@ -592,6 +599,7 @@ __global__ __launch_bounds__(NW * 64) void k_ordered(GemmArgs a) {
   for (int i = 0; i < D; ++i) {
     wb[i] = wsrc.fetch(b0 + i, b0 + i < b1, a.ldq);
     if constexpr (AG) asrc.fetch(b0 + i, b0 + i < b1, kq, kw, ab[i]);
+    __builtin_amdgcn_sched_barrier(0);
   }
 
   // 2. activations to LDS; the metadata and weights stay in flight
@@ -644,7 +652,8 @@ __global__ __launch_bounds__(NW * 64) void k_ordered(GemmArgs a) {
       h8_t av[MT];
 #pragma unroll
       for (int t = 0; t < MT; ++t)
-        av[t] = AG ? as_h8(av_g[u][t]) : as_h8(xs[aa[t].base + aa[t].stride * st]);
+        av[t] = AG ? as_h8(AM == kAGlobalPrep ? av_g[u][t] : permute_octet(av_g[u][t]))
+                   : as_h8(xs[aa[t].base + aa[t].stride * st]);
       const h8_t bv = unpack_sub(kc, w[u], z1024, z64);
 #pragma unroll
       for (int t = 0; t < MT; ++t) gacc[t] = mfma16x16x32(av[t], bv, open ? fz : gacc[t]);
@@ -661,12 +670,14 @@ __global__ __launch_bounds__(NW * 64) void k_ordered(GemmArgs a) {
   for (int c = b0; c < b1; c += 4) {
     cm.decode();
     cm.load((4 * (c + 4)) / SPG, c + 4 < b1, ng, kq);
+    __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int b = c + i;
       if (b < b1) block(c, i, wb[i % D], ab[AG ? i % D : 0]);
       wb[i % D] = wsrc.fetch(b + D, b + D < b1, a.ldq);
       if constexpr (AG) asrc.fetch(b + D, b + D < b1, kq, kw, ab[i % D]);
+      __builtin_amdgcn_sched_barrier(0);
     }
   }
   reduce_store<MT, NW>(a, acc, n0, smem);
@@ -816,15 +827,21 @@ typedef void (*DecodeKernel)(GemmArgs);
 
 template <int MT, int NW, int SPG, int L>
 DecodeKernel pick_ordered_am(int am) {
-  // A fragments held in registers for two row tiles do not fit 16 waves
-  constexpr bool ag_ok = !(NW == 16 && MT > 1);
+  // plan_decode gives the ordered kernel 4 or 8 waves with X in LDS and 4
+  // with X from global memory; only those are instantiated
   switch (am) {
-    case kAGlobal: if constexpr (ag_ok) return k_ordered<MT, NW, SPG, kAGlobal, L>; return nullptr;
-    case kAGlobalPrep:
-      if constexpr (ag_ok) return k_ordered<MT, NW, SPG, kAGlobalPrep, L>;
+    case kAGlobal:
+      if constexpr (NW == 4) return k_ordered<MT, NW, SPG, kAGlobal, L>;
       return nullptr;
-    case kALds: return k_ordered<MT, NW, SPG, kALds, L>;
-    case kALdsGather: return k_ordered<MT, NW, SPG, kALdsGather, L>;
+    case kAGlobalPrep:
+      if constexpr (NW == 4) return k_ordered<MT, NW, SPG, kAGlobalPrep, L>;
+      return nullptr;
+    case kALds:
+      if constexpr (NW <= 8) return k_ordered<MT, NW, SPG, kALds, L>;
+      return nullptr;
+    case kALdsGather:
+      if constexpr (NW <= 8) return k_ordered<MT, NW, SPG, kALdsGather, L>;
+      return nullptr;
   }
   return nullptr;
 }
@@ -853,7 +870,7 @@ DecodeKernel pick_row_am(int am) {
 template <int MT, int NW, int L>
 DecodeKernel pick_mt_nw(const DecodePlan& p) {
   if (p.meta == kMetaGroup) return pick_ordered_spg<MT, NW, L>(p.spg, p.amode);
-  if constexpr (NW <= 8) {
+  if constexpr (NW <= 8 && !(MT == 4 && NW > 4)) {
     if (p.meta == kMetaRowLds) return pick_row_am<MT, NW, L, kMetaRowLds>(p.amode);
     return pick_row_am<MT, NW, L, kMetaRowGlobal>(p.amode);
   }
@@ -906,6 +923,7 @@ bool plan_decode(int M, int K, int N, int G, int num_groups, int layout, int met
       (G % 32 != 0 || K % G != 0 || !(spg == 1 || spg == 2 || spg == 4 || spg == 8)))
     meta = kMetaRowLds;  // sorted rows of another G: per-row groups floor(k / G)
   if ((meta != kMetaGroup || mt == 4) && nw > 8) nw = 8;
+  if (meta != kMetaGroup && mt == 4) nw = 4;  // four row tiles of per-row dequant: registers
   // tile metadata in LDS: the per-row act-order kernel only (the ordered
   // kernel's travels with its weight stream)
   int meta_rows = meta == kMetaRowLds ? num_groups : 0;
