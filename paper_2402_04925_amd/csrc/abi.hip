@@ -71,7 +71,11 @@ tpdq_status check_layer(const tpdq_w4* w, const char* name, bool need_gidx, bool
 
 // Workspace of the GEMM and MLP calls: only the gathered activations, when
 // the gather X[:, perm] cannot be done inside the GEMM's LDS.
-size_t gather_ws_bytes(int M, int K) { return align_up((size_t)M * K * 2); }
+// the prepared operand (k_gather_prep): 16 rows x 128 columns x 2 bytes per
+// (row tile, 128-row block)
+size_t gather_ws_bytes(int M, int K) {
+  return align_up((size_t)((M + kTileM - 1) / kTileM) * ((K + 127) / 128) * 4096);
+}
 
 int meta_mode(tpdq_path path) {
   if (path == TPDQ_PATH_ORDERED) return kMetaGroup;

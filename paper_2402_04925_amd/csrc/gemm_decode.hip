@@ -254,7 +254,7 @@ struct MetaStage {
 // at no cost and go to the spare entry.
 template <int NT, bool GATHER>
 struct XStage {
-  static constexpr int R = 4;
+  static constexpr int R = 8;
   __amdgpu_buffer_rsrc_t rx;
   u4_t v[R];   // first-pass pieces: item = tid + i * NT, item = m * kw + r
   u4_t p[2];   // GATHER: permutation entries of octet tid
@@ -342,30 +342,34 @@ struct XStage {
   }
 };
 
-// Sum the NW waves' 16-column partial tiles in LDS and write fp16.
-// acc[t] of lane l holds rows t*16 + 4*(l/16) + e, column l % 16.
-template <int MT, int NW>
-__device__ __forceinline__ void reduce_store(const GemmArgs& a, f4_t (&acc)[MT], int n0,
+// Sum the NW waves' partial tiles (TN tiles of 16 columns from n0) in LDS
+// and write fp16. acc[t][n] of lane l holds rows t*16 + 4*(l/16) + e, column
+// n0 + 16 n + l % 16.
+template <int MT, int NW, int TN>
+__device__ __forceinline__ void reduce_store(const GemmArgs& a, f4_t (&acc)[MT][TN], int n0,
                                              unsigned char* smem) {
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = tid >> 6;
   __syncthreads();  // everyone is done with the staged operands
-  float* red = (float*)smem;  // [NW][MT][4][64]
+  float* red = (float*)smem;  // [NW][MT][TN][4][64]
 #pragma unroll
   for (int t = 0; t < MT; ++t)
 #pragma unroll
-    for (int e = 0; e < 4; ++e) red[((wave * MT + t) * 4 + e) * 64 + lane] = acc[t][e];
+    for (int n = 0; n < TN; ++n)
+#pragma unroll
+      for (int e = 0; e < 4; ++e)
+        red[(((wave * MT + t) * TN + n) * 4 + e) * 64 + lane] = acc[t][n][e];
   __syncthreads();
-  for (int idx = tid; idx < MT * 256; idx += NW * 64) {
-    const int t = idx >> 8;
+  for (int idx = tid; idx < MT * TN * 256; idx += NW * 64) {
+    const int tn = idx >> 8;  // t * TN + n
     const int e = (idx >> 6) & 3;
     const int ln = idx & 63;
     float s = 0.f;
 #pragma unroll
-    for (int w = 0; w < NW; ++w) s += red[((w * MT + t) * 4 + e) * 64 + ln];
-    const int row = t * kTileM + 4 * (ln >> 4) + e;
-    const int c = n0 + (ln & 15);
+    for (int w = 0; w < NW; ++w) s += red[((w * MT * TN + tn) * 4 + e) * 64 + ln];
+    const int row = (tn / TN) * kTileM + 4 * (ln >> 4) + e;
+    const int c = n0 + (tn % TN) * kTileN + (ln & 15);
     if (row < a.M && c < a.N) a.Y[(int64_t)row * a.ldy + c] = float_to_half_bits(s);
   }
 }
@@ -401,10 +405,17 @@ __device__ __forceinline__ void load_a_block(const GemmArgs& a, int j, int kq, i
 #pragma unroll
     for (int t = 0; t < MT; ++t) {
       const int row = t * kTileM + j;
-      const u4_t v = (ok && wr < kw && row < a.M)
-                         ? *(const u4_t*)(a.X + (int64_t)row * a.ldx + wr * 8)
-                         : u4_t{0u, 0u, 0u, 0u};
-      x[u][t] = AM == kAGlobalPrep ? v : permute_octet(v);
+      if constexpr (AM == kAGlobalPrep) {
+        // the prepared operand's record [t][4b + u][16 kq + j] (see k_gather_prep)
+        const int64_t nsteps = 4 * (int64_t)((a.K + 127) >> 7);
+        const int64_t rec = ((int64_t)t * nsteps + 4 * b + u) * 64 + 16 * kq + j;
+        x[u][t] = ok ? *(const u4_t*)(a.X + rec * 8) : u4_t{0u, 0u, 0u, 0u};
+      } else {
+        const u4_t v = (ok && wr < kw && row < a.M)
+                           ? *(const u4_t*)(a.X + (int64_t)row * a.ldx + wr * 8)
+                           : u4_t{0u, 0u, 0u, 0u};
+        x[u][t] = permute_octet(v);
+      }
     }
   }
 }
@@ -420,14 +431,15 @@ struct WeightStream {
   __amdgpu_buffer_rsrc_t rs;
   uint32_t lane_off;   // byte offset of the lane's data in block 0
   uint32_t blk_bytes;  // bytes between consecutive blocks
-  __device__ __forceinline__ WeightStream(const GemmArgs& a, int tile, int lane, int kq, int col,
-                                          int nblk) {
+  // tile_ok false (a tile past N): every load returns zeros
+  __device__ __forceinline__ void init(const GemmArgs& a, int tile, bool tile_ok, int lane, int kq,
+                                       int col, int nblk) {
     if constexpr (LAYOUT == TPDQ_LAYOUT_TILED) {
-      rs = buffer_rsrc(a.qw + (int64_t)tile * a.ldq, (uint32_t)nblk * 1024u);
+      rs = buffer_rsrc(a.qw + (int64_t)tile * a.ldq, tile_ok ? (uint32_t)nblk * 1024u : 0u);
       lane_off = (uint32_t)lane * 16u;
       blk_bytes = 1024u;
     } else {
-      rs = buffer_rsrc(a.qw, (uint32_t)(a.K >> 3) * (uint32_t)a.ldq * 4u);
+      rs = buffer_rsrc(a.qw, tile_ok ? (uint32_t)(a.K >> 3) * (uint32_t)a.ldq * 4u : 0u);
       lane_off = ((uint32_t)kq * (uint32_t)a.ldq + (uint32_t)col) * 4u;
       blk_bytes = 16u * (uint32_t)a.ldq * 4u;
     }
@@ -453,26 +465,39 @@ struct WeightStream {
 // unless they already are, kAGlobalPrep: permuting at the load would make
 // the load be waited for at once).
 // Rows past M read zeros from the resource bound; columns past K are zeroed.
+// kAGlobalPrep reads the prepared operand (k_gather_prep): 16-byte records
+// [row tile t][step s][lane], one contiguous KiB per load instruction, in
+// operand order and zero-padded.
 template <int MT, int AM>
 struct AStream {
   __amdgpu_buffer_rsrc_t rs;
   uint32_t row_off[MT];
-  __device__ __forceinline__ AStream(const GemmArgs& a, int j) {
-    rs = buffer_rsrc(a.X, (uint32_t)a.M * (uint32_t)a.ldx * 2u);
+  __device__ __forceinline__ AStream(const GemmArgs& a, int j, int lane) {
+    if constexpr (AM == kAGlobalPrep) {
+      const uint32_t nsteps = 4u * (uint32_t)((a.K + 127) >> 7);
+      rs = buffer_rsrc(a.X, (uint32_t)MT * nsteps * 1024u);
 #pragma unroll
-    for (int t = 0; t < MT; ++t) {
-      const int row = t * kTileM + j;
-      row_off[t] = row < a.M ? (uint32_t)row * (uint32_t)a.ldx * 2u : kOutOfRange;
+      for (int t = 0; t < MT; ++t) row_off[t] = ((uint32_t)t * nsteps * 64u + (uint32_t)lane) * 16u;
+    } else {
+      rs = buffer_rsrc(a.X, (uint32_t)a.M * (uint32_t)a.ldx * 2u);
+#pragma unroll
+      for (int t = 0; t < MT; ++t) {
+        const int row = t * kTileM + j;
+        row_off[t] = row < a.M ? (uint32_t)row * (uint32_t)a.ldx * 2u : kOutOfRange;
+      }
     }
   }
   __device__ __forceinline__ void fetch(int b, bool valid, int kq, int kw, u4_t (&x)[4][MT]) const {
 #pragma unroll
     for (int u = 0; u < 4; ++u) {
       const int wr = 4 * (4 * b + u) + kq;
-      const bool in_k = valid && wr < kw;
 #pragma unroll
       for (int t = 0; t < MT; ++t) {
-        const uint32_t off = in_k && row_off[t] != kOutOfRange ? row_off[t] + (uint32_t)wr * 16u
+        uint32_t off;
+        if constexpr (AM == kAGlobalPrep)
+          off = valid ? row_off[t] + (uint32_t)(4 * b + u) * 1024u : kOutOfRange;
+        else
+          off = valid && wr < kw && row_off[t] != kOutOfRange ? row_off[t] + (uint32_t)wr * 16u
                                                               : kOutOfRange;
         x[u][t] = buffer_load16(rs, off);  // raw: permuted where it is used
       }
@@ -510,7 +535,7 @@ struct ChunkMeta {
   uint32_t raw_s[NL], raw_z[NL];
   float s[NL];
   uint32_t z1024[NL], z64[NL];
-  __device__ __forceinline__ ChunkMeta(const GemmArgs& a, int ng, int col, int q) {
+  __device__ __forceinline__ void init(const GemmArgs& a, int ng, int col, int q) {
     rs = buffer_rsrc(a.sc, (uint32_t)ng * (uint32_t)a.lds * 2u);
     rz = buffer_rsrc(a.qz, (uint32_t)ng * (uint32_t)a.ldz * 4u);
     sgrp = (uint32_t)a.lds * 2u;
@@ -547,15 +572,17 @@ struct ChunkMeta {
 };
 
 // ---------------------------------------------------------------------------
-// Ordered kernel: sorted rows, group of row k = k / G, G = 32 * SPG. Each wave
-// owns a run of 128-row blocks and keeps D of them in flight: the loads are
-// issued in the order the blocks are consumed and waited for one block at a
-// time, so the dequant and MFMAs of a block run while later blocks are still
-// arriving. Each chunk's scales and zeros are loaded just before its first
-// block. Block ranges and the loop are wave-uniform (scalar); group
+// Ordered kernel: sorted rows, group of row k = k / G, G = 32 * SPG. A
+// workgroup owns TN 16-column tiles over all of K (TN = 2 halves the
+// activation traffic per column where X is read from global memory). Each
+// wave owns a run of 128-row blocks and keeps D of them in flight: the loads
+// are issued in the order the blocks are consumed and waited for one block at
+// a time, so the dequant and MFMAs of a block run while later blocks are
+// still arriving. Each chunk's scales and zeros are loaded just before its
+// first block. Block ranges and the loop are wave-uniform (scalar); group
 // boundaries inside a chunk sit at compile-time positions for G <= 128.
 // ---------------------------------------------------------------------------
-template <int MT, int NW, int SPG, int AM, int LAYOUT>
+template <int MT, int NW, int SPG, int AM, int LAYOUT, int TN>
 __global__ __launch_bounds__(NW * 64) void k_ordered(GemmArgs a) {
   extern __shared__ __align__(16) unsigned char smem[];
   constexpr int NT = NW * 64;
@@ -568,9 +595,8 @@ __global__ __launch_bounds__(NW * 64) void k_ordered(GemmArgs a) {
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int j = lane & 15;
   const int kq = lane >> 4;
-  const int tile = xcd_tile(blockIdx.x, gridDim.x);
-  const int n0 = tile * kTileN;
-  const int col = n0 + j;
+  const int tile0 = xcd_tile(blockIdx.x, gridDim.x) * TN;
+  const int ntiles = (a.N + kTileN - 1) / kTileN;
   const int kw = a.K >> 3;
   const int ng = a.K / (32 * SPG);
   const int nblk = (a.K + 127) >> 7;
@@ -588,24 +614,35 @@ __global__ __launch_bounds__(NW * 64) void k_ordered(GemmArgs a) {
   XStage<NT, AM == kALdsGather> xst;
   if constexpr (!AG) xst.load(a, tid);
   __builtin_amdgcn_sched_barrier(0);
-  ChunkMeta<SPG> cm(a, ng, col, kq);
-  cm.load((4 * b0) / SPG, b0 < b1, ng, kq);
+  ChunkMeta<SPG> cm[TN];
+#pragma unroll
+  for (int n = 0; n < TN; ++n) {
+    cm[n].init(a, ng, (tile0 + n) * kTileN + j, kq);
+    cm[n].load((4 * b0) / SPG, b0 < b1, ng, kq);
+  }
   __builtin_amdgcn_sched_barrier(0);
-  const WeightStream<LAYOUT> wsrc(a, tile, lane, kq, col, nblk);
-  const AStream<MT, AM> asrc(a, j);
-  u4_t wb[D];
+  WeightStream<LAYOUT> wsrc[TN];
+#pragma unroll
+  for (int n = 0; n < TN; ++n)
+    wsrc[n].init(a, tile0 + n, tile0 + n < ntiles, lane, kq, (tile0 + n) * kTileN + j, nblk);
+  const AStream<MT, AM> asrc(a, j, lane);
+  u4_t wb[D][TN];
   u4_t ab[AG ? D : 1][4][MT];
+  auto fetch = [&](int b, int slot) {
+#pragma unroll
+    for (int n = 0; n < TN; ++n) wb[slot][n] = wsrc[n].fetch(b, b < b1, a.ldq);
+    if constexpr (AG) asrc.fetch(b, b < b1, kq, kw, ab[slot]);
+  };
 #pragma unroll
   for (int i = 0; i < D; ++i) {
-    wb[i] = wsrc.fetch(b0 + i, b0 + i < b1, a.ldq);
-    if constexpr (AG) asrc.fetch(b0 + i, b0 + i < b1, kq, kw, ab[i]);
+    fetch(b0 + i, i);
     __builtin_amdgcn_sched_barrier(0);
   }
 
   // 2. activations to LDS; the metadata and weights stay in flight
   if constexpr (!AG) {
     xst.store(a, xs, xr, tid);
-    wait_vmcnt<2 * ChunkMeta<SPG>::NL + D * (LAYOUT == TPDQ_LAYOUT_TILED ? 1 : 4)>();
+    wait_vmcnt<TN * (2 * ChunkMeta<SPG>::NL + D * (LAYOUT == TPDQ_LAYOUT_TILED ? 1 : 4))>();
     __syncthreads();
   }
 
@@ -613,21 +650,29 @@ __global__ __launch_bounds__(NW * 64) void k_ordered(GemmArgs a) {
   AAddr aa[MT];
 #pragma unroll
   for (int t = 0; t < MT; ++t) aa[t].init(a.M, j, kq, t, zero_slot);
-  f4_t acc[MT], gacc[MT];
+  f4_t acc[MT][TN], gacc[MT][TN];
 #pragma unroll
-  for (int t = 0; t < MT; ++t) {
-    acc[t] = f4_t{0.f, 0.f, 0.f, 0.f};
-    gacc[t] = f4_t{0.f, 0.f, 0.f, 0.f};
-  }
+  for (int t = 0; t < MT; ++t)
+#pragma unroll
+    for (int n = 0; n < TN; ++n) {
+      acc[t][n] = f4_t{0.f, 0.f, 0.f, 0.f};
+      gacc[t][n] = f4_t{0.f, 0.f, 0.f, 0.f};
+    }
   const f4_t fz = {0.f, 0.f, 0.f, 0.f};
-  float s_cur = 0.f;
-  uint32_t z1024 = 0x64006400u, z64 = 0x54005400u;
+  float s_cur[TN];
+  uint32_t z1024[TN], z64[TN];
+#pragma unroll
+  for (int n = 0; n < TN; ++n) {
+    s_cur[n] = 0.f;
+    z1024[n] = 0x64006400u;
+    z64[n] = 0x54005400u;
+  }
 
   // block c + i of the chunk starting at block c: 4 steps of 32 rows; a group
   // opens at its first step (fresh MFMA accumulator, its scale and zeros) and
   // closes at its last (acc += s * group_acc). Steps past K have zero
   // activations and groups past the last one zero metadata.
-  auto block = [&](int c, int i, const u4_t& w, const u4_t (&av_g)[4][MT]) {
+  auto block = [&](int c, int i, const u4_t (&w)[TN], const u4_t (&av_g)[4][MT]) {
     const int b = c + i;
 #pragma unroll
     for (int u = 0; u < 4; ++u) {
@@ -641,12 +686,15 @@ __global__ __launch_bounds__(NW * 64) void k_ordered(GemmArgs a) {
         close = u == 3 && ((b & 1) == 1 || b == b1 - 1);
       }
       if (open) {
-        if constexpr (SPG <= 4) {
-          const int rel = (4 * i + u) / SPG;  // compile-time once unrolled
-          cm.get(rel >> 2, 16 * (rel & 3) + j, s_cur, z1024, z64);
-        } else {
-          const int rel = st / SPG - (4 * c) / SPG;  // 0..2
-          cm.get(0, 16 * rel + j, s_cur, z1024, z64);
+#pragma unroll
+        for (int n = 0; n < TN; ++n) {
+          if constexpr (SPG <= 4) {
+            const int rel = (4 * i + u) / SPG;  // compile-time once unrolled
+            cm[n].get(rel >> 2, 16 * (rel & 3) + j, s_cur[n], z1024[n], z64[n]);
+          } else {
+            const int rel = st / SPG - (4 * c) / SPG;  // 0..2
+            cm[n].get(0, 16 * rel + j, s_cur[n], z1024[n], z64[n]);
+          }
         }
       }
       h8_t av[MT];
@@ -654,12 +702,18 @@ __global__ __launch_bounds__(NW * 64) void k_ordered(GemmArgs a) {
       for (int t = 0; t < MT; ++t)
         av[t] = AG ? as_h8(AM == kAGlobalPrep ? av_g[u][t] : permute_octet(av_g[u][t]))
                    : as_h8(xs[aa[t].base + aa[t].stride * st]);
-      const h8_t bv = unpack_sub(kc, w[u], z1024, z64);
 #pragma unroll
-      for (int t = 0; t < MT; ++t) gacc[t] = mfma16x16x32(av[t], bv, open ? fz : gacc[t]);
+      for (int n = 0; n < TN; ++n) {
+        const h8_t bv = unpack_sub(kc, w[n][u], z1024[n], z64[n]);
+#pragma unroll
+        for (int t = 0; t < MT; ++t)
+          gacc[t][n] = mfma16x16x32(av[t], bv, open ? fz : gacc[t][n]);
+      }
       if (close) {
 #pragma unroll
-        for (int t = 0; t < MT; ++t) acc[t] += s_cur * gacc[t];
+        for (int t = 0; t < MT; ++t)
+#pragma unroll
+          for (int n = 0; n < TN; ++n) acc[t][n] += s_cur[n] * gacc[t][n];
       }
     }
   };
@@ -668,19 +722,21 @@ __global__ __launch_bounds__(NW * 64) void k_ordered(GemmArgs a) {
   // for free), so that each use waits for exactly what it needs: a load
   // behind a branch makes the wait counts fall back to waiting for all.
   for (int c = b0; c < b1; c += 4) {
-    cm.decode();
-    cm.load((4 * (c + 4)) / SPG, c + 4 < b1, ng, kq);
+#pragma unroll
+    for (int n = 0; n < TN; ++n) {
+      cm[n].decode();
+      cm[n].load((4 * (c + 4)) / SPG, c + 4 < b1, ng, kq);
+    }
     __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int b = c + i;
       if (b < b1) block(c, i, wb[i % D], ab[AG ? i % D : 0]);
-      wb[i % D] = wsrc.fetch(b + D, b + D < b1, a.ldq);
-      if constexpr (AG) asrc.fetch(b + D, b + D < b1, kq, kw, ab[i % D]);
+      fetch(b + D, i % D);
       __builtin_amdgcn_sched_barrier(0);
     }
   }
-  reduce_store<MT, NW>(a, acc, n0, smem);
+  reduce_store<MT, NW, TN>(a, acc, tile0 * kTileN, smem);
 }
 
 // ---------------------------------------------------------------------------
@@ -797,62 +853,79 @@ __global__ __launch_bounds__(NW * 64) void k_rowmeta(GemmArgs a) {
       }
     }
   }
-  reduce_store<MT, NW>(a, acc, n0, smem);
+  f4_t acc1[MT][1];
+#pragma unroll
+  for (int t = 0; t < MT; ++t) acc1[t][0] = acc[t];
+  reduce_store<MT, NW, 1>(a, acc1, n0, smem);
 }
 
-// X'[m][k] = X[m][perm[k]] (perm NULL: X itself), written in operand order
-// (each 8-column octet permuted as x0, x4, x1, x5, x2, x6, x3, x7) for
-// kAGlobalPrep.
+// The prepared operand: X'[m][k] = X[m][perm[k]] (perm NULL: X itself) as
+// 16-byte records [row tile t][step s][lane l]: row 16 t + l % 16, operand
+// rows 8 (4 s + l / 16) .. +7 in operand order (x0, x4, x1, x5, ...), zero
+// past M or K. A decode wave reads one step of one row tile as one
+// contiguous KiB.
 __global__ void k_gather_prep(const uint16_t* __restrict__ X, int64_t ldx, int M, int K,
                               const int32_t* __restrict__ perm, uint16_t* __restrict__ Xp) {
   const int kw = K >> 3;
-  const int64_t total = (int64_t)M * kw;
+  const int nsteps = 4 * ((K + 127) >> 7);
+  const int mt = (M + kTileM - 1) / kTileM;
+  const int64_t total = (int64_t)mt * nsteps * 64;
   const uint32_t kmax = (uint32_t)(K - 1);
   for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < total;
        i += (int64_t)gridDim.x * blockDim.x) {
-    const int m = (int)(i / kw);
-    const int r = (int)(i - (int64_t)m * kw);
-    const uint16_t* xr = X + (int64_t)m * ldx;
-    uint32_t x[8];
+    const int l = (int)(i & 63);
+    const int ts = (int)(i >> 6);
+    const int t = ts / nsteps;
+    const int st = ts - t * nsteps;
+    const int m = t * kTileM + (l & 15);
+    const int r = 4 * st + (l >> 4);
+    u4_t v = {0u, 0u, 0u, 0u};
+    if (m < M && r < kw) {
+      const uint16_t* xr = X + (int64_t)m * ldx;
+      uint32_t x[8];
 #pragma unroll
-    for (int e = 0; e < 8; ++e)
-      x[e] = xr[perm ? min((uint32_t)perm[r * 8 + e], kmax) : (uint32_t)(r * 8 + e)];
-    const u4_t v = {x[0] | (x[4] << 16), x[1] | (x[5] << 16), x[2] | (x[6] << 16),
-                    x[3] | (x[7] << 16)};
-    *(u4_t*)(Xp + (int64_t)m * K + r * 8) = v;
+      for (int e = 0; e < 8; ++e)
+        x[e] = xr[perm ? min((uint32_t)perm[r * 8 + e], kmax) : (uint32_t)(r * 8 + e)];
+      v = u4_t{x[0] | (x[4] << 16), x[1] | (x[5] << 16), x[2] | (x[6] << 16), x[3] | (x[7] << 16)};
+    }
+    *(u4_t*)(Xp + i * 8) = v;
   }
 }
 
 typedef void (*DecodeKernel)(GemmArgs);
 
 template <int MT, int NW, int SPG, int L>
-DecodeKernel pick_ordered_am(int am) {
-  // plan_decode gives the ordered kernel 4 or 8 waves with X in LDS and 4
-  // with X from global memory; only those are instantiated
+DecodeKernel pick_ordered_am(int am, int tn) {
+  // plan_decode gives the ordered kernel 4 or 8 waves and one tile with X in
+  // LDS, 4 waves and one or two tiles with X from global memory; only those
+  // are instantiated
   switch (am) {
     case kAGlobal:
-      if constexpr (NW == 4) return k_ordered<MT, NW, SPG, kAGlobal, L>;
+      if constexpr (NW == 4)
+        return tn == 2 ? k_ordered<MT, NW, SPG, kAGlobal, L, 2> : k_ordered<MT, NW, SPG, kAGlobal, L, 1>;
       return nullptr;
     case kAGlobalPrep:
-      if constexpr (NW == 4) return k_ordered<MT, NW, SPG, kAGlobalPrep, L>;
+      if constexpr (NW == 4)
+        return tn == 2 ? k_ordered<MT, NW, SPG, kAGlobalPrep, L, 2>
+                       : k_ordered<MT, NW, SPG, kAGlobalPrep, L, 1>;
       return nullptr;
     case kALds:
-      if constexpr (NW <= 8) return k_ordered<MT, NW, SPG, kALds, L>;
+      if constexpr (NW <= 8) return tn == 1 ? k_ordered<MT, NW, SPG, kALds, L, 1> : nullptr;
       return nullptr;
     case kALdsGather:
-      if constexpr (NW <= 8) return k_ordered<MT, NW, SPG, kALdsGather, L>;
+      if constexpr (NW <= 8) return tn == 1 ? k_ordered<MT, NW, SPG, kALdsGather, L, 1> : nullptr;
       return nullptr;
   }
   return nullptr;
 }
 
 template <int MT, int NW, int L>
-DecodeKernel pick_ordered_spg(int spg, int am) {
+DecodeKernel pick_ordered_spg(int spg, int am, int tn) {
   switch (spg) {
-    case 1: return pick_ordered_am<MT, NW, 1, L>(am);
-    case 2: return pick_ordered_am<MT, NW, 2, L>(am);
-    case 4: return pick_ordered_am<MT, NW, 4, L>(am);
-    case 8: return pick_ordered_am<MT, NW, 8, L>(am);
+    case 1: return pick_ordered_am<MT, NW, 1, L>(am, tn);
+    case 2: return pick_ordered_am<MT, NW, 2, L>(am, tn);
+    case 4: return pick_ordered_am<MT, NW, 4, L>(am, tn);
+    case 8: return pick_ordered_am<MT, NW, 8, L>(am, tn);
   }
   return nullptr;
 }
@@ -869,7 +942,7 @@ DecodeKernel pick_row_am(int am) {
 
 template <int MT, int NW, int L>
 DecodeKernel pick_mt_nw(const DecodePlan& p) {
-  if (p.meta == kMetaGroup) return pick_ordered_spg<MT, NW, L>(p.spg, p.amode);
+  if (p.meta == kMetaGroup) return pick_ordered_spg<MT, NW, L>(p.spg, p.amode, p.tn);
   if constexpr (NW <= 8 && !(MT == 4 && NW > 4)) {
     if (p.meta == kMetaRowLds) return pick_row_am<MT, NW, L, kMetaRowLds>(p.amode);
     return pick_row_am<MT, NW, L, kMetaRowGlobal>(p.amode);
@@ -952,13 +1025,17 @@ bool plan_decode(int M, int K, int N, int G, int num_groups, int layout, int met
     am = fits ? kALds : kAGlobal;
   }
   if (a_global(am) && mt > 1 && nw > 8) nw = 8;
+  int tn = 1;
   if (meta == kMetaGroup) {
     // the ordered kernel streams best with about 8 blocks of 128 rows per
     // wave and at most 8 waves per workgroup (measured on the Llama-70B
-    // shard shapes); with X read from global memory, 4 waves
+    // shard shapes); with X read from global memory, 4 waves, and two tiles
+    // per workgroup when that still leaves a workgroup per CU
     const int nblk = (K + 127) / 128;
     nw = (!a_global(am) && nblk >= 48) ? 8 : 4;
+    if (a_global(am) && ntiles >= 512) tn = 2;
   }
+  p->tn = tn;
   p->layout = layout;
   p->meta = meta;
   p->amode = am;
@@ -970,7 +1047,7 @@ bool plan_decode(int M, int K, int N, int G, int num_groups, int layout, int met
   p->lds_xr_off = (int)(meta_bytes + x_bytes);
   size_t need = a_global(am) ? meta_bytes : meta_bytes + x_bytes;  // <= budget when staged
   if (am == kALdsGather) need += xr_bytes;
-  const size_t red_final = (size_t)nw * mt * 1024;  // reduce_store's partial tiles
+  const size_t red_final = (size_t)nw * mt * tn * 1024;  // reduce_store's partial tiles
   if (need < red_final) need = red_final;
   p->lds_bytes = need;
   return pick_kernel(*p) != nullptr;
@@ -989,13 +1066,13 @@ hipError_t launch_decode(const GemmArgs& a0, const DecodePlan& p, hipStream_t s)
     if (e != hipSuccess) return e;
   }
   const int ntiles = (a.N + kTileN - 1) / kTileN;
-  hipLaunchKernelGGL(k, dim3(ntiles), dim3(p.nw * 64), p.lds_bytes, s, a);
+  hipLaunchKernelGGL(k, dim3((ntiles + p.tn - 1) / p.tn), dim3(p.nw * 64), p.lds_bytes, s, a);
   return hipGetLastError();
 }
 
 hipError_t launch_gather_prep(const uint16_t* X, int64_t ldx, int M, int K, const int32_t* perm,
                               uint16_t* Xp, hipStream_t s) {
-  const int64_t total = (int64_t)M * (K / 8);
+  const int64_t total = (int64_t)((M + kTileM - 1) / kTileM) * 4 * ((K + 127) / 128) * 64;
   int blocks = (int)((total + 255) / 256);
   if (blocks > 4096) blocks = 4096;
   if (blocks < 1) blocks = 1;

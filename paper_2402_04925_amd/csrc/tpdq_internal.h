@@ -72,6 +72,7 @@ struct DecodePlan {
   int amode;    // AMode
   int nw;       // waves per workgroup
   int mt;       // row tiles (1, 2, 4)
+  int tn;       // 16-column tiles per workgroup (ordered kernel: 1 or 2)
   int spg;      // 32-row steps per group (kMetaGroup)
   int meta_rows;
   size_t lds_bytes;
