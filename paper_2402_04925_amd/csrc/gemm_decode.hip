@@ -476,8 +476,11 @@ struct AStream {
     if constexpr (AM == kAGlobalPrep) {
       const uint32_t nsteps = 4u * (uint32_t)((a.K + 127) >> 7);
       rs = buffer_rsrc(a.X, (uint32_t)MT * nsteps * 1024u);
+      // rows past M hold zeros: skip them (out of range loads cost nothing)
 #pragma unroll
-      for (int t = 0; t < MT; ++t) row_off[t] = ((uint32_t)t * nsteps * 64u + (uint32_t)lane) * 16u;
+      for (int t = 0; t < MT; ++t)
+        row_off[t] = t * kTileM + j < a.M ? ((uint32_t)t * nsteps * 64u + (uint32_t)lane) * 16u
+                                          : kOutOfRange;
     } else {
       rs = buffer_rsrc(a.X, (uint32_t)a.M * (uint32_t)a.ldx * 2u);
 #pragma unroll
@@ -495,7 +498,8 @@ struct AStream {
       for (int t = 0; t < MT; ++t) {
         uint32_t off;
         if constexpr (AM == kAGlobalPrep)
-          off = valid ? row_off[t] + (uint32_t)(4 * b + u) * 1024u : kOutOfRange;
+          off = valid && row_off[t] != kOutOfRange ? row_off[t] + (uint32_t)(4 * b + u) * 1024u
+                                                   : kOutOfRange;
         else
           off = valid && wr < kw && row_off[t] != kOutOfRange ? row_off[t] + (uint32_t)wr * 16u
                                                               : kOutOfRange;
@@ -864,8 +868,9 @@ __global__ __launch_bounds__(NW * 64) void k_rowmeta(GemmArgs a) {
 // rows 8 (4 s + l / 16) .. +7 in operand order (x0, x4, x1, x5, ...), zero
 // past M or K. A decode wave reads one step of one row tile as one
 // contiguous KiB.
-__global__ void k_gather_prep(const uint16_t* __restrict__ X, int64_t ldx, int M, int K,
-                              const int32_t* __restrict__ perm, uint16_t* __restrict__ Xp) {
+__global__ __launch_bounds__(64) void k_gather_prep(const uint16_t* __restrict__ X, int64_t ldx,
+                                                    int M, int K, const int32_t* __restrict__ perm,
+                                                    uint16_t* __restrict__ Xp) {
   const int kw = K >> 3;
   const int nsteps = 4 * ((K + 127) >> 7);
   const int mt = (M + kTileM - 1) / kTileM;
@@ -882,10 +887,22 @@ __global__ void k_gather_prep(const uint16_t* __restrict__ X, int64_t ldx, int M
     u4_t v = {0u, 0u, 0u, 0u};
     if (m < M && r < kw) {
       const uint16_t* xr = X + (int64_t)m * ldx;
+      uint32_t c[8];
+      if (perm) {
+        const u4_t p0 = *(const u4_t*)(perm + r * 8);
+        const u4_t p1 = *(const u4_t*)(perm + r * 8 + 4);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          c[e] = min(p0[e], kmax);
+          c[e + 4] = min(p1[e], kmax);
+        }
+      } else {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) c[e] = (uint32_t)(r * 8 + e);
+      }
       uint32_t x[8];
 #pragma unroll
-      for (int e = 0; e < 8; ++e)
-        x[e] = xr[perm ? min((uint32_t)perm[r * 8 + e], kmax) : (uint32_t)(r * 8 + e)];
+      for (int e = 0; e < 8; ++e) x[e] = xr[c[e]];
       v = u4_t{x[0] | (x[4] << 16), x[1] | (x[5] << 16), x[2] | (x[6] << 16), x[3] | (x[7] << 16)};
     }
     *(u4_t*)(Xp + i * 8) = v;
@@ -1073,10 +1090,12 @@ hipError_t launch_decode(const GemmArgs& a0, const DecodePlan& p, hipStream_t s)
 hipError_t launch_gather_prep(const uint16_t* X, int64_t ldx, int M, int K, const int32_t* perm,
                               uint16_t* Xp, hipStream_t s) {
   const int64_t total = (int64_t)((M + kTileM - 1) / kTileM) * 4 * ((K + 127) / 128) * 64;
-  int blocks = (int)((total + 255) / 256);
-  if (blocks > 4096) blocks = 4096;
+  // one record per thread, 64-thread workgroups: the work is a few hundred
+  // KiB of dependent loads, so it is spread over as many CUs as it fills
+  int blocks = (int)((total + 63) / 64);
+  if (blocks > 16384) blocks = 16384;
   if (blocks < 1) blocks = 1;
-  hipLaunchKernelGGL(k_gather_prep, dim3(blocks), dim3(256), 0, s, X, ldx, M, K, perm, Xp);
+  hipLaunchKernelGGL(k_gather_prep, dim3(blocks), dim3(64), 0, s, X, ldx, M, K, perm, Xp);
   return hipGetLastError();
 }
 
