@@ -250,30 +250,35 @@ struct MetaStage {
 // AAddr), then a spare entry. With GATHER the operand column k is X column
 // perm[k] (X[:, perm]): the rows of X are first copied to LDS as they are
 // (at xr, [M][K]) and gathered from there, so no global load waits on
-// another. Global loads are buffer loads: items past the end load zeros
-// at no cost and go to the spare entry.
+// another. Global loads are buffer loads: octets past K load zeros at no
+// cost and go to a spare entry.
 template <int NT, bool GATHER>
 struct XStage {
   static constexpr int R = 8;
+  // Slot s holds the 16 bytes of row m, octet r = tid + i * NT, stepping
+  // (m, i) through rows 0..M-1 and passes 0..P-1, P = ceil(kw / NT): the
+  // bookkeeping is wave-uniform, no per-lane division.
   __amdgpu_buffer_rsrc_t rx;
-  u4_t v[R];   // first-pass pieces: item = tid + i * NT, item = m * kw + r
+  u4_t v[R];
   u4_t p[2];   // GATHER: permutation entries of octet tid
-  __device__ __forceinline__ u4_t piece(const GemmArgs& a, int item, int kw) const {
-    const int m = item / kw;
-    const int r = item - m * kw;
-    const uint32_t off = item < a.M * kw ? ((uint32_t)m * (uint32_t)a.ldx + (uint32_t)r * 8u) * 2u
-                                         : kOutOfRange;
+  __device__ __forceinline__ u4_t piece(const GemmArgs& a, int m, int r, int kw) const {
+    const uint32_t off = r < kw ? ((uint32_t)m * (uint32_t)a.ldx + (uint32_t)r * 8u) * 2u
+                                : kOutOfRange;
     return buffer_load16(rx, off);
   }
-  // Pass i (items tid + i * NT) is issued only when some item of it exists:
-  // a wave-uniform test, so the vector memory path is not clogged with
-  // out-of-range loads ahead of the weight stream.
   __device__ __forceinline__ void load(const GemmArgs& a, int tid) {
     const int kw = a.K >> 3;
+    const int P = (kw + NT - 1) / NT;
     rx = buffer_rsrc(a.X, (uint32_t)a.M * (uint32_t)a.ldx * 2u);
+    int m = 0, i = 0;
 #pragma unroll
-    for (int i = 0; i < R; ++i)
-      if (i * NT < a.M * kw) v[i] = piece(a, tid + i * NT, kw);
+    for (int sl = 0; sl < R; ++sl) {
+      if (m < a.M) v[sl] = piece(a, m, tid + i * NT, kw);
+      if (++i == P) {
+        i = 0;
+        ++m;
+      }
+    }
     if (GATHER) {
       const __amdgpu_buffer_rsrc_t rp = buffer_rsrc(a.perm, (uint32_t)a.K * 4u);
       const uint32_t off = tid < kw ? (uint32_t)tid * 32u : kOutOfRange;
@@ -281,35 +286,48 @@ struct XStage {
       p[1] = buffer_load16(rp, off + 16u);
     }
   }
-  // operand entry of (m, r) from a piece of X, or (GATHER) the LDS copy;
-  // items past the end go to the spare entry (xs[spare] or xr[items]).
-  __device__ __forceinline__ static void put(u4_t* xs, u4_t* xr, int M, int kw, int items,
-                                             int spare, int item, const u4_t& x) {
-    if (GATHER) {
-      xr[min(item, items)] = x;
-    } else {
-      const int it = min(item, items - 1);
-      const int m = it / kw;
-      const int r = it - m * kw;
-      xs[item < items ? r * M + m : spare] = permute_octet(x);
-    }
+  // row m, octet r to its operand entry, or (GATHER) to the LDS copy of X;
+  // octets past K go to the spare entry (xs[spare] or xr[M * kw])
+  __device__ __forceinline__ static void put(u4_t* xs, u4_t* xr, int M, int kw, int spare, int m,
+                                             int r, const u4_t& x) {
+    if (GATHER)
+      xr[r < kw ? m * kw + r : M * kw] = x;
+    else
+      xs[r < kw ? r * M + m : spare] = permute_octet(x);
   }
   __device__ __forceinline__ void store(const GemmArgs& a, u4_t* xs, u4_t* xr, int tid) {
     const int kw = a.K >> 3;
     const int M = a.M;
-    const int items = M * kw;
+    const int P = (kw + NT - 1) / NT;
     const int kwp = 16 * ((a.K + 127) >> 7);
     const int spare = kwp * M + 1;  // after the zero entry
-    for (int i = kw * M + tid; i <= kwp * M; i += NT) xs[i] = u4_t{0u, 0u, 0u, 0u};
+    for (int e = kw * M + tid; e <= kwp * M; e += NT) xs[e] = u4_t{0u, 0u, 0u, 0u};
+    int m = 0, i = 0;
 #pragma unroll
-    for (int i = 0; i < R; ++i)
-      if (i * NT < items) put(xs, xr, M, kw, items, spare, tid + i * NT, v[i]);
-    for (int base = tid + R * NT; base < items; base += 4 * NT) {
+    for (int sl = 0; sl < R; ++sl) {
+      if (m < M) put(xs, xr, M, kw, spare, m, tid + i * NT, v[sl]);
+      if (++i == P) {
+        i = 0;
+        ++m;
+      }
+    }
+    // what did not fit in the registers, four loads in flight at a time
+    while (m < M) {
       u4_t t4[4];
+      int mm[4], rr[4];
 #pragma unroll
-      for (int i = 0; i < 4; ++i) t4[i] = piece(a, base + i * NT, kw);
+      for (int q = 0; q < 4; ++q) {
+        mm[q] = m;
+        rr[q] = tid + i * NT;
+        t4[q] = m < M ? piece(a, m, rr[q], kw) : u4_t{0u, 0u, 0u, 0u};
+        if (++i == P) {
+          i = 0;
+          ++m;
+        }
+      }
 #pragma unroll
-      for (int i = 0; i < 4; ++i) put(xs, xr, M, kw, items, spare, base + i * NT, t4[i]);
+      for (int q = 0; q < 4; ++q)
+        if (mm[q] < M) put(xs, xr, M, kw, spare, mm[q], rr[q], t4[q]);
       wait_vmcnt<0>();  // no load of this loop outlives it (see wait_vmcnt)
     }
     if (GATHER) {
@@ -329,13 +347,13 @@ struct XStage {
           c[e] = min(p0[e], kmax);
           c[e + 4] = min(p1[e], kmax);
         }
-        for (int m = 0; m < M; ++m) {
-          const uint16_t* xm = x16 + m * a.K;
+        for (int mr = 0; mr < M; ++mr) {
+          const uint16_t* xm = x16 + mr * a.K;
           // x0, x4, x1, x5, x2, x6, x3, x7
-          xs[r * M + m] = u4_t{xm[c[0]] | ((uint32_t)xm[c[4]] << 16),
-                               xm[c[1]] | ((uint32_t)xm[c[5]] << 16),
-                               xm[c[2]] | ((uint32_t)xm[c[6]] << 16),
-                               xm[c[3]] | ((uint32_t)xm[c[7]] << 16)};
+          xs[r * M + mr] = u4_t{xm[c[0]] | ((uint32_t)xm[c[4]] << 16),
+                                xm[c[1]] | ((uint32_t)xm[c[5]] << 16),
+                                xm[c[2]] | ((uint32_t)xm[c[6]] << 16),
+                                xm[c[3]] | ((uint32_t)xm[c[7]] << 16)};
         }
       }
     }
