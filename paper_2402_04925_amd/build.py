@@ -15,7 +15,7 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 BUILD = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libtpdq.so")
-SOURCES = ["abi.hip", "gemm_decode.hip", "reorder.hip"]
+SOURCES = ["abi.hip", "gemm_decode.hip", "gemm_prefill.hip", "reorder.hip"]
 ARCH = "gfx950"
 
 HIPCC_FLAGS = [

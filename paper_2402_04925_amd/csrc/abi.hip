@@ -71,10 +71,15 @@ tpdq_status check_layer(const tpdq_w4* w, const char* name, bool need_gidx, bool
 
 // Workspace of the GEMM and MLP calls: only the gathered activations, when
 // the gather X[:, perm] cannot be done inside the GEMM's LDS.
-// the prepared operand (k_gather_prep): 16 rows x 128 columns x 2 bytes per
-// (row tile, 128-row block)
+// the activations gathered through a permutation: for the decode kernels the
+// prepared operand (k_gather_prep: 16 rows x 128 columns x 2 bytes per row
+// tile and 128-row block, chunks of 64 rows), for the prefill kernel X[:, P]
+// row-major
 size_t gather_ws_bytes(int M, int K) {
-  return align_up((size_t)((M + kTileM - 1) / kTileM) * ((K + 127) / 128) * 4096);
+  const int mc = std::min(M, kDecodeMaxM);
+  size_t n = align_up((size_t)((mc + kTileM - 1) / kTileM) * ((K + 127) / 128) * 4096);
+  if (M >= kPrefillMinM) n = std::max(n, align_up((size_t)M * K * 2));
+  return n;
 }
 
 int meta_mode(tpdq_path path) {
@@ -91,6 +96,37 @@ tpdq_status run_gemm(const uint16_t* X, int64_t ldx, int M, const int32_t* perm,
                      tpdq_path path, uint16_t* Y, int64_t ldy, char* ws, hipStream_t st) {
   const int meta = meta_mode(path);
   const int32_t* gidx = path == TPDQ_PATH_ORDERED ? nullptr : w->g_idx;
+  if (prefill_supported(M, w->K, w->N, w->group_size, w->layout, meta, w->ld_q)) {
+    // prefill: one MFMA GEMM over all rows, the activations gathered first
+    const uint16_t* Xa = X;
+    int64_t lda = ldx;
+    if (perm) {
+      uint16_t* Xp = (uint16_t*)ws;
+      hipError_t e = launch_gather_rows(X, ldx, M, w->K, perm, Xp, st);
+      if (e != hipSuccess) return hip_fail(e, "activation gather launch");
+      Xa = Xp;
+      lda = w->K;
+    }
+    GemmArgs a{};
+    a.X = Xa;
+    a.ldx = lda;
+    a.M = M;
+    a.qw = (const uint32_t*)w->qweight;
+    a.ldq = w->ld_q;
+    a.sc = (const uint16_t*)w->scales;
+    a.lds = w->ld_s;
+    a.qz = (const uint32_t*)w->qzeros;
+    a.ldz = w->ld_z;
+    a.K = w->K;
+    a.N = w->N;
+    a.G = w->group_size;
+    a.num_groups = w->num_groups;
+    a.Y = Y;
+    a.ldy = ldy;
+    hipError_t e = launch_prefill(a, st);
+    if (e != hipSuccess) return hip_fail(e, "prefill GEMM launch");
+    return TPDQ_OK;
+  }
   for (int m0 = 0; m0 < M; m0 += kDecodeMaxM) {
     const int mc = std::min(kDecodeMaxM, M - m0);
     const uint16_t* Xc = X + (int64_t)m0 * ldx;
@@ -182,10 +218,10 @@ size_t tpdq_workspace_bytes(int op, int32_t M, const tpdq_w4* a, const tpdq_w4* 
     return n;
   }
   if (M < 1) return 0;
-  if (op == 1) return gather_ws_bytes(std::min(M, (int32_t)kDecodeMaxM), a->K);
+  if (op == 1) return gather_ws_bytes(M, a->K);
   if (op == 2) {
     if (!b) return 0;
-    return gather_ws_bytes(std::min(M, (int32_t)kDecodeMaxM), a->K);
+    return gather_ws_bytes(M, a->K);
   }
   return 0;
 }

@@ -91,6 +91,14 @@ hipError_t launch_decode(const GemmArgs& a, const DecodePlan& p, hipStream_t s);
 hipError_t launch_gather_prep(const uint16_t* X, int64_t ldx, int M, int K, const int32_t* perm,
                               uint16_t* Xp, hipStream_t s);
 
+// Prefill GEMM (gemm_prefill.hip): sorted rows, tiled weights, M >= kPrefillMinM.
+constexpr int kPrefillMinM = 256;
+bool prefill_supported(int M, int K, int N, int G, int layout, int meta, int64_t ldq);
+hipError_t launch_prefill(const GemmArgs& a, hipStream_t s);
+// Xp [M][K] = X[:, perm] row-major (for the prefill GEMM's activations)
+hipError_t launch_gather_rows(const uint16_t* X, int64_t ldx, int M, int K, const int32_t* perm,
+                              uint16_t* Xp, hipStream_t s);
+
 // Reorder (device code in reorder.hip).
 struct ReorderLayer {
   const int32_t* g_idx;

@@ -1,0 +1,95 @@
+"""GPU prefill GEMM (ordered path, tiled weights, M >= 256) against the oracle."""
+import numpy as np
+import pytest
+
+from oracle import tpdq_oracle as o
+from paper_2402_04925_amd import inputs
+from tests.gpu_util import TOL_FP16, layer_to_dev, log, np_of, sample_cols, to_dev, torch_dev
+
+pytestmark = pytest.mark.gpu
+
+# K, N, G, M: several 128 x 256 tiles, ragged M, N and K, every group size the
+# kernel handles (G = 256 spans two 128-row blocks)
+SHAPES = [
+    (256, 256, 32, 256), (512, 520, 64, 300), (1024, 1032, 128, 257), (2048, 512, 256, 512),
+    (288, 200, 32, 260), (1152, 768, 128, 640),
+]
+
+
+@pytest.mark.parametrize("K,N,G,M", SHAPES)
+def test_prefill_gemm(K, N, G, M):
+    """Sorted rows from the GPU reorder, X[:, P] gathered in the call, then
+    without the gather (X multiplies the sorted rows directly)."""
+    import torch
+    import paper_2402_04925_amd as tpdq
+    dev = torch_dev()
+    log(f"prefill K={K} N={N} G={G} M={M}")
+    w1, _ = inputs.make_custom(K, N, 0, G, seed=K + N + G + 7)
+    X = inputs.random_activations(M, K, np.random.default_rng(M))
+    P, gs, _, _, wo, _ = tpdq.reorder(layer_to_dev(w1, dev), layout=tpdq.LAYOUT_TILED)
+    Xd = to_dev(X, dev)
+    Y = tpdq.w4a16_gemm(Xd, wo, tpdq.PATH_ORDERED, x_perm=P)
+    torch.cuda.synchronize()
+    ref = o.w4a16_gemm(X, w1.qweight, w1.scales, w1.qzeros, w1.g_idx)
+    assert o.rel_err(np_of(Y), ref) <= TOL_FP16
+    Y2 = tpdq.w4a16_gemm(Xd, wo, tpdq.PATH_ORDERED)
+    torch.cuda.synchronize()
+    eP, eg = o.reorder(w1.g_idx)
+    ws = o.permute_rows(dict(qweight=w1.qweight, scales=w1.scales, qzeros=w1.qzeros), eP)
+    ref2 = o.w4a16_gemm(X, ws["qweight"], ws["scales"], ws["qzeros"], eg)
+    assert o.rel_err(np_of(Y2), ref2) <= TOL_FP16
+
+
+def test_prefill_zero_codes():
+    """q == z everywhere -> Y == 0 exactly (the fp16 weights are exact zeros)."""
+    import torch
+    import paper_2402_04925_amd as tpdq
+    dev = torch_dev()
+    K, N, M = 512, 256, 256
+    z = np.random.default_rng(1).integers(0, 16, size=(K // 128, N))
+    qz = o.pack_cols(z)
+    qw = o.pack_rows(np.repeat(z, 128, axis=0))
+    s = inputs.random_scales((K // 128, N), np.random.default_rng(2))
+    w = tpdq.QuantWeight.from_tensors(to_dev(qw, dev), to_dev(s, dev), to_dev(qz, dev), None, 128)
+    wt = tpdq.pack_tiled(w)
+    X = to_dev(inputs.random_activations(M, K, np.random.default_rng(3)), dev)
+    Y = tpdq.w4a16_gemm(X, wt, tpdq.PATH_ORDERED)
+    torch.cuda.synchronize()
+    assert np.all(np_of(Y) == 0)
+
+
+def test_prefill_mlp_llama_tp2():
+    """The Llama-70B TP = 2 prefill shard (M = 2048, W1 8192 x 14336, W2 14336 x
+    8192) through tpdq_mlp_shard. Y1 is checked on sampled columns against the
+    oracle; Y2_partial on sampled columns against the oracle applied to the
+    fp16 Y1 the GPU produced (the oracle's GEMM2 input is that same fp16
+    tensor)."""
+    import torch
+    import paper_2402_04925_amd as tpdq
+    from tests.gpu_util import workload_layers
+    dev = torch_dev()
+    wl = inputs.WORKLOADS["llama70b_tp2_prefill"]
+    M = wl.Ms[0]
+    log(f"prefill mlp {wl.name} M={M}")
+    L1, L2 = workload_layers(wl.name)
+    X = inputs.make_x(wl, M)
+    d1, d2 = layer_to_dev(L1, dev), layer_to_dev(L2, dev)
+    P1, _, P2, _, w1o, w2o = tpdq.reorder(d1, d2)
+    s1 = w1o.column_shard(0, wl.tp)
+    s2 = w2o.row_shard(0, wl.tp, sorted_rows=True)
+    Y1, Y2 = tpdq.mlp_shard(to_dev(X, dev), s1, s2, tpdq.PATH_ORDERED, P1=P1)
+    torch.cuda.synchronize()
+    Y1h, Y2h = np_of(Y1), np_of(Y2)
+    rng = np.random.default_rng(11)
+    eP1, _ = o.reorder(L1.g_idx)
+    eP2, _ = o.reorder(L2.g_idx)
+    n1 = L1.N // wl.tp
+    cols1 = sample_cols(n1, rng)
+    # column c of rank 0's Y1 is column P2[c] of X @ deq(W1) (the fold)
+    ref1 = o.w4a16_gemm(X, L1.qweight, L1.scales, L1.qzeros, L1.g_idx, cols=eP2[cols1])
+    assert o.rel_err(Y1h[:, cols1], ref1) <= TOL_FP16
+    cols2 = sample_cols(L2.N, rng)
+    k2 = L2.K // wl.tp
+    W2 = o.dequant(L2.qweight, L2.scales, L2.qzeros, L2.g_idx, cols=cols2)[eP2[:k2]]
+    ref2 = o.to_fp16(o.matmul(Y1h.astype(np.float64), W2))
+    assert o.rel_err(Y2h[:, cols2], ref2) <= TOL_FP16
