@@ -67,7 +67,12 @@ typedef enum { TPDQ_FP16 = 0, TPDQ_BF16 = 1 } tpdq_dtype;
  *   ld_q >= ceil(K/128)*256; for 16-column tile t, 128-row block b, lane
  *   l = 16*kq + j (0 <= j < 16, 0 <= kq < 4) and step u (0 <= u < 4):
  *     tiled[t][256*b + 4*l + u] = gptq[4*(4*b + u) + kq][16*t + j]
- *   Words of rows at or beyond K (padding of the last block) are zero. A row
+ *   with the eight codes of each word reordered: the code of row 8r + i
+ *   (bits 4i of the GPTQ word) sits at bits 4*(i/2) + 16*(i%2), i.e. rows
+ *   8r, 8r+2, 8r+4, 8r+6 in the low half-word and 8r+1, 8r+3, 8r+5, 8r+7 in
+ *   the high one, so that the two codes under one 16-bit mask are
+ *   consecutive rows. Words of rows at or beyond K (padding of the last
+ *   block) are zero. A row
  *   shard starting at a multiple of 128 rows is the view qweight + 256*(k0/128)
  *   with the same ld_q; a column shard starting at a multiple of 16 columns is
  *   qweight + ld_q*(c0/16). Produced by tpdq_reorder or tpdq_pack_tiled. */

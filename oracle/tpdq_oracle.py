@@ -81,17 +81,42 @@ def tiled_ld(K: int) -> int:
     return (K + 127) // 128 * 256
 
 
+def _tiled_nibble_shifts():
+    """Bit position, in a tiled word, of the code of row 8 r + i: even rows in
+    the low half-word, odd rows in the high one (i // 2 nibbles up)."""
+    return [4 * (i // 2) + 16 * (i % 2) for i in range(8)]
+
+
+def interleave_word(w: np.ndarray) -> np.ndarray:
+    """GPTQ words (row 8 r + i at bits 4 i) -> the tiled nibble order."""
+    w = np.asarray(w).view(np.uint32)
+    out = np.zeros_like(w)
+    for i, sh in enumerate(_tiled_nibble_shifts()):
+        out |= ((w >> np.uint32(4 * i)) & np.uint32(0xF)) << np.uint32(sh)
+    return out
+
+
+def deinterleave_word(w: np.ndarray) -> np.ndarray:
+    """Inverse of interleave_word."""
+    w = np.asarray(w).view(np.uint32)
+    out = np.zeros_like(w)
+    for i, sh in enumerate(_tiled_nibble_shifts()):
+        out |= ((w >> np.uint32(sh)) & np.uint32(0xF)) << np.uint32(4 * i)
+    return out
+
+
 def untile(qt: np.ndarray, K: int, N: int) -> np.ndarray:
     """GPTQ words [K/8][N] of a qweight stored in the tiled order: for tile t
     (16 columns), block b (128 rows), lane l = 16 kq + j and step u,
-    tiled[t][256 b + 4 l + u] is GPTQ word [4 (4 b + u) + kq][16 t + j]."""
+    tiled[t][256 b + 4 l + u] is GPTQ word [4 (4 b + u) + kq][16 t + j] with
+    its codes interleaved (interleave_word)."""
     qt = np.asarray(qt).view(np.uint32)
     r = np.arange(K // 8)[:, None]
     c = np.arange(N)[None, :]
     s, kq = r // 4, r % 4
     b, u = s // 4, s % 4
     t, jj = c // 16, c % 16
-    return qt[t, 256 * b + 4 * (16 * kq + jj) + u].view(np.int32)
+    return deinterleave_word(qt[t, 256 * b + 4 * (16 * kq + jj) + u]).view(np.int32)
 
 
 def tile(qw: np.ndarray) -> np.ndarray:
@@ -105,7 +130,7 @@ def tile(qw: np.ndarray) -> np.ndarray:
     s, kq = r // 4, r % 4
     b, u = s // 4, s % 4
     t, jj = c // 16, c % 16
-    out[t, 256 * b + 4 * (16 * kq + jj) + u] = qw
+    out[t, 256 * b + 4 * (16 * kq + jj) + u] = interleave_word(qw)
     return out.view(np.int32)
 
 

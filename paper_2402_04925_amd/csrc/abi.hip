@@ -96,7 +96,7 @@ tpdq_status run_gemm(const uint16_t* X, int64_t ldx, int M, const int32_t* perm,
                      tpdq_path path, uint16_t* Y, int64_t ldy, char* ws, hipStream_t st) {
   const int meta = meta_mode(path);
   const int32_t* gidx = path == TPDQ_PATH_ORDERED ? nullptr : w->g_idx;
-  if (prefill_supported(M, w->K, w->N, w->group_size, w->layout, meta, w->ld_q)) {
+  if (prefill_supported(M, perm ? (int64_t)w->K : ldx, w, meta)) {
     // prefill: one MFMA GEMM over all rows, the activations gathered first
     const uint16_t* Xa = X;
     int64_t lda = ldx;
@@ -139,7 +139,7 @@ tpdq_status run_gemm(const uint16_t* X, int64_t ldx, int M, const int32_t* perm,
       ok = plan_decode(mc, w->K, w->N, w->group_size, w->num_groups, w->layout, meta, operand, &plan);
       if (!ok) {
         uint16_t* Xp = (uint16_t*)ws;
-        hipError_t e = launch_gather_prep(Xc, ldx, mc, w->K, perm, Xp, st);
+        hipError_t e = launch_gather_prep(Xc, ldx, mc, w->K, perm, w->layout, Xp, st);
         if (e != hipSuccess) return hip_fail(e, "activation gather launch");
         Xc = Xp;
         ldc = w->K;

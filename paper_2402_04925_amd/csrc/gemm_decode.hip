@@ -118,14 +118,15 @@ struct MetaStage {
 };
 
 // Activations in operand order: LDS entry (r * M + m) holds row m, rows
-// 8r..8r+7 of the operand, permuted as x0, x4, x1, x5, x2, x6, x3, x7, for
-// r < 16 * ceil(K / 128) (zero past K). One more zero entry follows (see
+// 8r..8r+7 of the operand (permuted as x0, x4, x1, x5, x2, x6, x3, x7 for
+// GPTQ weights, as they are for tiled ones), for r < 16 * ceil(K / 128)
+// (zero past K). One more zero entry follows (see
 // AAddr), then a spare entry. With GATHER the operand column k is X column
 // perm[k] (X[:, perm]): the rows of X are first copied to LDS as they are
 // (at xr, [M][K]) and gathered from there, so no global load waits on
 // another. Global loads are buffer loads: octets past K load zeros at no
 // cost and go to a spare entry.
-template <int NT, bool GATHER>
+template <int NT, bool GATHER, int LAYOUT>
 struct XStage {
   static constexpr int R = 8;
   // Slot s holds the 16 bytes of row m, octet r = tid + i * NT, stepping
@@ -166,7 +167,7 @@ struct XStage {
     if (GATHER)
       xr[r < kw ? m * kw + r : M * kw] = x;
     else
-      xs[r < kw ? r * M + m : spare] = permute_octet(x);
+      xs[r < kw ? r * M + m : spare] = to_operand<LAYOUT>(x);
   }
   __device__ __forceinline__ void store(const GemmArgs& a, u4_t* xs, u4_t* xr, int tid) {
     const int kw = a.K >> 3;
@@ -222,11 +223,10 @@ struct XStage {
         }
         for (int mr = 0; mr < M; ++mr) {
           const uint16_t* xm = x16 + mr * a.K;
-          // x0, x4, x1, x5, x2, x6, x3, x7
-          xs[r * M + mr] = u4_t{xm[c[0]] | ((uint32_t)xm[c[4]] << 16),
-                                xm[c[1]] | ((uint32_t)xm[c[5]] << 16),
-                                xm[c[2]] | ((uint32_t)xm[c[6]] << 16),
-                                xm[c[3]] | ((uint32_t)xm[c[7]] << 16)};
+          xs[r * M + mr] = to_operand<LAYOUT>(u4_t{xm[c[0]] | ((uint32_t)xm[c[1]] << 16),
+                                                   xm[c[2]] | ((uint32_t)xm[c[3]] << 16),
+                                                   xm[c[4]] | ((uint32_t)xm[c[5]] << 16),
+                                                   xm[c[6]] | ((uint32_t)xm[c[7]] << 16)});
         }
       }
     }
@@ -286,8 +286,8 @@ __device__ __forceinline__ u4_t load_block(const GemmArgs& a, const uint32_t* qc
 }
 
 // A fragments of one block from global memory (rows t*16 + j, 8 halfs each),
-// permuted into operand order unless the operand already is (kAGlobalPrep).
-template <int MT, int AM>
+// in operand order (the prepared operand already is).
+template <int MT, int AM, int LAYOUT>
 __device__ __forceinline__ void load_a_block(const GemmArgs& a, int j, int kq, int b, bool ok,
                                              int kw, u4_t (&x)[4][MT]) {
 #pragma unroll
@@ -305,7 +305,7 @@ __device__ __forceinline__ void load_a_block(const GemmArgs& a, int j, int kq, i
         const u4_t v = (ok && wr < kw && row < a.M)
                            ? *(const u4_t*)(a.X + (int64_t)row * a.ldx + wr * 8)
                            : u4_t{0u, 0u, 0u, 0u};
-        x[u][t] = permute_octet(v);
+        x[u][t] = to_operand<LAYOUT>(v);
       }
     }
   }
@@ -352,9 +352,9 @@ struct WeightStream {
 };
 
 // A fragments of block b from global memory: row t*16 + j, rows 8 (4 (4b + u)
-// + kq) .. +7, as stored (the consumer permutes them into operand order
-// unless they already are, kAGlobalPrep: permuting at the load would make
-// the load be waited for at once).
+// + kq) .. +7, as stored (for GPTQ weights the consumer permutes them into
+// operand order unless they already are, kAGlobalPrep: permuting at the load
+// would make the load be waited for at once).
 // Rows past M read zeros from the resource bound; columns past K are zeroed.
 // kAGlobalPrep reads the prepared operand (k_gather_prep): 16-byte records
 // [row tile t][step s][lane], one contiguous KiB per load instruction, in
@@ -506,7 +506,7 @@ __global__ __launch_bounds__(NW * 64) void k_ordered(GemmArgs a) {
   //    LDS), the first chunk's scales and zeros, the first D weight blocks
   //    (the scheduling barriers keep that issue order: loads complete in
   //    order, so a load moved behind the weights would be waited for last)
-  XStage<NT, AM == kALdsGather> xst;
+  XStage<NT, AM == kALdsGather, LAYOUT> xst;
   if constexpr (!AG) xst.load(a, tid);
   __builtin_amdgcn_sched_barrier(0);
   ChunkMeta<SPG> cm[TN];
@@ -595,7 +595,7 @@ __global__ __launch_bounds__(NW * 64) void k_ordered(GemmArgs a) {
       h8_t av[MT];
 #pragma unroll
       for (int t = 0; t < MT; ++t)
-        av[t] = AG ? as_h8(AM == kAGlobalPrep ? av_g[u][t] : permute_octet(av_g[u][t]))
+        av[t] = AG ? as_h8(AM == kAGlobalPrep ? av_g[u][t] : to_operand<LAYOUT>(av_g[u][t]))
                    : as_h8(xs[aa[t].base + aa[t].stride * st]);
 #pragma unroll
       for (int n = 0; n < TN; ++n) {
@@ -667,7 +667,7 @@ __global__ __launch_bounds__(NW * 64) void k_rowmeta(GemmArgs a) {
 
   MetaStage<NT, 8, 0> ms;
   if constexpr (META == kMetaRowLds) ms.load(a, n0, a.meta_rows, tid);
-  XStage<NT, false> xst;
+  XStage<NT, false, LAYOUT> xst;
   if constexpr (!AG) xst.load(a, tid);
 
   auto load_g = [&](int b, u4_t (&g)[4][2]) {
@@ -681,7 +681,7 @@ __global__ __launch_bounds__(NW * 64) void k_rowmeta(GemmArgs a) {
   u4_t gb[4][2];
   load_g(b0, gb);
   u4_t ab[4][MT];
-  if constexpr (AG) load_a_block<MT, AM>(a, j, kq, b0, b0 < b1, kw, ab);
+  if constexpr (AG) load_a_block<MT, AM, LAYOUT>(a, j, kq, b0, b0 < b1, kw, ab);
 
   if constexpr (META == kMetaRowLds) ms.store(a, meta, n0, a.meta_rows, tid);
   if constexpr (!AG) xst.store(a, xs, nullptr, tid);
@@ -703,7 +703,7 @@ __global__ __launch_bounds__(NW * 64) void k_rowmeta(GemmArgs a) {
     if (more) {
       wn = load_block<LAYOUT>(a, qcol, qtile, lane, kq, b + 1, wok, kw);
       load_g(b + 1, gn);
-      if constexpr (AG) load_a_block<MT, AM>(a, j, kq, b + 1, true, kw, an);
+      if constexpr (AG) load_a_block<MT, AM, LAYOUT>(a, j, kq, b + 1, true, kw, an);
     }
 #pragma unroll
     for (int u = 0; u < 4; ++u) {
@@ -729,7 +729,7 @@ __global__ __launch_bounds__(NW * 64) void k_rowmeta(GemmArgs a) {
           zr[r] = col_ok ? (a.qz[(int64_t)g * a.ldz + (col >> 3)] >> zshift) & 0xFu : 0u;
         }
       }
-      const h8_t bv = dequant_rows(kc, wb[u], zr, sr);
+      const h8_t bv = dequant_rows<LAYOUT == TPDQ_LAYOUT_TILED>(kc, wb[u], zr, sr);
 #pragma unroll
       for (int t = 0; t < MT; ++t) acc[t] = mfma16x16x32(av[t], bv, acc[t]);
     }
@@ -756,12 +756,12 @@ __global__ __launch_bounds__(NW * 64) void k_rowmeta(GemmArgs a) {
 
 // The prepared operand: X'[m][k] = X[m][perm[k]] (perm NULL: X itself) as
 // 16-byte records [row tile t][step s][lane l]: row 16 t + l % 16, operand
-// rows 8 (4 s + l / 16) .. +7 in operand order (x0, x4, x1, x5, ...), zero
-// past M or K. A decode wave reads one step of one row tile as one
+// rows 8 (4 s + l / 16) .. +7 in operand order (natural for tiled weights,
+// x0, x4, x1, x5, ... for GPTQ ones), zero past M or K. A decode wave reads one step of one row tile as one
 // contiguous KiB.
 __global__ __launch_bounds__(64) void k_gather_prep(const uint16_t* __restrict__ X, int64_t ldx,
                                                     int M, int K, const int32_t* __restrict__ perm,
-                                                    uint16_t* __restrict__ Xp) {
+                                                    int natural, uint16_t* __restrict__ Xp) {
   const int kw = K >> 3;
   const int nsteps = 4 * ((K + 127) >> 7);
   const int mt = (M + kTileM - 1) / kTileM;
@@ -794,7 +794,8 @@ __global__ __launch_bounds__(64) void k_gather_prep(const uint16_t* __restrict__
       uint32_t x[8];
 #pragma unroll
       for (int e = 0; e < 8; ++e) x[e] = xr[c[e]];
-      v = u4_t{x[0] | (x[4] << 16), x[1] | (x[5] << 16), x[2] | (x[6] << 16), x[3] | (x[7] << 16)};
+      v = natural ? u4_t{x[0] | (x[1] << 16), x[2] | (x[3] << 16), x[4] | (x[5] << 16), x[6] | (x[7] << 16)}
+                  : u4_t{x[0] | (x[4] << 16), x[1] | (x[5] << 16), x[2] | (x[6] << 16), x[3] | (x[7] << 16)};
     }
     *(u4_t*)(Xp + i * 8) = v;
   }
@@ -979,14 +980,15 @@ hipError_t launch_decode(const GemmArgs& a0, const DecodePlan& p, hipStream_t s)
 }
 
 hipError_t launch_gather_prep(const uint16_t* X, int64_t ldx, int M, int K, const int32_t* perm,
-                              uint16_t* Xp, hipStream_t s) {
+                              int layout, uint16_t* Xp, hipStream_t s) {
   const int64_t total = (int64_t)((M + kTileM - 1) / kTileM) * 4 * ((K + 127) / 128) * 64;
   // one record per thread, 64-thread workgroups: the work is a few hundred
   // KiB of dependent loads, so it is spread over as many CUs as it fills
   int blocks = (int)((total + 63) / 64);
   if (blocks > 16384) blocks = 16384;
   if (blocks < 1) blocks = 1;
-  hipLaunchKernelGGL(k_gather_prep, dim3(blocks), dim3(64), 0, s, X, ldx, M, K, perm, Xp);
+  hipLaunchKernelGGL(k_gather_prep, dim3(blocks), dim3(64), 0, s, X, ldx, M, K, perm,
+                     layout == TPDQ_LAYOUT_TILED ? 1 : 0, Xp);
   return hipGetLastError();
 }
 

@@ -3,19 +3,24 @@
 //
 // At M in the thousands the product is a dense contraction and the MFMA pipe
 // bounds it (2 M K N flops against K N / 2 bytes of weights), so the kernel
-// is a classic register-blocked MFMA GEMM:
-//   * a workgroup computes a 128 x 256 tile of Y with 8 waves, each a 64 x 64
-//     sub-tile (4 row tiles x 4 column tiles of v_mfma_f32_16x16x32_f16), so
-//     that two waves share each SIMD and hide each other's load latency;
+// is a register-blocked MFMA GEMM:
+//   * a workgroup of 4 waves computes a 128 x 256 tile of Y; each wave owns
+//     64 columns over all 128 rows (8 row tiles x 4 column tiles of
+//     v_mfma_f32_16x16x32_f16), so that each dequantized weight fragment feeds
+//     8 MFMAs: the unpack and scaling cost about 1.6 VALU per MFMA;
 //   * K advances one 128-row block at a time (4 MFMA steps of 32 rows);
-//   * the activations of the block (128 rows x 128 columns, fp16) are staged
-//     in LDS in MFMA operand order, double-buffered so that the next block's
-//     loads overlap the current block's MFMAs;
-//   * the weights go straight from the tiled layout to registers (one 16-byte
-//     load per lane per 16-column tile and block), are unpacked to exact
-//     q - z and scaled to fp16 (s (q - z)) right before the MFMA; one
-//     (scale, zero) per column and group comes from LDS, staged with the
-//     activations.
+//   * every operand goes from global memory straight to LDS (buffer loads
+//     with the LDS bit, one record of 64 lanes per instruction): activations
+//     laid out as the A operand, the wave's weights as they are tiled (one
+//     16-byte record per lane and 16-column tile: the B operand), the scales
+//     and zeros of the wave's columns; nothing is staged through registers,
+//     so the loop keeps one copy of the accumulators;
+//   * three stages: while block b is multiplied, blocks b + 1 and b + 2 are in
+//     flight; one barrier per block hands a stage from its loads to its
+//     readers and back.
+// The waits are explicit: loads complete in order, so before block b each
+// wave waits until only the loads of block b + 1 are outstanding, and the
+// barrier then makes every wave's LDS writes of block b visible.
 // Dequantizing to fp16 before the MFMA rounds each weight once (relative
 // error 2^-12); the decode kernels keep q - z exact and scale in fp32, but
 // here that would double the accumulator registers and the VALU work per
@@ -25,18 +30,37 @@
 namespace tpdq {
 namespace {
 
-constexpr int kPBM = 128;  // rows of Y per workgroup
+constexpr int kPBM = 128;  // rows of Y per workgroup (8 row tiles)
 constexpr int kPBN = 256;  // columns of Y per workgroup (16 tiles of 16)
-constexpr int kPNW = 8;    // waves: 2 (rows) x 4 (columns)
+constexpr int kPNW = 4;    // waves, each 64 columns x 128 rows
 constexpr int kPWT = 4;    // column tiles per wave
+constexpr int kPRT = 8;    // row tiles per wave
 constexpr int kPNT = kPNW * 64;
-// LDS: two activation buffers [8 row tiles][4 steps][64 lanes] x 16 B and
-// two metadata buffers [4 groups][256 columns] x 4 B
-constexpr int kPAbuf = 8 * 4 * 64 * 16;
-constexpr int kPMbuf = 4 * kPBN * 4;
-constexpr int kPLds = 2 * kPAbuf + 2 * kPMbuf;
+constexpr int kPStages = 3;
+// LDS per stage: activations [8 row tiles][4 steps][64 lanes] x 16 B, then per
+// wave its weights [4 tiles][64 lanes] x 16 B and its metadata: scales
+// [groups][64 columns] x 2 B (two 256-byte records at most) and zeros
+// [groups][8 words] x 4 B (one 256-byte record)
+constexpr int kPAbytes = kPRT * 4 * 64 * 16;
+constexpr int kPWwave = kPWT * 64 * 16;
+constexpr int kPMwave = 3 * 256;
+constexpr int kPStage = kPAbytes + kPNW * (kPWwave + kPMwave);
+constexpr int kPLds = kPStages * kPStage;
 
-// fp16 x2 of the dequantized weights: (q - z) * s
+typedef __attribute__((address_space(3))) void* lds_ptr_t;
+
+// Buffer load of `bytes` per lane straight into LDS: lane l's data lands at
+// dst + bytes * l (dst is wave-uniform).
+template <int BYTES>
+__device__ __forceinline__ void dma_to_lds(__amdgpu_buffer_rsrc_t r, void* dst, uint32_t off) {
+  static_assert(BYTES == 4 || BYTES == 16, "4- or 16-byte records");
+  if constexpr (BYTES == 16)
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_ptr_t)dst, 16, off, 0, 0, 0);
+  else
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_ptr_t)dst, 4, off, 0, 0, 0);
+}
+
+// fp16 x8 of the dequantized weights: (q - z) * s
 __device__ __forceinline__ h8_t dequant_scaled(const UnpackConsts& kc, uint32_t w, uint32_t z1024,
                                                uint32_t z64, uint32_t s2) {
   const h8_t d = unpack_sub(kc, w, z1024, z64);
@@ -48,100 +72,107 @@ __device__ __forceinline__ h8_t dequant_scaled(const UnpackConsts& kc, uint32_t 
 template <int SPG>
 __global__ __launch_bounds__(kPNT) void k_prefill(GemmArgs a) {
   // groups per 128-row block: G = 32, 64, 128 -> 4, 2, 1; G = 256 -> one
-  // group spans two blocks
+  // group spans two blocks (each block stages it)
   constexpr int GPK = SPG >= 4 ? 1 : 4 / SPG;
+  constexpr int NSD = (GPK + 1) / 2;  // scale records per wave and block
+  // loads per wave and block, in issue order: activations, scales, zeros,
+  // weights
+  constexpr int LPB = 2 * 4 + NSD + 1 + kPWT;
   extern __shared__ __align__(16) unsigned char smem[];
-  u4_t* abuf[2] = {(u4_t*)smem, (u4_t*)(smem + kPAbuf)};
-  uint32_t* mbuf[2] = {(uint32_t*)(smem + 2 * kPAbuf), (uint32_t*)(smem + 2 * kPAbuf + kPMbuf)};
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int j = lane & 15;
   const int kq = lane >> 4;
-  const int wm = wave & 1, wn = wave >> 1;
-  const int nbn = (a.N + kPBN - 1) / kPBN;
-  const int bm = blockIdx.x / nbn;
-  const int bn = blockIdx.x - bm * nbn;
+  const int nbm = (a.M + kPBM - 1) / kPBM;
+  const int lt = xcd_tile(blockIdx.x, gridDim.x);
+  const int bn = lt / nbm;
+  const int bm = lt - bn * nbm;
   const int row0 = bm * kPBM;
   const int col0 = bn * kPBN;
-  const int kw = a.K >> 3;
+  const int cw = col0 + 64 * wave;  // the wave's first column
   const int nblk = (a.K + 127) >> 7;
   const int ng = a.num_groups;
   const int ntiles = (a.N + kTileN - 1) / kTileN;
   const UnpackConsts kc;
 
-  // sources (buffer resources: rows past M, columns past N and octets past K
-  // load zeros)
-  const __amdgpu_buffer_rsrc_t rx = buffer_rsrc(a.X, (uint32_t)a.M * (uint32_t)a.ldx * 2u);
-  const __amdgpu_buffer_rsrc_t rw =
-      buffer_rsrc(a.qw, (uint32_t)ntiles * (uint32_t)a.ldq * 4u);
+  // sources: rows past M, groups past the last one and tiles past N load
+  // zeros from the resource bounds
+  const __amdgpu_buffer_rsrc_t rx =
+      buffer_rsrc(a.X + (int64_t)row0 * a.ldx, (uint32_t)(a.M - row0) * (uint32_t)a.ldx * 2u);
+  const __amdgpu_buffer_rsrc_t rw = buffer_rsrc(a.qw, (uint32_t)ntiles * (uint32_t)a.ldq * 4u);
   const __amdgpu_buffer_rsrc_t rs = buffer_rsrc(a.sc, (uint32_t)ng * (uint32_t)a.lds * 2u);
   const __amdgpu_buffer_rsrc_t rz = buffer_rsrc(a.qz, (uint32_t)ng * (uint32_t)a.ldz * 4u);
 
-  // activation piece p (0..3) of this thread: row tid / 16 + 32 p of the
-  // tile, octet tid % 16 of the block
-  constexpr int AP = kPBM * 16 / kPNT;
-  const int a_oct = tid & 15;
-  auto load_a = [&](int b, u4_t (&x)[AP]) {
-    const int o = 16 * b + a_oct;
+  // per-lane parts of the offsets
+  // activations: record (rt, u) of block b, lane l = row 16 rt + l % 16,
+  // columns 128 b + 32 u + 8 (l / 16) .. +7
+  const uint32_t x_lane = ((uint32_t)j * (uint32_t)a.ldx + 8u * (uint32_t)kq) * 2u;
+  const uint32_t x_rt = 16u * (uint32_t)a.ldx * 2u;
+  // scales: record d, lane l = group 2 d + l / 32, columns 2 (l % 32), +1
+  const uint32_t s_lane = (uint32_t)(lane >> 5) * (uint32_t)a.lds * 2u +
+                          ((uint32_t)cw + 2u * (uint32_t)(lane & 31)) * 2u;
+  // zeros: lane l = group l / 8, word l % 8 of the wave's 8
+  const uint32_t z_lane =
+      ((uint32_t)(lane >> 3) * (uint32_t)a.ldz + (uint32_t)(cw >> 3) + (uint32_t)(lane & 7)) * 4u;
+  const bool z_used = (lane >> 3) < GPK;
+  // weights: tile (cw / 16 + i), block b: lane l's 16 bytes
+  const uint32_t w_lane = ((uint32_t)(cw >> 4) * (uint32_t)a.ldq + 4u * (uint32_t)lane) * 4u;
+  const uint32_t w_tile = (uint32_t)a.ldq * 4u;
+
+  // block b (b >= nblk: zeros, no traffic) into LDS stage `st`
+  auto issue = [&](int b, int st) {
+    unsigned char* sb = smem + st * kPStage;
 #pragma unroll
-    for (int p = 0; p < AP; ++p) {
-      const int r = row0 + (tid >> 4) + (kPNT / 16) * p;
-      const uint32_t off = (r < a.M && o < kw) ? ((uint32_t)r * (uint32_t)a.ldx + (uint32_t)o * 8u) * 2u
-                                               : kOutOfRange;
-      x[p] = buffer_load16(rx, off);
+    for (int r = 0; r < 2; ++r) {
+      const int rt = 2 * wave + r;
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const bool ok = 128 * b + 32 * u < a.K;
+        const uint32_t off = ok ? x_lane + (uint32_t)rt * x_rt + (uint32_t)(128 * b + 32 * u) * 2u
+                                : kOutOfRange;
+        dma_to_lds<16>(rx, sb + (rt * 4 + u) * 1024, off);
+      }
     }
-  };
-  auto store_a = [&](u4_t* dst, const u4_t (&x)[AP]) {
-    // record [row tile][step][lane]: lane = 16 (octet % 4) + row % 16
+    unsigned char* wb = sb + kPAbytes + wave * (kPWwave + kPMwave);
+    unsigned char* mb = wb + kPWwave;
+    const int g0 = (128 * b) / (32 * SPG);
+    const bool bok = b < nblk;
 #pragma unroll
-    for (int p = 0; p < AP; ++p) {
-      const int r = (tid >> 4) + (kPNT / 16) * p;
-      dst[((r >> 4) * 4 + (a_oct >> 2)) * 64 + (a_oct & 3) * 16 + (r & 15)] = permute_octet(x[p]);
+    for (int d = 0; d < NSD; ++d) {
+      const int gi = 2 * d + (lane >> 5);
+      const bool ok = bok && gi < GPK && g0 + gi < ng;
+      const uint32_t off = ok ? s_lane + (uint32_t)(g0 + 2 * d) * (uint32_t)a.lds * 2u : kOutOfRange;
+      dma_to_lds<4>(rs, mb + d * 256, off);
     }
-  };
-  // metadata of the groups of block b for column col0 + tid
-  // (threads tid < 256: one column each)
-  auto load_m = [&](int b, uint32_t (&sv)[GPK], uint32_t (&zv)[GPK]) {
-    const int c = col0 + tid;
-    const int gb = (4 * b) / SPG;
-#pragma unroll
-    for (int gi = 0; gi < GPK; ++gi) {
-      const int g = gb + gi;
-      const bool ok = tid < kPBN && c < a.N && g < ng;
-      sv[gi] = buffer_load2(rs, ok ? ((uint32_t)g * (uint32_t)a.lds + (uint32_t)c) * 2u : kOutOfRange);
-      zv[gi] = buffer_load4(rz, ok ? ((uint32_t)g * (uint32_t)a.ldz + (uint32_t)(c >> 3)) * 4u
-                                   : kOutOfRange);
+    {
+      const bool ok = bok && z_used && g0 + (lane >> 3) < ng;
+      const uint32_t off = ok ? z_lane + (uint32_t)g0 * (uint32_t)a.ldz * 4u : kOutOfRange;
+      dma_to_lds<4>(rz, mb + 512, off);
     }
-  };
-  auto store_m = [&](uint32_t* dst, const uint32_t (&sv)[GPK], const uint32_t (&zv)[GPK]) {
-    const uint32_t shift = 4u * (uint32_t)((col0 + tid) & 7);
-#pragma unroll
-    for (int gi = 0; gi < GPK; ++gi)
-      if (tid < kPBN) dst[gi * kPBN + tid] = (sv[gi] & 0xFFFFu) | (((zv[gi] >> shift) & 0xFu) << 16);
-  };
-  // weights of block b for the wave's column tiles
-  const int tw0 = col0 / kTileN + wn * kPWT;
-  auto load_w = [&](int b, u4_t (&w)[kPWT]) {
 #pragma unroll
     for (int i = 0; i < kPWT; ++i) {
-      const int t = tw0 + i;
-      const uint32_t off = (t < ntiles && b < nblk)
-                               ? ((uint32_t)t * (uint32_t)a.ldq + (uint32_t)b * 256u + (uint32_t)lane * 4u) * 4u
-                               : kOutOfRange;
-      w[i] = buffer_load16<kNonTemporal>(rw, off);
+      uint32_t off = bok ? w_lane + (uint32_t)i * w_tile + (uint32_t)b * 1024u : kOutOfRange;
+      asm("" : "+v"(off));  // one load with a selected offset, not one per outcome
+      dma_to_lds<16>(rw, wb + i * 1024, off);
     }
   };
 
-  f4_t acc[4][kPWT];
+  f4_t acc[kPRT][kPWT];
 #pragma unroll
-  for (int r = 0; r < 4; ++r)
+  for (int r = 0; r < kPRT; ++r)
 #pragma unroll
     for (int i = 0; i < kPWT; ++i) acc[r][i] = f4_t{0.f, 0.f, 0.f, 0.f};
 
-  // one block: 4 steps of 32 rows from LDS buffer `ab`, weights w
-  auto compute = [&](int b, const u4_t* ab, const uint32_t* mb, const u4_t (&w)[kPWT]) {
+  // one block from LDS stage `st`
+  auto compute = [&](int st) {
+    const u4_t* ab = (const u4_t*)(smem + st * kPStage);
+    const u4_t* wb = (const u4_t*)(smem + st * kPStage + kPAbytes + wave * (kPWwave + kPMwave));
+    const unsigned char* mb = (const unsigned char*)wb + kPWwave;
+    u4_t w[kPWT];
+#pragma unroll
+    for (int i = 0; i < kPWT; ++i) w[i] = wb[i * 64 + lane];
     uint32_t z1024[kPWT], z64[kPWT], s2[kPWT];
 #pragma unroll
     for (int u = 0; u < 4; ++u) {
@@ -150,71 +181,57 @@ __global__ __launch_bounds__(kPNT) void k_prefill(GemmArgs a) {
         const int gi = SPG >= 4 ? 0 : u / SPG;
 #pragma unroll
         for (int i = 0; i < kPWT; ++i) {
-          const uint32_t m = mb[gi * kPBN + (wn * kPWT + i) * kTileN + j];
-          const uint32_t zc = m >> 16;
+          const int c = 16 * i + j;
+          const uint32_t sv = *(const uint16_t*)(mb + gi * 128 + 2 * c);
+          const uint32_t zw = *(const uint32_t*)(mb + 512 + gi * 32 + 4 * (c >> 3));
+          const uint32_t zc = (zw >> (4 * (c & 7))) & 0xFu;
           z1024[i] = (0x6400u | zc) * 0x10001u;
           z64[i] = (0x5400u | (zc << 4)) * 0x10001u;
-          s2[i] = (m & 0xFFFFu) * 0x10001u;
+          s2[i] = sv * 0x10001u;
         }
       }
-      h8_t av[4];
+      h8_t av[kPRT];
 #pragma unroll
-      for (int r = 0; r < 4; ++r) av[r] = as_h8(ab[((wm * 4 + r) * 4 + u) * 64 + lane]);
+      for (int r = 0; r < kPRT; ++r) av[r] = as_h8(ab[(r * 4 + u) * 64 + lane]);
 #pragma unroll
       for (int i = 0; i < kPWT; ++i) {
         const h8_t bv = dequant_scaled(kc, w[i][u], z1024[i], z64[i], s2[i]);
 #pragma unroll
-        for (int r = 0; r < 4; ++r) acc[r][i] = mfma16x16x32(av[r], bv, acc[r][i]);
+        for (int r = 0; r < kPRT; ++r) acc[r][i] = mfma16x16x32(av[r], bv, acc[r][i]);
       }
     }
   };
 
-  // prologue: block 0 to LDS buffer 0, its weights to registers
-  u4_t wA[kPWT], wB[kPWT];
-  {
-    u4_t x[AP];
-    uint32_t sv[GPK], zv[GPK];
-    load_a(0, x);
-    load_m(0, sv, zv);
-    load_w(0, wA);
-    store_a(abuf[0], x);
-    store_m(mbuf[0], sv, zv);
-    __syncthreads();
-  }
-  // block b from buffer b % 2 with weights wc; meanwhile block b + 1 is
-  // loaded (activations and metadata to the other buffer, weights to wnx)
-  auto step = [&](int b, const u4_t (&wc)[kPWT], u4_t (&wnx)[kPWT]) {
-    u4_t x[AP];
-    uint32_t sv[GPK], zv[GPK];
-    const bool more = b + 1 < nblk;
-    if (more) {
-      load_a(b + 1, x);
-      load_m(b + 1, sv, zv);
-    }
-    load_w(b + 1, wnx);
-    __builtin_amdgcn_sched_barrier(0);
-    compute(b, abuf[b & 1], mbuf[b & 1], wc);
-    if (more) {
-      store_a(abuf[(b + 1) & 1], x);
-      store_m(mbuf[(b + 1) & 1], sv, zv);
-    }
-    __syncthreads();
+  // Before block b: this wave's loads of block b have landed (only block
+  // b + 1's are still outstanding) and its LDS reads of block b - 1 are done;
+  // the barrier then publishes every wave's block b and frees block b - 1's
+  // stage, which receives block b + 2.
+  auto sync = [&]() {
+    asm volatile("s_waitcnt vmcnt(%0)\n\ts_waitcnt lgkmcnt(0)\n\ts_barrier" ::"n"(LPB) : "memory");
   };
-  for (int b = 0; b < nblk; b += 2) {
-    step(b, wA, wB);
-    if (b + 1 < nblk) step(b + 1, wB, wA);
+  issue(0, 0);
+  issue(1, 1);
+  int st = 0;  // stage of block b
+#pragma unroll 1
+  for (int b = 0; b < nblk; ++b) {
+    sync();
+    issue(b + 2, st == 0 ? 2 : st - 1);
+    compute(st);
+    st = st == 2 ? 0 : st + 1;
   }
+  // the loads past the last block (zeros) still write LDS: let them land
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
 
   // epilogue: acc[r][i] of lane (j, kq) holds rows 4 kq .. +3 of row tile r,
-  // column j of tile i
+  // column j of the wave's tile i
 #pragma unroll
-  for (int r = 0; r < 4; ++r)
+  for (int r = 0; r < kPRT; ++r)
 #pragma unroll
     for (int i = 0; i < kPWT; ++i) {
-      const int c = (tw0 + i) * kTileN + j;
+      const int c = cw + 16 * i + j;
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
-        const int row = row0 + (wm * 4 + r) * kTileM + 4 * kq + e;
+        const int row = row0 + 16 * r + 4 * kq + e;
         if (row < a.M && c < a.N) a.Y[(int64_t)row * a.ldy + c] = float_to_half_bits(acc[r][i][e]);
       }
     }
@@ -249,14 +266,20 @@ __global__ __launch_bounds__(256) void k_gather_rows(const uint16_t* __restrict_
 
 }  // namespace
 
-bool prefill_supported(int M, int K, int N, int G, int layout, int meta, int64_t ldq) {
-  if (meta != kMetaGroup || layout != TPDQ_LAYOUT_TILED) return false;
+bool prefill_supported(int M, int64_t ldx, const tpdq_w4* w, int meta) {
+  if (meta != kMetaGroup || w->layout != TPDQ_LAYOUT_TILED) return false;
+  const int K = w->K, N = w->N, G = w->group_size;
   if (M < kPrefillMinM || K % 8 != 0 || G % 32 != 0 || K % G != 0) return false;
   const int spg = G / 32;
   if (!(spg == 1 || spg == 2 || spg == 4 || spg == 8)) return false;
+  // activation rows on 16 bytes, scale rows on 4 (the LDS loads move 16 and
+  // 4 bytes per lane)
+  if (ldx % 8 != 0 || w->ld_s % 2 != 0 || ((uintptr_t)w->scales & 3) != 0) return false;
   // byte offsets of the buffer loads are 32-bit
+  const int64_t lim = (int64_t)1 << 31;
   const int64_t ntiles = (N + kTileN - 1) / kTileN;
-  return ntiles * ldq * 4 < ((int64_t)1 << 31);
+  return ntiles * w->ld_q * 4 < lim && (int64_t)M * ldx * 2 < lim &&
+         (int64_t)w->num_groups * w->ld_s * 2 < lim && (int64_t)w->num_groups * w->ld_z * 4 < lim;
 }
 
 hipError_t launch_prefill(const GemmArgs& a, hipStream_t s) {

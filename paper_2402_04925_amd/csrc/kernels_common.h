@@ -31,8 +31,12 @@ __device__ __forceinline__ uint16_t float_to_half_bits(float f) {
 // Packed word -> 8 fp16 values (q - z) of one column, exact.
 // OR-ing a nibble into the mantissa of 1024.0 (0x6400) gives 1024 + q; the
 // nibbles at bits 4..7 land as 1024 + 16 q and are rescaled by 1/16 inside
-// the same fused op. Order: k0, k4, k1, k5, k2, k6, k3, k7 (the A operand is
-// staged in the same order).
+// the same fused op. The value pairs come from nibble positions (0, 4),
+// (1, 5), (2, 6), (3, 7): for a GPTQ word (row 8r + i at position i) that is
+// rows k0, k4, k1, k5, k2, k6, k3, k7, and the A operand is permuted to match
+// (permute_octet); a tiled word stores row 8r + i at position
+// 4 (i >> 1) + 16 (i & 1) (even rows in the low half-word, odd rows in the
+// high one), so the values come out as k0 .. k7 and A is used as loaded.
 // The masks live in VGPRs (v_and_or_b32 takes no two literals and reads one
 // SGPR at most on this ISA), so each pair costs one v_and_or_b32.
 struct UnpackConsts {
@@ -59,21 +63,26 @@ __device__ __forceinline__ h8_t unpack_sub(const UnpackConsts& k, uint32_t w, ui
 
 
 // Per-row dequant of one word: row r (0..7) has zero z[r] and scale bits
-// s[r]; returns fp16(s * (q - z)) in the order k0, k4, k1, k5, k2, k6, k3, k7.
+// s[r]; returns fp16(s * (q - z)) in the unpack order of the word's layout
+// (NAT: a tiled word, rows k0 .. k7; else k0, k4, k1, k5, k2, k6, k3, k7).
+template <bool NAT>
 __device__ __forceinline__ h8_t dequant_rows(const UnpackConsts& k, uint32_t w,
                                              const uint32_t (&z)[8], const uint32_t (&s)[8]) {
   const uint32_t lo = k.lo, hi = k.hi, magic = k.magic;
   const uint32_t w8 = w >> 8;
   const h2_t inv16 = {(_Float16)0.0625f, (_Float16)0.0625f};
-  const uint32_t z04 = ((0x6400u | z[0]) | ((0x6400u | z[4]) << 16));
-  const uint32_t z15 = ((0x5400u | (z[1] << 4)) | ((0x5400u | (z[5] << 4)) << 16));
-  const uint32_t z26 = ((0x6400u | z[2]) | ((0x6400u | z[6]) << 16));
-  const uint32_t z37 = ((0x5400u | (z[3] << 4)) | ((0x5400u | (z[7] << 4)) << 16));
+  // rows held by nibble positions 0, 1, 2, 3 (low halves) and 4, 5, 6, 7
+  constexpr int r0 = 0, r1 = NAT ? 2 : 1, r2 = NAT ? 4 : 2, r3 = NAT ? 6 : 3;
+  constexpr int r4 = NAT ? 1 : 4, r5 = NAT ? 3 : 5, r6 = NAT ? 5 : 6, r7 = 7;
+  const uint32_t z04 = ((0x6400u | z[r0]) | ((0x6400u | z[r4]) << 16));
+  const uint32_t z15 = ((0x5400u | (z[r1] << 4)) | ((0x5400u | (z[r5] << 4)) << 16));
+  const uint32_t z26 = ((0x6400u | z[r2]) | ((0x6400u | z[r6]) << 16));
+  const uint32_t z37 = ((0x5400u | (z[r3] << 4)) | ((0x5400u | (z[r7] << 4)) << 16));
   u4_t r;
-  r.x = as_u32((as_h2((w & lo) | magic) - as_h2(z04)) * as_h2(s[0] | (s[4] << 16)));
-  r.y = as_u32((as_h2((w & hi) | magic) * inv16 - as_h2(z15)) * as_h2(s[1] | (s[5] << 16)));
-  r.z = as_u32((as_h2((w8 & lo) | magic) - as_h2(z26)) * as_h2(s[2] | (s[6] << 16)));
-  r.w = as_u32((as_h2((w8 & hi) | magic) * inv16 - as_h2(z37)) * as_h2(s[3] | (s[7] << 16)));
+  r.x = as_u32((as_h2((w & lo) | magic) - as_h2(z04)) * as_h2(s[r0] | (s[r4] << 16)));
+  r.y = as_u32((as_h2((w & hi) | magic) * inv16 - as_h2(z15)) * as_h2(s[r1] | (s[r5] << 16)));
+  r.z = as_u32((as_h2((w8 & lo) | magic) - as_h2(z26)) * as_h2(s[r2] | (s[r6] << 16)));
+  r.w = as_u32((as_h2((w8 & hi) | magic) * inv16 - as_h2(z37)) * as_h2(s[r3] | (s[r7] << 16)));
   return as_h8(r);
 }
 
@@ -85,6 +94,13 @@ __device__ __forceinline__ u4_t permute_octet(u4_t x) {
   r.z = (x.y & 0xFFFFu) | (x.w << 16);
   r.w = (x.y >> 16) | (x.w & 0xFFFF0000u);
   return r;
+}
+
+// Activations as loaded -> the A operand for weights of the given layout.
+template <int LAYOUT>
+__device__ __forceinline__ u4_t to_operand(u4_t x) {
+  if constexpr (LAYOUT == TPDQ_LAYOUT_TILED) return x;
+  else return permute_octet(x);
 }
 
 // s_waitcnt vmcnt(N) alone (expcnt and lgkmcnt at their maxima). Placed

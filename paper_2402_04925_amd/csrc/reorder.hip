@@ -101,8 +101,18 @@ __global__ void k_permute_qweight(const uint32_t* __restrict__ src, int64_t ld_s
   }
 }
 
-// Tiled output: dst[t][256 b + 4 l + u] = word [4 (4 b + u) + kq][16 t + j],
-// l = 16 kq + j; words past K or N are zero.
+// A GPTQ word (row 8r + i at bits 4i) in the tiled nibble order: row 8r + i
+// at bits 4 (i >> 1) + 16 (i & 1), the even rows in the low half-word and the
+// odd rows in the high one.
+__device__ __forceinline__ uint32_t interleave_nibbles(uint32_t w) {
+  uint32_t out = 0;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) out |= ((w >> (4 * i)) & 0xFu) << (4 * (i >> 1) + 16 * (i & 1));
+  return out;
+}
+
+// Tiled output: dst[t][256 b + 4 l + u] = word [4 (4 b + u) + kq][16 t + j]
+// with its nibbles interleaved, l = 16 kq + j; words past K or N are zero.
 __global__ void k_permute_qweight_tiled(const uint32_t* __restrict__ src, int64_t ld_src, int K,
                                         int N, const int32_t* __restrict__ Prow,
                                         const int32_t* __restrict__ Pcol,
@@ -124,7 +134,7 @@ __global__ void k_permute_qweight_tiled(const uint32_t* __restrict__ src, int64_
     uint32_t v = 0u;
     if (r < kw && c < N) {
       const uint32_t cs = Pcol ? min((uint32_t)Pcol[c], nmax) : (uint32_t)c;
-      v = gather_word(src, ld_src, K, Prow, r, cs);
+      v = interleave_nibbles(gather_word(src, ld_src, K, Prow, r, cs));
     }
     dst[idx] = v;
   }

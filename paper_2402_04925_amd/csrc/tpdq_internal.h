@@ -89,11 +89,11 @@ bool plan_decode(int M, int K, int N, int G, int num_groups, int layout, int met
 hipError_t launch_decode(const GemmArgs& a, const DecodePlan& p, hipStream_t s);
 // Xp [M][K] = X[:, perm] (perm may be NULL), each octet in operand order.
 hipError_t launch_gather_prep(const uint16_t* X, int64_t ldx, int M, int K, const int32_t* perm,
-                              uint16_t* Xp, hipStream_t s);
+                              int layout, uint16_t* Xp, hipStream_t s);
 
 // Prefill GEMM (gemm_prefill.hip): sorted rows, tiled weights, M >= kPrefillMinM.
 constexpr int kPrefillMinM = 256;
-bool prefill_supported(int M, int K, int N, int G, int layout, int meta, int64_t ldq);
+bool prefill_supported(int M, int64_t ldx, const tpdq_w4* w, int meta);
 hipError_t launch_prefill(const GemmArgs& a, hipStream_t s);
 // Xp [M][K] = X[:, perm] row-major (for the prefill GEMM's activations)
 hipError_t launch_gather_rows(const uint16_t* X, int64_t ldx, int M, int K, const int32_t* perm,

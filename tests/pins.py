@@ -357,23 +357,33 @@ def pin_distinct_groups(o, seed=13):
 
 
 def pin_tiled_layout(o):
-    """The tiled storage order on a value-equals-address example: with
-    GPTQ word [r][c] = 16 r + c (K = 256, N = 32), the word a lane finds at
-    tiled[t][256 b + 4 l + u] must be the one for row 4 (4 b + u) + l // 16
-    and column 16 t + l % 16, worked out here by walking the lanes; and the
-    round trip is the identity for a ragged shape (padding is zero)."""
+    """The tiled storage order, walked lane by lane: for K = 256, N = 32 and
+    random codes q[k][n] (packed by pack_rows), the word a lane finds at
+    tiled[t][256 b + 4 l + u] covers rows 8 (4 (4 b + u) + l // 16) .. +7 of
+    column 16 t + l % 16, and the code of row 8 r + i sits at bits
+    4 (i // 2) + 16 (i % 2); so the 16-bit masks the unpack uses
+    (0x000F000F and 0x00F000F0, on the word and on the word >> 8) pick two
+    consecutive rows each, low half first. The round trip is the identity
+    for a ragged shape (padding is zero)."""
     K, N = 256, 32
-    qw = (16 * np.arange(K // 8)[:, None] + np.arange(N)[None, :]).astype(np.int32)
-    qt = o.tile(qw)
+    q = np.random.default_rng(5).integers(0, 16, size=(K, N))
+    qt = o.tile(o.pack_rows(q)).view(np.uint32)
     assert qt.shape == (2, 512)
     for t in range(2):
         for b in range(2):
             for lane in range(64):
                 for u in range(4):
-                    row = 4 * (4 * b + u) + lane // 16
-                    colm = 16 * t + lane % 16
-                    assert qt[t, 256 * b + 4 * lane + u] == 16 * row + colm
-    assert np.array_equal(o.untile(qt, K, N), qw)
+                    r = 4 * (4 * b + u) + lane // 16
+                    col = 16 * t + lane % 16
+                    w = int(qt[t, 256 * b + 4 * lane + u])
+                    for i in range(8):
+                        assert (w >> (4 * (i // 2) + 16 * (i % 2))) & 0xF == q[8 * r + i, col]
+                    pairs = [(w & 0x000F000F), (w & 0x00F000F0) >> 4,
+                             ((w >> 8) & 0x000F000F), ((w >> 8) & 0x00F000F0) >> 4]
+                    for p_, v in enumerate(pairs):
+                        assert v & 0xF == q[8 * r + 2 * p_, col]
+                        assert (v >> 16) & 0xF == q[8 * r + 2 * p_ + 1, col]
+    assert np.array_equal(o.untile(qt, K, N), o.pack_rows(q))
     w1, _ = inputs.make_custom(160, 24, 0, 32, 14)          # K % 128 != 0, N % 16 != 0
     qt2 = o.tile(w1.qweight)
     assert qt2.shape == (2, 512)
