@@ -4,10 +4,11 @@
 // At M in the thousands the product is a dense contraction and the MFMA pipe
 // bounds it (2 M K N flops against K N / 2 bytes of weights), so the kernel
 // is a register-blocked MFMA GEMM:
-//   * a workgroup of 4 waves computes a 128 x 256 tile of Y; each wave owns
-//     64 columns over all 128 rows (8 row tiles x 4 column tiles of
-//     v_mfma_f32_16x16x32_f16), so that each dequantized weight fragment feeds
-//     8 MFMAs: the unpack and scaling cost about 1.6 VALU per MFMA;
+//   * a workgroup of 8 waves (two per SIMD, so that one wave's waits are
+//     covered by the other's MFMAs) computes a 128 x 512 tile of Y; each wave
+//     owns 64 columns over all 128 rows (8 row tiles x 4 column tiles of
+//     v_mfma_f32_16x16x32_f16), so that each dequantized weight fragment
+//     feeds 8 MFMAs and the unpack and scaling cost about 2 VALU per MFMA;
 //   * K advances one 128-row block at a time (4 MFMA steps of 32 rows);
 //   * every operand goes from global memory straight to LDS (buffer loads
 //     with the LDS bit, one record of 64 lanes per instruction): activations
@@ -15,12 +16,13 @@
 //     16-byte record per lane and 16-column tile: the B operand), the scales
 //     and zeros of the wave's columns; nothing is staged through registers,
 //     so the loop keeps one copy of the accumulators;
-//   * three stages: while block b is multiplied, blocks b + 1 and b + 2 are in
-//     flight; one barrier per block hands a stage from its loads to its
-//     readers and back.
-// The waits are explicit: loads complete in order, so before block b each
-// wave waits until only the loads of block b + 1 are outstanding, and the
-// barrier then makes every wave's LDS writes of block b visible.
+//   * two stages: block b + 1 is loaded while block b is multiplied, its
+//     loads issued one after each column tile's MFMAs (a burst of them at
+//     the start of a block stalls the issuing waves); one barrier per block
+//     hands a stage from its loads to its readers and back.
+// The waits are explicit: before block b each wave waits for its own loads
+// of block b (the most recent ones), and the barrier then makes every wave's
+// LDS writes visible.
 // Dequantizing to fp16 before the MFMA rounds each weight once (relative
 // error 2^-12); the decode kernels keep q - z exact and scale in fp32, but
 // here that would double the accumulator registers and the VALU work per
@@ -31,26 +33,15 @@ namespace tpdq {
 namespace {
 
 constexpr int kPBM = 128;  // rows of Y per workgroup (8 row tiles)
-constexpr int kPBN = 256;  // columns of Y per workgroup (16 tiles of 16)
-constexpr int kPNW = 4;    // waves, each 64 columns x 128 rows
 constexpr int kPWT = 4;    // column tiles per wave
 constexpr int kPRT = 8;    // row tiles per wave
-constexpr int kPNT = kPNW * 64;
-constexpr int kPStages = 3;
-// LDS per stage: activations [8 row tiles][4 steps][64 lanes] x 16 B, then per
-// wave its weights [4 tiles][64 lanes] x 16 B and its metadata: scales
-// [groups][64 columns] x 2 B (two 256-byte records at most) and zeros
-// [groups][8 words] x 4 B (one 256-byte record)
 constexpr int kPAbytes = kPRT * 4 * 64 * 16;
 constexpr int kPWwave = kPWT * 64 * 16;
 constexpr int kPMwave = 3 * 256;
-constexpr int kPStage = kPAbytes + kPNW * (kPWwave + kPMwave);
-constexpr int kPLds = kPStages * kPStage;
+__host__ __device__ constexpr int pf_stage(int nw) { return kPAbytes + nw * (kPWwave + kPMwave); }
 
 typedef __attribute__((address_space(3))) void* lds_ptr_t;
 
-// Buffer load of `bytes` per lane straight into LDS: lane l's data lands at
-// dst + bytes * l (dst is wave-uniform).
 template <int BYTES>
 __device__ __forceinline__ void dma_to_lds(__amdgpu_buffer_rsrc_t r, void* dst, uint32_t off) {
   static_assert(BYTES == 4 || BYTES == 16, "4- or 16-byte records");
@@ -60,7 +51,6 @@ __device__ __forceinline__ void dma_to_lds(__amdgpu_buffer_rsrc_t r, void* dst, 
     __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_ptr_t)dst, 4, off, 0, 0, 0);
 }
 
-// fp16 x8 of the dequantized weights: (q - z) * s
 __device__ __forceinline__ h8_t dequant_scaled(const UnpackConsts& kc, uint32_t w, uint32_t z1024,
                                                uint32_t z64, uint32_t s2) {
   const h8_t d = unpack_sub(kc, w, z1024, z64);
@@ -69,15 +59,18 @@ __device__ __forceinline__ h8_t dequant_scaled(const UnpackConsts& kc, uint32_t 
   return d * sv;
 }
 
-template <int SPG>
-__global__ __launch_bounds__(kPNT) void k_prefill(GemmArgs a) {
+// NW waves (64 columns each), ST stages (2 or 3) of LDS.
+template <int SPG, int NW, int ST>
+__global__ __launch_bounds__(NW * 64) void k_prefill(GemmArgs a) {
   // groups per 128-row block: G = 32, 64, 128 -> 4, 2, 1; G = 256 -> one
-  // group spans two blocks (each block stages it)
+  // group spans two blocks (each block loads it)
   constexpr int GPK = SPG >= 4 ? 1 : 4 / SPG;
   constexpr int NSD = (GPK + 1) / 2;  // scale records per wave and block
-  // loads per wave and block, in issue order: activations, scales, zeros,
-  // weights
-  constexpr int LPB = 2 * 4 + NSD + 1 + kPWT;
+  constexpr int AREC = 32 / NW;       // activation records per wave and block
+  // loads per wave and block: activations, scales, zeros, weights
+  constexpr int LPB = AREC + NSD + 1 + kPWT;
+  constexpr int STAGE = pf_stage(NW);
+  constexpr int BN = 64 * NW;
   extern __shared__ __align__(16) unsigned char smem[];
 
   const int tid = threadIdx.x;
@@ -90,8 +83,8 @@ __global__ __launch_bounds__(kPNT) void k_prefill(GemmArgs a) {
   const int bn = lt / nbm;
   const int bm = lt - bn * nbm;
   const int row0 = bm * kPBM;
-  const int col0 = bn * kPBN;
-  const int cw = col0 + 64 * wave;  // the wave's first column
+  const int col0 = bn * BN;
+  const int cw = col0 + 64 * wave;
   const int nblk = (a.K + 127) >> 7;
   const int ng = a.num_groups;
   const int ntiles = (a.N + kTileN - 1) / kTileN;
@@ -113,50 +106,52 @@ __global__ __launch_bounds__(kPNT) void k_prefill(GemmArgs a) {
   // scales: record d, lane l = group 2 d + l / 32, columns 2 (l % 32), +1
   const uint32_t s_lane = (uint32_t)(lane >> 5) * (uint32_t)a.lds * 2u +
                           ((uint32_t)cw + 2u * (uint32_t)(lane & 31)) * 2u;
-  // zeros: lane l = group l / 8, word l % 8 of the wave's 8
   const uint32_t z_lane =
       ((uint32_t)(lane >> 3) * (uint32_t)a.ldz + (uint32_t)(cw >> 3) + (uint32_t)(lane & 7)) * 4u;
+  // zeros: lane l = group l / 8, word l % 8 of the wave's 8
   const bool z_used = (lane >> 3) < GPK;
   // weights: tile (cw / 16 + i), block b: lane l's 16 bytes
   const uint32_t w_lane = ((uint32_t)(cw >> 4) * (uint32_t)a.ldq + 4u * (uint32_t)lane) * 4u;
   const uint32_t w_tile = (uint32_t)a.ldq * 4u;
 
-  // block b (b >= nblk: zeros, no traffic) into LDS stage `st`
-  auto issue = [&](int b, int st) {
-    unsigned char* sb = smem + st * kPStage;
-#pragma unroll
-    for (int r = 0; r < 2; ++r) {
-      const int rt = 2 * wave + r;
-#pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        const bool ok = 128 * b + 32 * u < a.K;
-        const uint32_t off = ok ? x_lane + (uint32_t)rt * x_rt + (uint32_t)(128 * b + 32 * u) * 2u
-                                : kOutOfRange;
-        dma_to_lds<16>(rx, sb + (rt * 4 + u) * 1024, off);
-      }
-    }
+  // load k (0 <= k < LPB) of block b (b >= nblk: zeros, no traffic) into
+  // LDS stage st; every offset is a select kept in one register, so each
+  // item is exactly one load on every path (the wait counts rely on it)
+  auto dma_item = [&](int b, int st, int k) {
+    unsigned char* sb = smem + st * STAGE;
     unsigned char* wb = sb + kPAbytes + wave * (kPWwave + kPMwave);
     unsigned char* mb = wb + kPWwave;
     const int g0 = (128 * b) / (32 * SPG);
     const bool bok = b < nblk;
-#pragma unroll
-    for (int d = 0; d < NSD; ++d) {
+    if (k < AREC) {
+      const int rec = AREC * wave + k;  // record (rt, u) = (rec / 4, rec % 4)
+      const int rt = rec >> 2, u = rec & 3;
+      const bool ok = 128 * b + 32 * u < a.K;
+      uint32_t off = ok ? x_lane + (uint32_t)rt * x_rt + (uint32_t)(128 * b + 32 * u) * 2u : kOutOfRange;
+      asm("" : "+v"(off));
+      dma_to_lds<16>(rx, sb + rec * 1024, off);
+    } else if (k < AREC + NSD) {
+      const int d = k - AREC;
       const int gi = 2 * d + (lane >> 5);
       const bool ok = bok && gi < GPK && g0 + gi < ng;
-      const uint32_t off = ok ? s_lane + (uint32_t)(g0 + 2 * d) * (uint32_t)a.lds * 2u : kOutOfRange;
+      uint32_t off = ok ? s_lane + (uint32_t)(g0 + 2 * d) * (uint32_t)a.lds * 2u : kOutOfRange;
+      asm("" : "+v"(off));
       dma_to_lds<4>(rs, mb + d * 256, off);
-    }
-    {
+    } else if (k == AREC + NSD) {
       const bool ok = bok && z_used && g0 + (lane >> 3) < ng;
-      const uint32_t off = ok ? z_lane + (uint32_t)g0 * (uint32_t)a.ldz * 4u : kOutOfRange;
+      uint32_t off = ok ? z_lane + (uint32_t)g0 * (uint32_t)a.ldz * 4u : kOutOfRange;
+      asm("" : "+v"(off));
       dma_to_lds<4>(rz, mb + 512, off);
-    }
-#pragma unroll
-    for (int i = 0; i < kPWT; ++i) {
+    } else {
+      const int i = k - AREC - NSD - 1;
       uint32_t off = bok ? w_lane + (uint32_t)i * w_tile + (uint32_t)b * 1024u : kOutOfRange;
-      asm("" : "+v"(off));  // one load with a selected offset, not one per outcome
+      asm("" : "+v"(off));
       dma_to_lds<16>(rw, wb + i * 1024, off);
     }
+  };
+  auto issue = [&](int b, int st) {
+#pragma unroll
+    for (int k = 0; k < LPB; ++k) dma_item(b, st, k);
   };
 
   f4_t acc[kPRT][kPWT];
@@ -165,10 +160,11 @@ __global__ __launch_bounds__(kPNT) void k_prefill(GemmArgs a) {
 #pragma unroll
     for (int i = 0; i < kPWT; ++i) acc[r][i] = f4_t{0.f, 0.f, 0.f, 0.f};
 
-  // one block from LDS stage `st`
-  auto compute = [&](int st) {
-    const u4_t* ab = (const u4_t*)(smem + st * kPStage);
-    const u4_t* wb = (const u4_t*)(smem + st * kPStage + kPAbytes + wave * (kPWwave + kPMwave));
+  // block in stage st; the loads of block bn go out one after each column
+  // tile's MFMAs, into stage sn
+  auto compute = [&](int st, int bnext, int sn) {
+    const u4_t* ab = (const u4_t*)(smem + st * STAGE);
+    const u4_t* wb = (const u4_t*)(smem + st * STAGE + kPAbytes + wave * (kPWwave + kPMwave));
     const unsigned char* mb = (const unsigned char*)wb + kPWwave;
     u4_t w[kPWT];
 #pragma unroll
@@ -198,26 +194,30 @@ __global__ __launch_bounds__(kPNT) void k_prefill(GemmArgs a) {
         const h8_t bv = dequant_scaled(kc, w[i][u], z1024[i], z64[i], s2[i]);
 #pragma unroll
         for (int r = 0; r < kPRT; ++r) acc[r][i] = mfma16x16x32(av[r], bv, acc[r][i]);
+        if (4 * u + i < LPB) dma_item(bnext, sn, 4 * u + i);
       }
     }
   };
 
-  // Before block b: this wave's loads of block b have landed (only block
-  // b + 1's are still outstanding) and its LDS reads of block b - 1 are done;
-  // the barrier then publishes every wave's block b and frees block b - 1's
-  // stage, which receives block b + 2.
+  // Before block b: this wave's loads of block b have landed (with three
+  // stages, those of block b + 1 may still be in flight) and its LDS reads of
+  // block b - 1 are done; the barrier then publishes every wave's block b
+  // and frees the stage that receives the next block.
   auto sync = [&]() {
-    asm volatile("s_waitcnt vmcnt(%0)\n\ts_waitcnt lgkmcnt(0)\n\ts_barrier" ::"n"(LPB) : "memory");
+    if constexpr (ST == 3)
+      asm volatile("s_waitcnt vmcnt(%0)\n\ts_waitcnt lgkmcnt(0)\n\ts_barrier" ::"n"(LPB) : "memory");
+    else
+      asm volatile("s_waitcnt vmcnt(0)\n\ts_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
   };
-  issue(0, 0);
-  issue(1, 1);
-  int st = 0;  // stage of block b
+#pragma unroll
+  for (int p = 0; p < ST - 1; ++p) issue(p, p);
+  int st = 0;
 #pragma unroll 1
   for (int b = 0; b < nblk; ++b) {
     sync();
-    issue(b + 2, st == 0 ? 2 : st - 1);
-    compute(st);
-    st = st == 2 ? 0 : st + 1;
+    const int sn = st == 0 ? ST - 1 : st - 1;
+    compute(st, b + ST - 1, sn);
+    st = st == ST - 1 ? 0 : st + 1;
   }
   // the loads past the last block (zeros) still write LDS: let them land
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
@@ -282,21 +282,30 @@ bool prefill_supported(int M, int64_t ldx, const tpdq_w4* w, int meta) {
          (int64_t)w->num_groups * w->ld_s * 2 < lim && (int64_t)w->num_groups * w->ld_z * 4 < lim;
 }
 
-hipError_t launch_prefill(const GemmArgs& a, hipStream_t s) {
+// 8 waves, 2 stages: 143360 bytes of LDS
+constexpr int kPNW = 8;
+constexpr int kPStages = 2;
+
+template <int NW, int ST>
+hipError_t launch_prefill_t(const GemmArgs& a, hipStream_t s) {
   typedef void (*Kern)(GemmArgs);
   Kern k = nullptr;
   switch (a.G / 32) {
-    case 1: k = k_prefill<1>; break;
-    case 2: k = k_prefill<2>; break;
-    case 4: k = k_prefill<4>; break;
-    case 8: k = k_prefill<8>; break;
+    case 1: k = k_prefill<1, NW, ST>; break;
+    case 2: k = k_prefill<2, NW, ST>; break;
+    case 4: k = k_prefill<4, NW, ST>; break;
+    case 8: k = k_prefill<8, NW, ST>; break;
   }
   if (!k) return hipErrorInvalidValue;
-  hipError_t e = hipFuncSetAttribute((const void*)k, hipFuncAttributeMaxDynamicSharedMemorySize, kPLds);
+  const int lds = ST * pf_stage(NW);
+  hipError_t e = hipFuncSetAttribute((const void*)k, hipFuncAttributeMaxDynamicSharedMemorySize, lds);
   if (e != hipSuccess) return e;
-  const int grid = ((a.M + kPBM - 1) / kPBM) * ((a.N + kPBN - 1) / kPBN);
-  hipLaunchKernelGGL(k, dim3(grid), dim3(kPNT), kPLds, s, a);
+  const int grid = ((a.M + kPBM - 1) / kPBM) * ((a.N + 64 * NW - 1) / (64 * NW));
+  hipLaunchKernelGGL(k, dim3(grid), dim3(NW * 64), lds, s, a);
   return hipGetLastError();
+}
+hipError_t launch_prefill(const GemmArgs& a, hipStream_t s) {
+  return launch_prefill_t<kPNW, kPStages>(a, s);
 }
 
 hipError_t launch_gather_rows(const uint16_t* X, int64_t ldx, int M, int K, const int32_t* perm,
