@@ -59,7 +59,7 @@ def gemm_bytes(M, K, N, G, ng=None, gidx=False, xperm=False):
 
 def kernel_source_hash():
     h = hashlib.sha256()
-    for f in ("gemm_decode.hip", "tpdq_internal.h"):
+    for f in ("gemm_decode.hip", "kernels_common.h", "tpdq_internal.h"):
         with open(os.path.join(ROOT, "paper_2402_04925_amd", "csrc", f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()[:16]
@@ -308,6 +308,45 @@ def profile_run(st, Ms, launches, dev):
     eprint(f"[profile] copy of {COPY_BYTES} bytes: {launches} launches")
 
 
+MFMA_F16_PEAK_TFLOPS = 2500.0   # MI355X dense fp16 MFMA
+
+
+def prefill_line(dev, steps=10):
+    """The Llama-70B TP = 2 prefill shard (M = 2048): the ordered MLP shard
+    and its two GEMMs (graph replay), TFLOP/s against the dense fp16 MFMA
+    peak, and the act-order MLP for the speedup. Weights are not rotated:
+    at this size the MFMA pipe, not HBM, bounds the GEMMs."""
+    import torch
+    from paper_2402_04925_amd import inputs
+    wl = inputs.WORKLOADS["llama70b_tp2_prefill"]
+    st = Setup(wl, dev, min_bytes=0)
+    M = wl.Ms[0]
+    c = Calls(st, M, dev)
+    reps = st.reps[:1]
+    ms, _ = capture_and_time([c.mlp(rep, "ordered") for rep in reps], steps, 2, dev)
+    g1, _ = capture_and_time([c.gemm(rep, 0, "ordered") for rep in reps], steps, 2, dev)
+    g2, _ = capture_and_time([c.gemm(rep, 1, "ordered") for rep in reps], steps, 2, dev)
+    ma, _ = capture_and_time([c.mlp(rep, "actorder") for rep in reps], 2, 1, dev)
+    N1 = wl.N1 // wl.tp
+    K2 = wl.K2 // wl.tp
+    flops = 2 * M * (wl.K1 * N1 + K2 * wl.N2)
+    tf = flops / (ms * 1e-3) / 1e12
+    tf_g = [2 * M * wl.K1 * N1 / (g1 * 1e-3) / 1e12, 2 * M * K2 * wl.N2 / (g2 * 1e-3) / 1e12]
+    eprint(f"[bench] prefill M={M}: ordered mlp {ms*1e3:.1f} us ({tf:.0f} TFLOP/s), gemm1 {g1*1e3:.1f} us, "
+           f"gemm2 {g2*1e3:.1f} us; actorder mlp {ma*1e3:.1f} us")
+    del c, st
+    torch.cuda.synchronize()
+    return dict(
+        workload=f"{wl.name}: rank-0 TP-aware MLP shard, W1 {wl.K1}x{N1}, W2 {K2}x{wl.N2}, "
+                 f"int4 G={wl.G}, fp16 X, M={M}",
+        bound="mfma", ordered_mlp_us=round(ms * 1e3, 1),
+        ordered_gemm_us=[round(g1 * 1e3, 1), round(g2 * 1e3, 1)],
+        tflops=round(tf, 1), gemm_tflops=[round(t, 1) for t in tf_g],
+        peak_tflops=MFMA_F16_PEAK_TFLOPS, frac=round(tf / MFMA_F16_PEAK_TFLOPS, 4),
+        actorder_mlp_us=round(ma * 1e3, 1), speedup_vs_actorder=round(ma / ms, 2),
+        timing="HIP graph replay, events, median of 5")
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -317,6 +356,8 @@ def main():
     ap.add_argument("--M", type=int, default=16)
     ap.add_argument("--sweep", default="1,4,16", help="extra batch sizes reported alongside")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-prefill", action="store_true",
+                    help="skip the Llama-70B TP=2 prefill shard (M=2048, MFMA-bound) line")
     ap.add_argument("--profile-run", action="store_true",
                     help="eager launches for rocprofv3 (kernel trace or counters); no JSON")
     args = ap.parse_args()
@@ -370,6 +411,7 @@ def main():
         torch.cuda.synchronize()
     copy_gbs = copy_ceiling(dev)
     eprint(f"[bench] 1 GiB device copy: {copy_gbs:.0f} GB/s (read + write)")
+    prefill = None if args.no_prefill else prefill_line(dev)
 
     M = args.M
     r = results[M]
@@ -422,7 +464,7 @@ def main():
         hbm_frac=round(b["mlp"] / (mlp_us * 1e-6) / 1e9 / HBM_PEAK_GBS, 4),
         tflops=round(r["flops"] / (mlp_us * 1e-6) / 1e12, 3),
         speedup_vs_actorder=round(r["actorder"]["mlp_us"] / mlp_us, 3),
-        roofline=roof, cpu_baseline=cpu,
+        roofline=roof, cpu_baseline=cpu, prefill=prefill,
         copy_1gib_gbs=round(copy_gbs, 1),
         roofline_frac_of_copy=round(achieved / copy_gbs, 4),
         sweep=sweep,
