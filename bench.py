@@ -311,6 +311,66 @@ def profile_run(st, Ms, launches, dev):
 MFMA_F16_PEAK_TFLOPS = 2500.0   # MI355X dense fp16 MFMA
 
 
+def config_lines(dev, steps, warmup):
+    """The other decode configurations, timed like the headline one: the
+    Granite-20B TP = 4 shard and the unsharded Llama-70B MLP (TP = 1, whose
+    117 MB GEMMs are large enough to stream near the HBM roofline), with the
+    ordered and act-order MLPs, the ordered GEMMs' achieved GB/s, and at TP = 1
+    an fp16 dense reference of the same shapes (torch.matmul on random fp16
+    weights, hipBLASLt)."""
+    import torch
+    from paper_2402_04925_amd import inputs
+    out = {}
+    for name in ("granite20b_tp4", "llama70b_tp1"):
+        wl = inputs.WORKLOADS[name]
+        st = Setup(wl, dev)
+        N1 = wl.N1 // wl.tp
+        K2 = wl.K2 // wl.tp
+        dense = None
+        if wl.tp == 1:
+            g = torch.Generator(device=dev).manual_seed(5)
+            dense = (torch.randn(wl.K1, N1, device=dev, generator=g).half() * 0.02,
+                     torch.randn(K2, wl.N2, device=dev, generator=g).half() * 0.02)
+        res = {}
+        for M in wl.Ms:
+            c = Calls(st, M, dev)
+            mo, _ = capture_and_time([c.mlp(rep, "ordered") for rep in st.reps], steps, warmup, dev)
+            ma, _ = capture_and_time([c.mlp(rep, "actorder") for rep in st.reps], steps, warmup, dev)
+            g1, _ = capture_and_time([c.gemm(rep, 0, "ordered") for rep in st.reps], steps, warmup, dev)
+            g2, _ = capture_and_time([c.gemm(rep, 1, "ordered") for rep in st.reps], steps, warmup, dev)
+            b1 = gemm_bytes(M, wl.K1, N1, wl.G)
+            b2 = gemm_bytes(M, K2, wl.N2, wl.G)
+            gbs = (b1 + b2) / ((g1 + g2) * 1e-3) / 1e9
+            flops = 2 * M * (wl.K1 * N1 + K2 * wl.N2)
+            r = dict(ordered_mlp_us=round(mo * 1e3, 3), actorder_mlp_us=round(ma * 1e3, 3),
+                     speedup_ordered_vs_actorder=round(ma / mo, 3),
+                     ordered_gemm_us=[round(g1 * 1e3, 3), round(g2 * 1e3, 3)],
+                     ordered_gemm_gbs=round(gbs, 1), ordered_gemm_hbm_frac=round(gbs / HBM_PEAK_GBS, 4),
+                     ordered_mlp_tflops=round(flops / (mo * 1e-3) / 1e12, 2))
+            if dense is not None:
+                X = c.X
+                y1 = torch.empty(M, N1, dtype=torch.float16, device=dev)
+                y2 = torch.empty(M, wl.N2, dtype=torch.float16, device=dev)
+
+                def dense_mlp():
+                    torch.matmul(X, dense[0], out=y1)
+                    torch.matmul(y1, dense[1], out=y2)
+                md, _ = capture_and_time([dense_mlp], steps, warmup, dev)
+                r["fp16_dense_mlp_us"] = round(md * 1e3, 3)
+                r["speedup_ordered_vs_fp16_dense"] = round(md / mo, 3)
+            eprint(f"[bench] {name} M={M}: ordered mlp {mo*1e3:.2f} us (gemms {g1*1e3:.2f} + {g2*1e3:.2f} us, "
+                   f"{gbs:.0f} GB/s), actorder mlp {ma*1e3:.2f} us"
+                   + (f", fp16 dense mlp {r['fp16_dense_mlp_us']:.2f} us" if dense is not None else ""))
+            res[str(M)] = r
+            del c
+        out[name] = dict(
+            workload=f"{wl.name}: rank-0 TP-aware MLP shard, W1 {wl.K1}x{N1}, W2 {K2}x{wl.N2}, int4 G={wl.G}, fp16 X",
+            weight_replicas=st.R, by_M=res)
+        del st, dense
+        torch.cuda.synchronize()
+    return out
+
+
 def prefill_line(dev, steps=10):
     """The Llama-70B TP = 2 prefill shard (M = 2048): the ordered MLP shard
     and its two GEMMs (graph replay), TFLOP/s against the dense fp16 MFMA
@@ -356,6 +416,8 @@ def main():
     ap.add_argument("--M", type=int, default=16)
     ap.add_argument("--sweep", default="1,4,16", help="extra batch sizes reported alongside")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-configs", action="store_true",
+                    help="skip the Granite-20B TP=4 and Llama-70B TP=1 decode lines")
     ap.add_argument("--no-prefill", action="store_true",
                     help="skip the Llama-70B TP=2 prefill shard (M=2048, MFMA-bound) line")
     ap.add_argument("--profile-run", action="store_true",
@@ -411,6 +473,7 @@ def main():
         torch.cuda.synchronize()
     copy_gbs = copy_ceiling(dev)
     eprint(f"[bench] 1 GiB device copy: {copy_gbs:.0f} GB/s (read + write)")
+    configs = None if args.no_configs else config_lines(dev, args.steps, args.warmup)
     prefill = None if args.no_prefill else prefill_line(dev)
 
     M = args.M
@@ -464,7 +527,7 @@ def main():
         hbm_frac=round(b["mlp"] / (mlp_us * 1e-6) / 1e9 / HBM_PEAK_GBS, 4),
         tflops=round(r["flops"] / (mlp_us * 1e-6) / 1e12, 3),
         speedup_vs_actorder=round(r["actorder"]["mlp_us"] / mlp_us, 3),
-        roofline=roof, cpu_baseline=cpu, prefill=prefill,
+        roofline=roof, cpu_baseline=cpu, configs=configs, prefill=prefill,
         copy_1gib_gbs=round(copy_gbs, 1),
         roofline_frac_of_copy=round(achieved / copy_gbs, 4),
         sweep=sweep,
