@@ -69,17 +69,25 @@ tpdq_status check_layer(const tpdq_w4* w, const char* name, bool need_gidx, bool
   return TPDQ_OK;
 }
 
-// Workspace of the GEMM and MLP calls: only the gathered activations, when
-// the gather X[:, perm] cannot be done inside the GEMM's LDS.
-// the activations gathered through a permutation: for the decode kernels the
-// prepared operand (k_gather_prep: 16 rows x 128 columns x 2 bytes per row
-// tile and 128-row block, chunks of 64 rows), for the prefill kernel X[:, P]
-// row-major
-size_t gather_ws_bytes(int M, int K) {
+// Workspace of one GEMM call. The decode kernels use it only for the
+// gathered activations when the gather X[:, perm] cannot be done inside the
+// GEMM's LDS: the prepared operand (k_gather_prep: 16 rows x 128 columns x
+// 2 bytes per row tile and 128-row block, chunks of 64 rows). The M-tiled
+// kernel uses [X[:, perm] row-major, M x K x 2 bytes, when perm is given]
+// [fp32 split-K partials].
+size_t decode_gather_bytes(int M, int K) {
   const int mc = std::min(M, kDecodeMaxM);
-  size_t n = align_up((size_t)((mc + kTileM - 1) / kTileM) * ((K + 127) / 128) * 4096);
-  if (M >= kPrefillMinM) n = std::max(n, align_up((size_t)M * K * 2));
-  return n;
+  return align_up((size_t)((mc + kTileM - 1) / kTileM) * ((K + 127) / 128) * 4096);
+}
+
+size_t mtile_gather_bytes(int M, int K, bool perm) { return perm ? align_up((size_t)M * K * 2) : 0; }
+
+// bytes the call (X with leading dimension ldx, optional perm) uses
+size_t gemm_ws_need(int M, int64_t ldx, bool perm, const tpdq_w4* w, int meta) {
+  MtilePlan p;
+  if (plan_mtile(M, perm ? (int64_t)w->K : ldx, w, meta, &p))
+    return mtile_gather_bytes(M, w->K, perm) + mtile_part_bytes(p, M, w->N);
+  return perm ? decode_gather_bytes(M, w->K) : 0;
 }
 
 int meta_mode(tpdq_path path) {
@@ -96,8 +104,9 @@ tpdq_status run_gemm(const uint16_t* X, int64_t ldx, int M, const int32_t* perm,
                      tpdq_path path, uint16_t* Y, int64_t ldy, char* ws, hipStream_t st) {
   const int meta = meta_mode(path);
   const int32_t* gidx = path == TPDQ_PATH_ORDERED ? nullptr : w->g_idx;
-  if (prefill_supported(M, perm ? (int64_t)w->K : ldx, w, meta)) {
-    // prefill: one MFMA GEMM over all rows, the activations gathered first
+  MtilePlan mp;
+  if (plan_mtile(M, perm ? (int64_t)w->K : ldx, w, meta, &mp)) {
+    // M-tiled MFMA GEMM over all rows, the activations gathered first
     const uint16_t* Xa = X;
     int64_t lda = ldx;
     if (perm) {
@@ -123,8 +132,9 @@ tpdq_status run_gemm(const uint16_t* X, int64_t ldx, int M, const int32_t* perm,
     a.num_groups = w->num_groups;
     a.Y = Y;
     a.ldy = ldy;
-    hipError_t e = launch_prefill(a, st);
-    if (e != hipSuccess) return hip_fail(e, "prefill GEMM launch");
+    float* part = (float*)(ws + mtile_gather_bytes(M, w->K, perm != nullptr));
+    hipError_t e = launch_mtile(a, mp, part, st);
+    if (e != hipSuccess) return hip_fail(e, "M-tiled GEMM launch");
     return TPDQ_OK;
   }
   for (int m0 = 0; m0 < M; m0 += kDecodeMaxM) {
@@ -218,10 +228,19 @@ size_t tpdq_workspace_bytes(int op, int32_t M, const tpdq_w4* a, const tpdq_w4* 
     return n;
   }
   if (M < 1) return 0;
-  if (op == 1) return gather_ws_bytes(M, a->K);
+  // the most any call of this shape can use (the leading dimension of X is
+  // not known here; ldx = K is the case that can take the M-tiled kernel)
+  auto gemm_max = [&](const tpdq_w4* w, bool perm_possible) {
+    size_t n = perm_possible ? decode_gather_bytes(M, w->K) : 0;
+    for (int pm = 0; pm <= (perm_possible ? 1 : 0); ++pm)
+      for (int meta : {kMetaGroup, kMetaRowLds, kMetaRowGlobal})
+        n = std::max(n, gemm_ws_need(M, w->K, pm == 1, w, meta));
+    return n;
+  };
+  if (op == 1) return gemm_max(a, true);
   if (op == 2) {
     if (!b) return 0;
-    return gather_ws_bytes(M, a->K);
+    return std::max(gemm_max(a, true), gemm_max(b, false));
   }
   return 0;
 }
@@ -340,8 +359,8 @@ tpdq_status tpdq_w4a16_gemm(const void* X, int64_t ldx, int32_t M, const int32_t
     return fail(TPDQ_ERR_ALIGN, "X needs 16-byte alignment and ldx %% 8 == 0");
   }
   if (!aligned(Y, 8) || ldy % 4) return fail(TPDQ_ERR_ALIGN, "Y needs 8-byte alignment, ldy %% 4 == 0");
-  const size_t need = tpdq_workspace_bytes(1, M, w, nullptr);
-  if (x_perm && (!workspace || ws_bytes < need))
+  const size_t need = gemm_ws_need(M, ldx, x_perm != nullptr, w, meta_mode(path));
+  if (need && (!workspace || ws_bytes < need))
     return fail(TPDQ_ERR_WORKSPACE, "GEMM needs %zu workspace bytes, got %zu", need, ws_bytes);
   if (workspace && !aligned(workspace, 16))
     return fail(TPDQ_ERR_ALIGN, "workspace needs 16-byte alignment");
@@ -373,8 +392,10 @@ tpdq_status tpdq_mlp_shard(const void* X, int64_t ldx, int32_t M, const int32_t*
   }
   if (!aligned(Y1, 16) || !aligned(Y2_partial, 8))
     return fail(TPDQ_ERR_ALIGN, "Y1 needs 16-byte and Y2_partial 8-byte alignment");
-  const size_t need = tpdq_workspace_bytes(2, M, w1, w2);
-  if (!act && (!workspace || ws_bytes < need))
+  const int meta = meta_mode(path);
+  const size_t need = std::max(gemm_ws_need(M, ldx, !act, w1, meta),
+                               gemm_ws_need(M, w1->N, false, w2, meta));
+  if (need && (!workspace || ws_bytes < need))
     return fail(TPDQ_ERR_WORKSPACE, "MLP needs %zu workspace bytes, got %zu", need, ws_bytes);
   if (workspace && !aligned(workspace, 16))
     return fail(TPDQ_ERR_ALIGN, "workspace needs 16-byte alignment");

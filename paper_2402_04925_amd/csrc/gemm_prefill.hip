@@ -29,16 +29,20 @@
 // MFMA.
 #include "kernels_common.h"
 
+#include <algorithm>
+
 namespace tpdq {
 namespace {
 
-constexpr int kPBM = 128;  // rows of Y per workgroup (8 row tiles)
 constexpr int kPWT = 4;    // column tiles per wave
-constexpr int kPRT = 8;    // row tiles per wave
-constexpr int kPAbytes = kPRT * 4 * 64 * 16;
 constexpr int kPWwave = kPWT * 64 * 16;
 constexpr int kPMwave = 3 * 256;
-__host__ __device__ constexpr int pf_stage(int nw) { return kPAbytes + nw * (kPWwave + kPMwave); }
+// LDS per stage with RT row tiles and NW waves: activations
+// [RT row tiles][4 steps][64 lanes] x 16 B, then per wave its weights
+// [4 tiles][64 lanes] x 16 B and its metadata (three 256-byte records)
+__host__ __device__ constexpr int pf_stage(int rt, int nw) {
+  return rt * 4 * 64 * 16 + nw * (kPWwave + kPMwave);
+}
 
 typedef __attribute__((address_space(3))) void* lds_ptr_t;
 
@@ -59,17 +63,24 @@ __device__ __forceinline__ h8_t dequant_scaled(const UnpackConsts& kc, uint32_t 
   return d * sv;
 }
 
-// NW waves (64 columns each), ST stages (2 or 3) of LDS.
-template <int SPG, int NW, int ST>
+// RT row tiles (16 RT rows of Y per workgroup), NW waves (64 columns each),
+// ST stages (2 or 3) of LDS. With a.ks > 1 the workgroup covers one of ks
+// contiguous ranges of 128-row blocks of K and writes its fp32 partial tile
+// to a.part[split][M][N] (k_splitk_reduce sums the splits); else it writes
+// fp16 Y.
+template <int SPG, int NW, int ST, int RT>
 __global__ __launch_bounds__(NW * 64) void k_prefill(GemmArgs a) {
   // groups per 128-row block: G = 32, 64, 128 -> 4, 2, 1; G = 256 -> one
   // group spans two blocks (each block loads it)
   constexpr int GPK = SPG >= 4 ? 1 : 4 / SPG;
   constexpr int NSD = (GPK + 1) / 2;  // scale records per wave and block
-  constexpr int AREC = 32 / NW;       // activation records per wave and block
+  static_assert((RT * 4) % NW == 0, "activation records split evenly over the waves");
+  constexpr int AREC = RT * 4 / NW;   // activation records per wave and block
   // loads per wave and block: activations, scales, zeros, weights
   constexpr int LPB = AREC + NSD + 1 + kPWT;
-  constexpr int STAGE = pf_stage(NW);
+  constexpr int STAGE = pf_stage(RT, NW);
+  constexpr int ABYTES = RT * 4 * 64 * 16;
+  constexpr int BM = 16 * RT;
   constexpr int BN = 64 * NW;
   extern __shared__ __align__(16) unsigned char smem[];
 
@@ -78,14 +89,23 @@ __global__ __launch_bounds__(NW * 64) void k_prefill(GemmArgs a) {
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int j = lane & 15;
   const int kq = lane >> 4;
-  const int nbm = (a.M + kPBM - 1) / kPBM;
+  const int nbm = (a.M + BM - 1) / BM;
+  const int ks = a.ks > 1 ? a.ks : 1;
+  const int ntl = (int)(gridDim.x / ks);  // output tiles
+  // consecutive workgroups (one XCD) take neighbouring tiles of one split:
+  // they share its activations in L2
   const int lt = xcd_tile(blockIdx.x, gridDim.x);
-  const int bn = lt / nbm;
-  const int bm = lt - bn * nbm;
-  const int row0 = bm * kPBM;
+  const int kidx = lt / ntl;
+  const int tl = lt - kidx * ntl;
+  const int bn = tl / nbm;
+  const int bm = tl - bn * nbm;
+  const int row0 = bm * BM;
   const int col0 = bn * BN;
   const int cw = col0 + 64 * wave;
-  const int nblk = (a.K + 127) >> 7;
+  const int nblk_all = (a.K + 127) >> 7;
+  // this workgroup's blocks [kb0, kb1)
+  const int kb0 = (int)((int64_t)nblk_all * kidx / ks);
+  const int kb1 = (int)((int64_t)nblk_all * (kidx + 1) / ks);
   const int ng = a.num_groups;
   const int ntiles = (a.N + kTileN - 1) / kTileN;
   const UnpackConsts kc;
@@ -119,14 +139,14 @@ __global__ __launch_bounds__(NW * 64) void k_prefill(GemmArgs a) {
   // item is exactly one load on every path (the wait counts rely on it)
   auto dma_item = [&](int b, int st, int k) {
     unsigned char* sb = smem + st * STAGE;
-    unsigned char* wb = sb + kPAbytes + wave * (kPWwave + kPMwave);
+    unsigned char* wb = sb + ABYTES + wave * (kPWwave + kPMwave);
     unsigned char* mb = wb + kPWwave;
     const int g0 = (128 * b) / (32 * SPG);
-    const bool bok = b < nblk;
+    const bool bok = b < kb1;
     if (k < AREC) {
       const int rec = AREC * wave + k;  // record (rt, u) = (rec / 4, rec % 4)
       const int rt = rec >> 2, u = rec & 3;
-      const bool ok = 128 * b + 32 * u < a.K;
+      const bool ok = bok && 128 * b + 32 * u < a.K;
       uint32_t off = ok ? x_lane + (uint32_t)rt * x_rt + (uint32_t)(128 * b + 32 * u) * 2u : kOutOfRange;
       asm("" : "+v"(off));
       dma_to_lds<16>(rx, sb + rec * 1024, off);
@@ -154,9 +174,9 @@ __global__ __launch_bounds__(NW * 64) void k_prefill(GemmArgs a) {
     for (int k = 0; k < LPB; ++k) dma_item(b, st, k);
   };
 
-  f4_t acc[kPRT][kPWT];
+  f4_t acc[RT][kPWT];
 #pragma unroll
-  for (int r = 0; r < kPRT; ++r)
+  for (int r = 0; r < RT; ++r)
 #pragma unroll
     for (int i = 0; i < kPWT; ++i) acc[r][i] = f4_t{0.f, 0.f, 0.f, 0.f};
 
@@ -164,7 +184,7 @@ __global__ __launch_bounds__(NW * 64) void k_prefill(GemmArgs a) {
   // tile's MFMAs, into stage sn
   auto compute = [&](int st, int bnext, int sn) {
     const u4_t* ab = (const u4_t*)(smem + st * STAGE);
-    const u4_t* wb = (const u4_t*)(smem + st * STAGE + kPAbytes + wave * (kPWwave + kPMwave));
+    const u4_t* wb = (const u4_t*)(smem + st * STAGE + ABYTES + wave * (kPWwave + kPMwave));
     const unsigned char* mb = (const unsigned char*)wb + kPWwave;
     u4_t w[kPWT];
 #pragma unroll
@@ -186,14 +206,14 @@ __global__ __launch_bounds__(NW * 64) void k_prefill(GemmArgs a) {
           s2[i] = sv * 0x10001u;
         }
       }
-      h8_t av[kPRT];
+      h8_t av[RT];
 #pragma unroll
-      for (int r = 0; r < kPRT; ++r) av[r] = as_h8(ab[(r * 4 + u) * 64 + lane]);
+      for (int r = 0; r < RT; ++r) av[r] = as_h8(ab[(r * 4 + u) * 64 + lane]);
 #pragma unroll
       for (int i = 0; i < kPWT; ++i) {
         const h8_t bv = dequant_scaled(kc, w[i][u], z1024[i], z64[i], s2[i]);
 #pragma unroll
-        for (int r = 0; r < kPRT; ++r) acc[r][i] = mfma16x16x32(av[r], bv, acc[r][i]);
+        for (int r = 0; r < RT; ++r) acc[r][i] = mfma16x16x32(av[r], bv, acc[r][i]);
         if (4 * u + i < LPB) dma_item(bnext, sn, 4 * u + i);
       }
     }
@@ -210,10 +230,10 @@ __global__ __launch_bounds__(NW * 64) void k_prefill(GemmArgs a) {
       asm volatile("s_waitcnt vmcnt(0)\n\ts_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
   };
 #pragma unroll
-  for (int p = 0; p < ST - 1; ++p) issue(p, p);
+  for (int p = 0; p < ST - 1; ++p) issue(kb0 + p, p);
   int st = 0;
 #pragma unroll 1
-  for (int b = 0; b < nblk; ++b) {
+  for (int b = kb0; b < kb1; ++b) {
     sync();
     const int sn = st == 0 ? ST - 1 : st - 1;
     compute(st, b + ST - 1, sn);
@@ -224,17 +244,47 @@ __global__ __launch_bounds__(NW * 64) void k_prefill(GemmArgs a) {
 
   // epilogue: acc[r][i] of lane (j, kq) holds rows 4 kq .. +3 of row tile r,
   // column j of the wave's tile i
+  float* part = a.part + (size_t)kidx * a.M * a.N;
 #pragma unroll
-  for (int r = 0; r < kPRT; ++r)
+  for (int r = 0; r < RT; ++r)
 #pragma unroll
     for (int i = 0; i < kPWT; ++i) {
       const int c = cw + 16 * i + j;
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
         const int row = row0 + 16 * r + 4 * kq + e;
-        if (row < a.M && c < a.N) a.Y[(int64_t)row * a.ldy + c] = float_to_half_bits(acc[r][i][e]);
+        if (row < a.M && c < a.N) {
+          if (ks > 1)
+            part[(int64_t)row * a.N + c] = acc[r][i][e];
+          else
+            a.Y[(int64_t)row * a.ldy + c] = float_to_half_bits(acc[r][i][e]);
+        }
       }
     }
+}
+
+// Y[m][n] = fp16(sum over s of part[s][m][n]), the splits added in order s =
+// 0, 1, ... (the result does not depend on which split finished first); 8
+// columns per thread.
+__global__ __launch_bounds__(256) void k_splitk_reduce(const float* __restrict__ part, int ks, int M,
+                                                       int N, uint16_t* __restrict__ Y, int64_t ldy) {
+  const int n8 = (N + 7) >> 3;
+  const int64_t total = (int64_t)M * n8;
+  const int64_t plane = (int64_t)M * N;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < total;
+       i += (int64_t)gridDim.x * blockDim.x) {
+    const int m = (int)(i / n8);
+    const int c0 = (int)(i - (int64_t)m * n8) * 8;
+    const float* src = part + (int64_t)m * N + c0;
+    float v[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+    for (int s = 0; s < ks; ++s)
+#pragma unroll
+      for (int e = 0; e < 8; ++e)
+        if (c0 + e < N) v[e] += src[s * plane + e];
+#pragma unroll
+    for (int e = 0; e < 8; ++e)
+      if (c0 + e < N) Y[(int64_t)m * ldy + c0 + e] = float_to_half_bits(v[e]);
+  }
 }
 
 // X'[m][k] = X[m][perm[k]] in row-major order, one workgroup per row: the row
@@ -266,10 +316,10 @@ __global__ __launch_bounds__(256) void k_gather_rows(const uint16_t* __restrict_
 
 }  // namespace
 
-bool prefill_supported(int M, int64_t ldx, const tpdq_w4* w, int meta) {
+bool plan_mtile(int M, int64_t ldx, const tpdq_w4* w, int meta, MtilePlan* p) {
   if (meta != kMetaGroup || w->layout != TPDQ_LAYOUT_TILED) return false;
   const int K = w->K, N = w->N, G = w->group_size;
-  if (M < kPrefillMinM || K % 8 != 0 || G % 32 != 0 || K % G != 0) return false;
+  if (M < kMtileMinM || K % 8 != 0 || G % 32 != 0 || K % G != 0) return false;
   const int spg = G / 32;
   if (!(spg == 1 || spg == 2 || spg == 4 || spg == 8)) return false;
   // activation rows on 16 bytes, scale rows on 4 (the LDS loads move 16 and
@@ -278,34 +328,77 @@ bool prefill_supported(int M, int64_t ldx, const tpdq_w4* w, int meta) {
   // byte offsets of the buffer loads are 32-bit
   const int64_t lim = (int64_t)1 << 31;
   const int64_t ntiles = (N + kTileN - 1) / kTileN;
-  return ntiles * w->ld_q * 4 < lim && (int64_t)M * ldx * 2 < lim &&
-         (int64_t)w->num_groups * w->ld_s * 2 < lim && (int64_t)w->num_groups * w->ld_z * 4 < lim;
+  if (!(ntiles * w->ld_q * 4 < lim && (int64_t)M * ldx * 2 < lim &&
+        (int64_t)w->num_groups * w->ld_s * 2 < lim && (int64_t)w->num_groups * w->ld_z * 4 < lim))
+    return false;
+  MtilePlan q{};
+  if (M >= kPrefillMinM) {
+    // a dense contraction: 8 waves (two per SIMD) over 128 x 512 tiles
+    q.rt = 8;
+    q.nw = 8;
+    q.st = 2;
+    q.ks = 1;
+  } else {
+    // below prefill sizes the weight stream bounds the product; worth it
+    // only when the weights are large enough that the decode kernels'
+    // per-workgroup re-reads of X dominate: 64-row tiles, 4 waves (two
+    // workgroups per CU), K split so that about kMtileTargetWgs workgroups
+    // stream
+    if ((int64_t)K * N < kMtileMinWeights) return false;
+    q.rt = 4;
+    q.nw = 4;
+    q.st = 2;
+    const int nblk = (K + 127) / 128;
+    const int tiles = ((M + 63) / 64) * ((N + 255) / 256);
+    int ks = (kMtileTargetWgs + tiles - 1) / tiles;
+    ks = std::max(1, std::min(ks, nblk / 4));
+    if ((int64_t)ks * M * N * 4 >= lim) ks = 1;
+    q.ks = ks;
+  }
+  *p = q;
+  return true;
 }
 
-// 8 waves, 2 stages: 143360 bytes of LDS
-constexpr int kPNW = 8;
-constexpr int kPStages = 2;
+size_t mtile_part_bytes(const MtilePlan& p, int M, int N) {
+  return p.ks > 1 ? align_up((size_t)p.ks * M * N * 4) : 0;
+}
 
-template <int NW, int ST>
-hipError_t launch_prefill_t(const GemmArgs& a, hipStream_t s) {
+template <int NW, int ST, int RT>
+hipError_t launch_mtile_t(const GemmArgs& a, int ks, hipStream_t s) {
   typedef void (*Kern)(GemmArgs);
   Kern k = nullptr;
   switch (a.G / 32) {
-    case 1: k = k_prefill<1, NW, ST>; break;
-    case 2: k = k_prefill<2, NW, ST>; break;
-    case 4: k = k_prefill<4, NW, ST>; break;
-    case 8: k = k_prefill<8, NW, ST>; break;
+    case 1: k = k_prefill<1, NW, ST, RT>; break;
+    case 2: k = k_prefill<2, NW, ST, RT>; break;
+    case 4: k = k_prefill<4, NW, ST, RT>; break;
+    case 8: k = k_prefill<8, NW, ST, RT>; break;
   }
   if (!k) return hipErrorInvalidValue;
-  const int lds = ST * pf_stage(NW);
+  const int lds = ST * pf_stage(RT, NW);
   hipError_t e = hipFuncSetAttribute((const void*)k, hipFuncAttributeMaxDynamicSharedMemorySize, lds);
   if (e != hipSuccess) return e;
-  const int grid = ((a.M + kPBM - 1) / kPBM) * ((a.N + 64 * NW - 1) / (64 * NW));
+  const int grid = ((a.M + 16 * RT - 1) / (16 * RT)) * ((a.N + 64 * NW - 1) / (64 * NW)) * ks;
   hipLaunchKernelGGL(k, dim3(grid), dim3(NW * 64), lds, s, a);
   return hipGetLastError();
 }
-hipError_t launch_prefill(const GemmArgs& a, hipStream_t s) {
-  return launch_prefill_t<kPNW, kPStages>(a, s);
+
+hipError_t launch_mtile(const GemmArgs& a0, const MtilePlan& p, float* part, hipStream_t s) {
+  GemmArgs a = a0;
+  a.ks = p.ks;
+  a.part = part;
+  if (p.ks > 1 && !part) return hipErrorInvalidValue;
+  hipError_t e;
+  if (p.rt == 8 && p.nw == 8 && p.st == 2)
+    e = launch_mtile_t<8, 2, 8>(a, p.ks, s);
+  else if (p.rt == 4 && p.nw == 4 && p.st == 2)
+    e = launch_mtile_t<4, 2, 4>(a, p.ks, s);
+  else
+    return hipErrorInvalidValue;
+  if (e != hipSuccess || p.ks == 1) return e;
+  const int64_t total = (int64_t)a.M * ((a.N + 7) / 8);
+  const int blocks = (int)std::min<int64_t>((total + 255) / 256, 4096);
+  hipLaunchKernelGGL(k_splitk_reduce, dim3(blocks), dim3(256), 0, s, part, p.ks, a.M, a.N, a.Y, a.ldy);
+  return hipGetLastError();
 }
 
 hipError_t launch_gather_rows(const uint16_t* X, int64_t ldx, int M, int K, const int32_t* perm,

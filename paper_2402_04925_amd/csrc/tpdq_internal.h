@@ -58,6 +58,8 @@ struct GemmArgs {
   int64_t ldz;
   const int32_t* g_idx;   // [K] (per-row metadata modes)
   int K, N, G, num_groups;
+  int ks;        // M-tiled kernel: K splits (<= 1: none)
+  float* part;   // M-tiled kernel: fp32 partials [ks][M][N] when ks > 1
   uint16_t* Y;            // [M][ldy]
   int64_t ldy;
   int meta_rows;          // metadata rows staged in LDS
@@ -91,10 +93,26 @@ hipError_t launch_decode(const GemmArgs& a, const DecodePlan& p, hipStream_t s);
 hipError_t launch_gather_prep(const uint16_t* X, int64_t ldx, int M, int K, const int32_t* perm,
                               int layout, uint16_t* Xp, hipStream_t s);
 
-// Prefill GEMM (gemm_prefill.hip): sorted rows, tiled weights, M >= kPrefillMinM.
+// M-tiled MFMA GEMM (gemm_prefill.hip): sorted rows, tiled weights. At
+// M >= kPrefillMinM, 128 x 512 tiles over the whole K; from kMtileMinM rows,
+// on weights of at least kMtileMinWeights elements, 64 x 256 tiles with K
+// split over ks workgroups (fp32 partials in the workspace, summed in split
+// order by a second kernel). Below kMtileMinM rows the decode kernels are
+// faster (measured on the Llama-70B TP=1 shapes: at M = 16 the decode GEMMs
+// take 38 / 34 us, the split-K tiles 57 / 61 us; at M = 64, 127 / 111 us
+// against 70 / 64 us).
 constexpr int kPrefillMinM = 256;
-bool prefill_supported(int M, int64_t ldx, const tpdq_w4* w, int meta);
-hipError_t launch_prefill(const GemmArgs& a, hipStream_t s);
+constexpr int kMtileMinM = 33;
+constexpr int64_t kMtileMinWeights = (int64_t)64 << 20;
+constexpr int kMtileTargetWgs = 256;
+struct MtilePlan {
+  int rt, nw, st, ks;  // row tiles and waves per workgroup, LDS stages, K splits
+};
+bool plan_mtile(int M, int64_t ldx, const tpdq_w4* w, int meta, MtilePlan* p);
+// workspace bytes of the fp32 partials (0 when ks == 1)
+size_t mtile_part_bytes(const MtilePlan& p, int M, int N);
+// part: the partials (ignored when p.ks == 1)
+hipError_t launch_mtile(const GemmArgs& a, const MtilePlan& p, float* part, hipStream_t s);
 // Xp [M][K] = X[:, perm] row-major (for the prefill GEMM's activations)
 hipError_t launch_gather_rows(const uint16_t* X, int64_t ldx, int M, int K, const int32_t* perm,
                               uint16_t* Xp, hipStream_t s);

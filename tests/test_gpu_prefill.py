@@ -1,4 +1,7 @@
-"""GPU prefill GEMM (ordered path, tiled weights, M >= 256) against the oracle."""
+"""GPU M-tiled GEMM (ordered path, tiled weights) against the oracle: the
+prefill configuration (M >= 256, 128 x 512 tiles over all of K) and the
+medium-M configuration (16 <= M < 256 on large weights, 64 x 256 tiles with
+K split over workgroups and the fp32 partials summed by a second kernel)."""
 import numpy as np
 import pytest
 
@@ -93,3 +96,54 @@ def test_prefill_mlp_llama_tp2():
     W2 = o.dequant(L2.qweight, L2.scales, L2.qzeros, L2.g_idx, cols=cols2)[eP2[:k2]]
     ref2 = o.to_fp16(o.matmul(Y1h.astype(np.float64), W2))
     assert o.rel_err(Y2h[:, cols2], ref2) <= TOL_FP16
+
+
+# K, N, G, M for the split-K configuration: at least 64M weights, ragged N and
+# M, every group size, M from 33 rows (one 64-row tile, half padding) to 255
+# (four tiles)
+MT_SHAPES = [
+    (8192, 8192, 128, 33), (8192, 8200, 128, 40), (4096, 16384, 64, 64), (16384, 4096, 256, 100),
+    (8192, 8192, 32, 255),
+]
+
+
+@pytest.mark.parametrize("K,N,G,M", MT_SHAPES)
+def test_mtile_splitk_gemm(K, N, G, M):
+    """Sorted rows from the GPU reorder, with and without the X[:, P] gather,
+    on sampled columns (tile edges, the ragged tail, random ones); then the
+    same call again (the partials are overwritten, not accumulated)."""
+    import torch
+    import paper_2402_04925_amd as tpdq
+    dev = torch_dev()
+    log(f"mtile K={K} N={N} G={G} M={M}")
+    w1, _ = inputs.make_custom(K, N, 0, G, seed=K + N + G + 11)
+    X = inputs.random_activations(M, K, np.random.default_rng(M + 5))
+    P, gs, _, _, wo, _ = tpdq.reorder(layer_to_dev(w1, dev), layout=tpdq.LAYOUT_TILED)
+    Xd = to_dev(X, dev)
+    cols = sample_cols(N, np.random.default_rng(K + M))
+    ref = o.w4a16_gemm(X, w1.qweight, w1.scales, w1.qzeros, w1.g_idx, cols=cols)
+    for _ in range(2):
+        Y = tpdq.w4a16_gemm(Xd, wo, tpdq.PATH_ORDERED, x_perm=P)
+        torch.cuda.synchronize()
+        assert o.rel_err(np_of(Y)[:, cols], ref) <= TOL_FP16
+    eP, eg = o.reorder(w1.g_idx)
+    ws = o.permute_rows(dict(qweight=w1.qweight, scales=w1.scales, qzeros=w1.qzeros), eP)
+    ref2 = o.w4a16_gemm(X, ws["qweight"], ws["scales"], ws["qzeros"], eg, cols=cols)
+    Y2 = tpdq.w4a16_gemm(Xd, wo, tpdq.PATH_ORDERED)
+    torch.cuda.synchronize()
+    assert o.rel_err(np_of(Y2)[:, cols], ref2) <= TOL_FP16
+
+
+def test_mtile_deterministic():
+    """The split-K partials are summed in split order: two calls agree bit for bit."""
+    import torch
+    import paper_2402_04925_amd as tpdq
+    dev = torch_dev()
+    K, N, G, M = 8192, 8192, 128, 48
+    w1, _ = inputs.make_custom(K, N, 0, G, seed=3)
+    X = to_dev(inputs.random_activations(M, K, np.random.default_rng(9)), dev)
+    _, _, _, _, wo, _ = tpdq.reorder(layer_to_dev(w1, dev), layout=tpdq.LAYOUT_TILED)
+    a = np_of(tpdq.w4a16_gemm(X, wo, tpdq.PATH_ORDERED))
+    b = np_of(tpdq.w4a16_gemm(X, wo, tpdq.PATH_ORDERED))
+    torch.cuda.synchronize()
+    assert np.array_equal(a.view(np.uint16), b.view(np.uint16))
