@@ -264,31 +264,38 @@ __global__ __launch_bounds__(NW * 64) void k_prefill(GemmArgs a) {
 }
 
 // Y[m][n] = fp16(sum over s of part[s][m][n]), the splits added in order s =
-// 0, 1, ... (the result does not depend on which split finished first); 8
-// columns per thread.
+// 0, 1, ... (the result does not depend on which split finished first). Four
+// columns per thread: one 16-byte load per split, one 8-byte store (N % 4 ==
+// 0 and 16-byte aligned rows; otherwise one column per thread).
 __global__ __launch_bounds__(256) void k_splitk_reduce(const float* __restrict__ part, int ks, int M,
                                                        int N, uint16_t* __restrict__ Y, int64_t ldy) {
-  const int n8 = (N + 7) >> 3;
-  const int64_t total = (int64_t)M * n8;
   const int64_t plane = (int64_t)M * N;
-  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < total;
+  if ((N & 3) == 0 && (ldy & 3) == 0) {
+    const int n4 = N >> 2;
+    const int64_t total = (int64_t)M * n4;
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < total;
+         i += (int64_t)gridDim.x * blockDim.x) {
+      const int m = (int)(i / n4);
+      const int c0 = (int)(i - (int64_t)m * n4) * 4;
+      const float* src = part + (int64_t)m * N + c0;
+      f4_t v = *(const f4_t*)src;
+      for (int s = 1; s < ks; ++s) v += *(const f4_t*)(src + s * plane);
+      const uint32_t lo = float_to_half_bits(v[0]) | ((uint32_t)float_to_half_bits(v[1]) << 16);
+      const uint32_t hi = float_to_half_bits(v[2]) | ((uint32_t)float_to_half_bits(v[3]) << 16);
+      *(uint2*)(Y + (int64_t)m * ldy + c0) = make_uint2(lo, hi);
+    }
+    return;
+  }
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < plane;
        i += (int64_t)gridDim.x * blockDim.x) {
-    const int m = (int)(i / n8);
-    const int c0 = (int)(i - (int64_t)m * n8) * 8;
-    const float* src = part + (int64_t)m * N + c0;
-    float v[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-    for (int s = 0; s < ks; ++s)
-#pragma unroll
-      for (int e = 0; e < 8; ++e)
-        if (c0 + e < N) v[e] += src[s * plane + e];
-#pragma unroll
-    for (int e = 0; e < 8; ++e)
-      if (c0 + e < N) Y[(int64_t)m * ldy + c0 + e] = float_to_half_bits(v[e]);
+    const int m = (int)(i / N);
+    const int c = (int)(i - (int64_t)m * N);
+    float v = part[i];
+    for (int s = 1; s < ks; ++s) v += part[s * plane + i];
+    Y[(int64_t)m * ldy + c] = float_to_half_bits(v);
   }
 }
 
-// X'[m][k] = X[m][perm[k]] in row-major order, one workgroup per row: the row
-// is copied to LDS and gathered from there.
 __global__ __launch_bounds__(256) void k_gather_rows(const uint16_t* __restrict__ X, int64_t ldx,
                                                      int K, const int32_t* __restrict__ perm,
                                                      uint16_t* __restrict__ Xp) {
@@ -395,8 +402,8 @@ hipError_t launch_mtile(const GemmArgs& a0, const MtilePlan& p, float* part, hip
   else
     return hipErrorInvalidValue;
   if (e != hipSuccess || p.ks == 1) return e;
-  const int64_t total = (int64_t)a.M * ((a.N + 7) / 8);
-  const int blocks = (int)std::min<int64_t>((total + 255) / 256, 4096);
+  const int64_t total = (int64_t)a.M * a.N / 4 + 1;
+  const int blocks = (int)std::min<int64_t>((total + 255) / 256, 16384);
   hipLaunchKernelGGL(k_splitk_reduce, dim3(blocks), dim3(256), 0, s, part, p.ks, a.M, a.N, a.Y, a.ldy);
   return hipGetLastError();
 }
