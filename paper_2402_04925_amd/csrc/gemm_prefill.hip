@@ -68,8 +68,11 @@ __device__ __forceinline__ h8_t dequant_scaled(const UnpackConsts& kc, uint32_t 
 // contiguous ranges of 128-row blocks of K and writes its fp32 partial tile
 // to a.part[split][M][N] (k_splitk_reduce sums the splits); else it writes
 // fp16 Y.
+// Two waves per SIMD (the 8-wave workgroup, or two 4-wave workgroups per CU):
+// 256 registers per lane, with the accumulators in the architectural VGPRs
+// (no accumulator copies between loop iterations).
 template <int SPG, int NW, int ST, int RT>
-__global__ __launch_bounds__(NW * 64) void k_prefill(GemmArgs a) {
+__global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2))) void k_prefill(GemmArgs a) {
   // groups per 128-row block: G = 32, 64, 128 -> 4, 2, 1; G = 256 -> one
   // group spans two blocks (each block loads it)
   constexpr int GPK = SPG >= 4 ? 1 : 4 / SPG;
