@@ -936,12 +936,13 @@ bool plan_decode(int M, int K, int N, int G, int num_groups, int layout, int met
   if (a_global(am) && mt > 1 && nw > 8) nw = 8;
   int tn = 1;
   if (meta == kMetaGroup) {
-    // the ordered kernel streams best with about 8 blocks of 128 rows per
-    // wave and at most 8 waves per workgroup (measured on the Llama-70B
-    // shard shapes); with X read from global memory, 4 waves, and two tiles
-    // per workgroup when that still leaves a workgroup per CU
+    // the ordered kernel streams best with 8 waves (about 8 blocks of 128
+    // rows each) when the grid has no more workgroups than CUs, else with 4
+    // (measured on the Llama-70B and Granite-20B shapes); with X read from
+    // global memory, 4 waves, and two tiles per workgroup when that still
+    // leaves a workgroup per CU
     const int nblk = (K + 127) / 128;
-    nw = (!a_global(am) && nblk >= 48) ? 8 : 4;
+    nw = (!a_global(am) && nblk >= 48 && ntiles <= 256) ? 8 : 4;
     if (a_global(am) && ntiles >= 512) tn = 2;
   }
   p->tn = tn;
