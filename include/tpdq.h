@@ -175,9 +175,12 @@ tpdq_status tpdq_pack_tiled(const tpdq_w4* w, int32_t* qweight_out, void* stream
  *    clamped into range (no fault; such rows give unspecified results).
  * Y  [M][ldy] output, 8 B aligned, ldy % 4 == 0, ldy >= N.
  * Workspace: at least tpdq_workspace_bytes(1, M, w, NULL) bytes, any content
- * (it holds the gathered X' when the gather cannot be done on chip). Calls
- * that overlap in time must not share a workspace. Deterministic: the same
- * inputs give bit-identical outputs.
+ * (it holds the gathered X' when the gather cannot be done on chip, and the
+ * fp32 split-K partials of the kernels that split K on large weights). A
+ * call with x_perm always needs one; without x_perm, a call that needs none
+ * accepts NULL. Calls that overlap in time must not share a workspace.
+ * Deterministic: the same inputs give bit-identical outputs (split-K
+ * partials are added in a fixed order).
  */
 tpdq_status tpdq_w4a16_gemm(const void* X, int64_t ldx, int32_t M, const int32_t* x_perm,
                             const tpdq_w4* w, tpdq_path path, tpdq_dtype dtype,

@@ -82,12 +82,42 @@ size_t decode_gather_bytes(int M, int K) {
 
 size_t mtile_gather_bytes(int M, int K, bool perm) { return perm ? align_up((size_t)M * K * 2) : 0; }
 
-// bytes the call (X with leading dimension ldx, optional perm) uses
+// The decode plan of one launch of mc <= 64 rows, as run_gemm makes it: with
+// a perm, the gather inside the kernel's LDS if it fits, else the prepared
+// operand (*prepared).
+bool decode_plan_for(int mc, bool perm, const tpdq_w4* w, int meta, DecodePlan* plan,
+                     bool* prepared) {
+  *prepared = false;
+  if (perm) {
+    if (plan_decode(mc, w->K, w->N, w->group_size, w->num_groups, w->layout, meta, kOperandGather,
+                    plan))
+      return true;
+    *prepared = true;
+    return plan_decode(mc, w->K, w->N, w->group_size, w->num_groups, w->layout, meta,
+                       kOperandPrepared, plan);
+  }
+  return plan_decode(mc, w->K, w->N, w->group_size, w->num_groups, w->layout, meta, kOperandPlain,
+                     plan);
+}
+
+// split-K partials of the wide decode kernel (0 when K is not split)
+size_t decode_part_bytes(const DecodePlan& p, int mc, int N) {
+  return p.wide && p.ks > 1 ? align_up((size_t)p.ks * mc * N * 4) : 0;
+}
+
+// Bytes the call (X with leading dimension ldx, optional perm) uses. Decode:
+// [prepared operand][wide kernel's partials], the partials after the
+// prepared-operand region whenever either is used.
 size_t gemm_ws_need(int M, int64_t ldx, bool perm, const tpdq_w4* w, int meta) {
   MtilePlan p;
   if (plan_mtile(M, perm ? (int64_t)w->K : ldx, w, meta, &p))
     return mtile_gather_bytes(M, w->K, perm) + mtile_part_bytes(p, M, w->N);
-  return perm ? decode_gather_bytes(M, w->K) : 0;
+  DecodePlan dp;
+  bool prepared = false;
+  const int mc = std::min(M, kDecodeMaxM);  // the largest launch
+  if (!decode_plan_for(mc, perm, w, meta, &dp, &prepared)) return perm ? decode_gather_bytes(M, w->K) : 0;
+  const size_t part = decode_part_bytes(dp, mc, w->N);
+  return (prepared || part ? decode_gather_bytes(M, w->K) : 0) + part;
 }
 
 int meta_mode(tpdq_path path) {
@@ -142,23 +172,15 @@ tpdq_status run_gemm(const uint16_t* X, int64_t ldx, int M, const int32_t* perm,
     const uint16_t* Xc = X + (int64_t)m0 * ldx;
     int64_t ldc = ldx;
     DecodePlan plan;
-    int operand = kOperandPlain;
-    bool ok;
-    if (perm) {
-      operand = kOperandGather;
-      ok = plan_decode(mc, w->K, w->N, w->group_size, w->num_groups, w->layout, meta, operand, &plan);
-      if (!ok) {
-        uint16_t* Xp = (uint16_t*)ws;
-        hipError_t e = launch_gather_prep(Xc, ldx, mc, w->K, perm, w->layout, Xp, st);
-        if (e != hipSuccess) return hip_fail(e, "activation gather launch");
-        Xc = Xp;
-        ldc = w->K;
-        operand = kOperandPrepared;
-        ok = plan_decode(mc, w->K, w->N, w->group_size, w->num_groups, w->layout, meta, operand,
-                         &plan);
-      }
-    } else {
-      ok = plan_decode(mc, w->K, w->N, w->group_size, w->num_groups, w->layout, meta, operand, &plan);
+    bool prepared = false;
+    const bool ok = decode_plan_for(mc, perm != nullptr, w, meta, &plan, &prepared);
+    int operand = perm ? (prepared ? kOperandPrepared : kOperandGather) : kOperandPlain;
+    if (ok && prepared) {
+      uint16_t* Xp = (uint16_t*)ws;
+      hipError_t e = launch_gather_prep(Xc, ldx, mc, w->K, perm, w->layout, Xp, st);
+      if (e != hipSuccess) return hip_fail(e, "activation gather launch");
+      Xc = Xp;
+      ldc = w->K;
     }
     if (!ok)
       return fail(TPDQ_ERR_UNSUPPORTED, "no decode kernel for M=%d K=%d N=%d G=%d", mc, w->K, w->N,
@@ -181,7 +203,8 @@ tpdq_status run_gemm(const uint16_t* X, int64_t ldx, int M, const int32_t* perm,
     a.num_groups = w->num_groups;
     a.Y = Y + (int64_t)m0 * ldy;
     a.ldy = ldy;
-    hipError_t e = launch_decode(a, plan, st);
+    float* part = (float*)(ws + decode_gather_bytes(M, w->K));
+    hipError_t e = launch_decode(a, plan, part, st);
     if (e != hipSuccess) return hip_fail(e, "decode GEMM launch");
   }
   return TPDQ_OK;
@@ -359,9 +382,12 @@ tpdq_status tpdq_w4a16_gemm(const void* X, int64_t ldx, int32_t M, const int32_t
     return fail(TPDQ_ERR_ALIGN, "X needs 16-byte alignment and ldx %% 8 == 0");
   }
   if (!aligned(Y, 8) || ldy % 4) return fail(TPDQ_ERR_ALIGN, "Y needs 8-byte alignment, ldy %% 4 == 0");
+  // a call that uses a workspace (a gather always does) takes the documented
+  // tpdq_workspace_bytes(1, ...), an upper bound of what it uses
+  const size_t bound = tpdq_workspace_bytes(1, M, w, nullptr);
   const size_t need = gemm_ws_need(M, ldx, x_perm != nullptr, w, meta_mode(path));
-  if (need && (!workspace || ws_bytes < need))
-    return fail(TPDQ_ERR_WORKSPACE, "GEMM needs %zu workspace bytes, got %zu", need, ws_bytes);
+  if ((x_perm || need) && (!workspace || ws_bytes < bound))
+    return fail(TPDQ_ERR_WORKSPACE, "GEMM needs %zu workspace bytes, got %zu", bound, ws_bytes);
   if (workspace && !aligned(workspace, 16))
     return fail(TPDQ_ERR_ALIGN, "workspace needs 16-byte alignment");
   return run_gemm((const uint16_t*)X, ldx, M, x_perm, w, path, (uint16_t*)Y, ldy, (char*)workspace,
@@ -393,10 +419,11 @@ tpdq_status tpdq_mlp_shard(const void* X, int64_t ldx, int32_t M, const int32_t*
   if (!aligned(Y1, 16) || !aligned(Y2_partial, 8))
     return fail(TPDQ_ERR_ALIGN, "Y1 needs 16-byte and Y2_partial 8-byte alignment");
   const int meta = meta_mode(path);
+  const size_t bound = tpdq_workspace_bytes(2, M, w1, w2);
   const size_t need = std::max(gemm_ws_need(M, ldx, !act, w1, meta),
                                gemm_ws_need(M, w1->N, false, w2, meta));
-  if (need && (!workspace || ws_bytes < need))
-    return fail(TPDQ_ERR_WORKSPACE, "MLP needs %zu workspace bytes, got %zu", need, ws_bytes);
+  if ((!act || need) && (!workspace || ws_bytes < bound))
+    return fail(TPDQ_ERR_WORKSPACE, "MLP needs %zu workspace bytes, got %zu", bound, ws_bytes);
   if (workspace && !aligned(workspace, 16))
     return fail(TPDQ_ERR_ALIGN, "workspace needs 16-byte alignment");
 

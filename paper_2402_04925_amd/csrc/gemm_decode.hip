@@ -32,6 +32,8 @@
 //     staged in LDS, or fetched from global memory row by row.
 #include "kernels_common.h"
 
+#include <algorithm>
+
 namespace tpdq {
 namespace {
 
@@ -634,6 +636,217 @@ __global__ __launch_bounds__(NW * 64) void k_ordered(GemmArgs a) {
   reduce_store<MT, NW, TN>(a, acc, tile0 * kTileN, smem);
 }
 
+
+// ---------------------------------------------------------------------------
+// Wide kernel (large weights, X too large to stage whole in LDS): the
+// workgroup's NW waves own NW * TN different 16-column tiles
+// over one range of 128-row blocks of K (all of K, or one of ks splits), so
+// that the activations are shared: they are staged in LDS four blocks at a
+// time (two buffers, loaded with the LDS bit, one barrier per chunk) while
+// each wave streams its own weights in registers, D blocks ahead, and owns
+// its outputs (no cross-wave reduction). With ks > 1 each workgroup writes
+// its fp32 partial tile to a.part[split][M][N] (k_splitk_reduce adds them).
+// PREP: the activations are the prepared operand (k_gather_prep records),
+// else X row-major.
+// ---------------------------------------------------------------------------
+template <int MT, int NW, int SPG, int TN, bool PREP>
+__global__ __launch_bounds__(NW * 64) void k_wide(GemmArgs a) {
+  extern __shared__ __align__(16) unsigned char smem[];
+  constexpr int D = 4;                  // weight blocks in flight per wave
+  constexpr int CB = 4;                 // blocks per activation chunk
+  constexpr int RECS = MT * CB * 4;     // 1 KiB operand records per chunk
+  static_assert(RECS % NW == 0, "records split evenly over the waves");
+  constexpr int RPW = RECS / NW;
+  constexpr int CHUNK = RECS * 1024;    // bytes per LDS buffer
+  constexpr int NL = ChunkMeta<SPG>::NL;
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int j = lane & 15;
+  const int kq = lane >> 4;
+  const int ks = a.ks > 1 ? a.ks : 1;
+  const int wgs = (int)(gridDim.x / ks);  // workgroups per split
+  const int lt = xcd_tile(blockIdx.x, gridDim.x);
+  const int kidx = lt / wgs;
+  const int tg = lt - kidx * wgs;
+  const int tile0 = (tg * NW + wave) * TN;  // this wave's first tile
+  const int ntiles = (a.N + kTileN - 1) / kTileN;
+  const int ng = a.K / (32 * SPG);
+  const int nblk = (a.K + 127) >> 7;
+  const int nsteps = a.K >> 5;
+  const int b0 = (int)((int64_t)nblk * kidx / ks);
+  const int b1 = (int)((int64_t)nblk * (kidx + 1) / ks);
+  const UnpackConsts kc;
+
+  // activation records: record r of a chunk is (row tile t, step sl) =
+  // (r / (4 CB), r % (4 CB)), stored at r KiB of the buffer; lane l holds
+  // row 16 t + l % 16, rows 8 (4 st + l / 16) .. +7 of the operand
+  __amdgpu_buffer_rsrc_t rx;
+  uint32_t x_lane, x_t, x_st;
+  if constexpr (PREP) {
+    const uint32_t nst = 4u * (uint32_t)nblk;
+    rx = buffer_rsrc(a.X, (uint32_t)((a.M + 15) / 16) * nst * 1024u);
+    x_lane = (uint32_t)lane * 16u;
+    x_t = nst * 1024u;
+    x_st = 1024u;
+  } else {
+    rx = buffer_rsrc(a.X, (uint32_t)a.M * (uint32_t)a.ldx * 2u);
+    x_lane = ((uint32_t)j * (uint32_t)a.ldx + 8u * (uint32_t)kq) * 2u;
+    x_t = 16u * (uint32_t)a.ldx * 2u;
+    x_st = 64u;
+  }
+  auto issue_a = [&](int cb0, int buf) {
+#pragma unroll
+    for (int i = 0; i < RPW; ++i) {
+      const int r = wave * RPW + i;
+      const int t = r / (4 * CB), sl = r % (4 * CB);
+      const int st = 4 * cb0 + sl;
+      uint32_t off = st < nsteps ? x_lane + (uint32_t)t * x_t + (uint32_t)st * x_st : kOutOfRange;
+      asm("" : "+v"(off));
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(
+          rx, (__attribute__((address_space(3))) void*)(smem + buf * CHUNK + r * 1024), 16, off, 0,
+          0, 0);
+    }
+  };
+
+  ChunkMeta<SPG> cm[TN];
+  WeightStream<TPDQ_LAYOUT_TILED> wsrc[TN];
+#pragma unroll
+  for (int n = 0; n < TN; ++n) {
+    cm[n].init(a, ng, (tile0 + n) * kTileN + j, kq);
+    wsrc[n].init(a, tile0 + n, tile0 + n < ntiles, lane, kq, (tile0 + n) * kTileN + j, nblk);
+  }
+  u4_t wb[D][TN];
+  auto fetch = [&](int b, int slot) {
+#pragma unroll
+    for (int n = 0; n < TN; ++n) wb[slot][n] = wsrc[n].fetch(b, b < b1, a.ldq);
+  };
+
+  // prologue, in the order the loads are needed
+  issue_a(b0, 0);
+  __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+  for (int n = 0; n < TN; ++n) cm[n].load((4 * b0) / SPG, b0 < b1, ng, kq);
+  __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+  for (int i = 0; i < D; ++i) {
+    fetch(b0 + i, i);
+    __builtin_amdgcn_sched_barrier(0);
+  }
+
+  f4_t acc[MT][TN], gacc[MT][TN];
+#pragma unroll
+  for (int t = 0; t < MT; ++t)
+#pragma unroll
+    for (int n = 0; n < TN; ++n) {
+      acc[t][n] = f4_t{0.f, 0.f, 0.f, 0.f};
+      gacc[t][n] = f4_t{0.f, 0.f, 0.f, 0.f};
+    }
+  const f4_t fz = {0.f, 0.f, 0.f, 0.f};
+  float s_cur[TN];
+  uint32_t z1024[TN], z64[TN];
+#pragma unroll
+  for (int n = 0; n < TN; ++n) {
+    s_cur[n] = 0.f;
+    z1024[n] = 0x64006400u;
+    z64[n] = 0x54005400u;
+  }
+
+  // block c + i, its activations in LDS buffer `buf`
+  auto block = [&](int c, int i, int buf, const u4_t (&w)[TN]) {
+    const int b = c + i;
+    const u4_t* ab = (const u4_t*)(smem + buf * CHUNK);
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int st = 4 * b + u;
+      bool open, close;
+      if constexpr (SPG <= 4) {
+        open = (u % SPG) == 0;
+        close = (u % SPG) == SPG - 1;
+      } else {  // SPG == 8: a group is blocks 2g and 2g + 1
+        open = u == 0 && ((b & 1) == 0 || b == b0);
+        close = u == 3 && ((b & 1) == 1 || b == b1 - 1);
+      }
+      if (open) {
+#pragma unroll
+        for (int n = 0; n < TN; ++n) {
+          if constexpr (SPG <= 4) {
+            const int rel = (4 * i + u) / SPG;
+            cm[n].get(rel >> 2, 16 * (rel & 3) + j, s_cur[n], z1024[n], z64[n]);
+          } else {
+            const int rel = st / SPG - (4 * c) / SPG;
+            cm[n].get(0, 16 * rel + j, s_cur[n], z1024[n], z64[n]);
+          }
+        }
+      }
+      h8_t av[MT];
+#pragma unroll
+      for (int t = 0; t < MT; ++t) av[t] = as_h8(ab[(t * 4 * CB + 4 * i + u) * 64 + lane]);
+#pragma unroll
+      for (int n = 0; n < TN; ++n) {
+        const h8_t bv = unpack_sub(kc, w[n][u], z1024[n], z64[n]);
+#pragma unroll
+        for (int t = 0; t < MT; ++t)
+          gacc[t][n] = mfma16x16x32(av[t], bv, open ? fz : gacc[t][n]);
+      }
+      if (close) {
+#pragma unroll
+        for (int t = 0; t < MT; ++t)
+#pragma unroll
+          for (int n = 0; n < TN; ++n) acc[t][n] += s_cur[n] * gacc[t][n];
+      }
+    }
+  };
+
+  // Chunk c (blocks c .. c + 3): its activations were loaded with the LDS
+  // bit before the metadata of this chunk and the D = 4 weight fetches that
+  // followed, and loads complete in order; after the barrier every wave's
+  // records of chunk c are in LDS and every wave is done with chunk c - 4's
+  // buffer, which receives chunk c + 4.
+  int buf = 0;
+  for (int c = b0; c < b1; c += CB) {
+    asm volatile("s_waitcnt vmcnt(%0)\n\ts_waitcnt lgkmcnt(0)\n\ts_barrier" ::"n"(TN * (2 * NL + D))
+                 : "memory");
+    issue_a(c + CB, buf ^ 1);
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int n = 0; n < TN; ++n) {
+      cm[n].decode();
+      cm[n].load((4 * (c + 4)) / SPG, c + 4 < b1, ng, kq);
+    }
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int i = 0; i < CB; ++i) {
+      const int b = c + i;
+      if (b < b1) block(c, i, buf, wb[i % D]);
+      fetch(b + D, i % D);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    buf ^= 1;
+  }
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+
+  // each wave owns its columns: acc[t][n] of lane (j, kq) holds rows
+  // 16 t + 4 kq .. +3, column 16 (tile0 + n) + j
+  float* part = a.part + (size_t)kidx * a.M * a.N;
+#pragma unroll
+  for (int t = 0; t < MT; ++t)
+#pragma unroll
+    for (int n = 0; n < TN; ++n) {
+      const int col = (tile0 + n) * kTileN + j;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int row = t * kTileM + 4 * kq + e;
+        if (row < a.M && col < a.N) {
+          if (ks > 1)
+            part[(int64_t)row * a.N + col] = acc[t][n][e];
+          else
+            a.Y[(int64_t)row * a.ldy + col] = float_to_half_bits(acc[t][n][e]);
+        }
+      }
+    }
+}
+
 // ---------------------------------------------------------------------------
 // Row-metadata kernel: each of the 8 rows of a word looks its group up
 // (g_idx, or floor(k / G) when g_idx is NULL) and is dequantized on its own.
@@ -881,6 +1094,27 @@ DecodeKernel pick_layout(const DecodePlan& p) {
   return nullptr;
 }
 
+template <int MT, int TN, bool PREP>
+DecodeKernel pick_wide_spg(int spg) {
+  switch (spg) {
+    case 1: return k_wide<MT, kWideWaves, 1, TN, PREP>;
+    case 2: return k_wide<MT, kWideWaves, 2, TN, PREP>;
+    case 4: return k_wide<MT, kWideWaves, 4, TN, PREP>;
+    case 8: return k_wide<MT, kWideWaves, 8, TN, PREP>;
+  }
+  return nullptr;
+}
+
+DecodeKernel pick_wide(const DecodePlan& p) {
+  const bool prep = p.amode == kAGlobalPrep;
+  switch (p.mt) {
+    case 1: return prep ? pick_wide_spg<1, 1, true>(p.spg) : pick_wide_spg<1, 1, false>(p.spg);
+    case 2: return prep ? pick_wide_spg<2, 1, true>(p.spg) : pick_wide_spg<2, 1, false>(p.spg);
+    case 4: return prep ? pick_wide_spg<4, 1, true>(p.spg) : pick_wide_spg<4, 1, false>(p.spg);
+  }
+  return nullptr;
+}
+
 DecodeKernel pick_kernel(const DecodePlan& p) {
   if (p.layout == TPDQ_LAYOUT_TILED) return pick_layout<TPDQ_LAYOUT_TILED>(p);
   return pick_layout<TPDQ_LAYOUT_GPTQ>(p);
@@ -945,6 +1179,18 @@ bool plan_decode(int M, int K, int N, int G, int num_groups, int layout, int met
     nw = (!a_global(am) && nblk >= 48 && ntiles <= 256) ? 8 : 4;
     if (a_global(am) && ntiles >= 512) tn = 2;
   }
+  // the wide kernel when X is read from global memory and the weights are
+  // large (the decode kernel re-reads X for every 16 columns): 8 waves over
+  // 128 columns share X through LDS, K split until about kWideTargetWgs
+  // workgroups stream
+  p->wide = meta == kMetaGroup && layout == TPDQ_LAYOUT_TILED && a_global(am) &&
+            (int64_t)K * N >= kWideMinWeights;
+  p->ks = 1;
+  if (p->wide) {
+    const int nblk = (K + 127) / 128;
+    const int wgs = (ntiles + kWideWaves - 1) / kWideWaves;
+    p->ks = std::max(1, std::min((kWideTargetWgs + wgs - 1) / wgs, std::max(1, nblk / 4)));
+  }
   p->tn = tn;
   p->layout = layout;
   p->meta = meta;
@@ -960,10 +1206,30 @@ bool plan_decode(int M, int K, int N, int G, int num_groups, int layout, int met
   const size_t red_final = (size_t)nw * mt * tn * 1024;  // reduce_store's partial tiles
   if (need < red_final) need = red_final;
   p->lds_bytes = need;
+  if (p->wide) {
+    p->lds_bytes = (size_t)2 * mt * 16 * 1024;  // two chunks of 4 blocks of activations
+    return pick_wide(*p) != nullptr;
+  }
   return pick_kernel(*p) != nullptr;
 }
 
-hipError_t launch_decode(const GemmArgs& a0, const DecodePlan& p, hipStream_t s) {
+hipError_t launch_decode(const GemmArgs& a0, const DecodePlan& p, float* part, hipStream_t s) {
+  if (p.wide) {
+    DecodeKernel k = pick_wide(p);
+    if (!k || (p.ks > 1 && !part)) return hipErrorInvalidValue;
+    GemmArgs a = a0;
+    a.ks = p.ks;
+    a.part = part;
+    hipError_t e = hipFuncSetAttribute((const void*)k, hipFuncAttributeMaxDynamicSharedMemorySize,
+                                       (int)p.lds_bytes);
+    if (e != hipSuccess) return e;
+    const int ntiles = (a.N + kTileN - 1) / kTileN;
+    const int wgs = (ntiles + kWideWaves - 1) / kWideWaves;
+    hipLaunchKernelGGL(k, dim3(wgs * p.ks), dim3(kWideWaves * 64), p.lds_bytes, s, a);
+    e = hipGetLastError();
+    if (e != hipSuccess || p.ks == 1) return e;
+    return launch_splitk_reduce(part, p.ks, a.M, a.N, a.Y, a.ldy, s);
+  }
   DecodeKernel k = pick_kernel(p);
   if (!k) return hipErrorInvalidValue;
   GemmArgs a = a0;

@@ -405,9 +405,14 @@ hipError_t launch_mtile(const GemmArgs& a0, const MtilePlan& p, float* part, hip
   else
     return hipErrorInvalidValue;
   if (e != hipSuccess || p.ks == 1) return e;
-  const int64_t total = (int64_t)a.M * a.N / 4 + 1;
+  return launch_splitk_reduce(part, p.ks, a.M, a.N, a.Y, a.ldy, s);
+}
+
+hipError_t launch_splitk_reduce(const float* part, int ks, int M, int N, uint16_t* Y, int64_t ldy,
+                                hipStream_t s) {
+  const int64_t total = (int64_t)M * N / 4 + 1;
   const int blocks = (int)std::min<int64_t>((total + 255) / 256, 16384);
-  hipLaunchKernelGGL(k_splitk_reduce, dim3(blocks), dim3(256), 0, s, part, p.ks, a.M, a.N, a.Y, a.ldy);
+  hipLaunchKernelGGL(k_splitk_reduce, dim3(blocks), dim3(256), 0, s, part, ks, M, N, Y, ldy);
   return hipGetLastError();
 }
 

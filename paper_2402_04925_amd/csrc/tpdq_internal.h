@@ -80,7 +80,15 @@ struct DecodePlan {
   size_t lds_bytes;
   int lds_x_off;
   int lds_xr_off;
+  bool wide;    // k_wide: waves over columns, X shared through LDS in chunks
+  int ks;       // k_wide: K splits (fp32 partials, then k_splitk_reduce)
 };
+// k_wide: 8 waves (128 columns) per workgroup; used on weights of at least
+// kWideMinWeights elements when X does not fit in LDS, K split until about
+// kWideTargetWgs workgroups stream.
+constexpr int kWideWaves = 8;
+constexpr int64_t kWideMinWeights = (int64_t)64 << 20;
+constexpr int kWideTargetWgs = 200;
 
 // meta_pref: kMetaGroup for sorted rows (needs G % 32 == 0), otherwise a
 // per-row mode; operand: an Operand. Returns false when no decode kernel
@@ -88,7 +96,8 @@ struct DecodePlan {
 // caller then runs launch_gather_prep and plans with kOperandPrepared).
 bool plan_decode(int M, int K, int N, int G, int num_groups, int layout, int meta_pref, int operand,
                  DecodePlan* p);
-hipError_t launch_decode(const GemmArgs& a, const DecodePlan& p, hipStream_t s);
+// part: the workspace for k_wide's split-K partials (ks x M x N floats)
+hipError_t launch_decode(const GemmArgs& a, const DecodePlan& p, float* part, hipStream_t s);
 // Xp [M][K] = X[:, perm] (perm may be NULL), each octet in operand order.
 hipError_t launch_gather_prep(const uint16_t* X, int64_t ldx, int M, int K, const int32_t* perm,
                               int layout, uint16_t* Xp, hipStream_t s);
@@ -113,6 +122,8 @@ bool plan_mtile(int M, int64_t ldx, const tpdq_w4* w, int meta, MtilePlan* p);
 size_t mtile_part_bytes(const MtilePlan& p, int M, int N);
 // part: the partials (ignored when p.ks == 1)
 hipError_t launch_mtile(const GemmArgs& a, const MtilePlan& p, float* part, hipStream_t s);
+hipError_t launch_splitk_reduce(const float* part, int ks, int M, int N, uint16_t* Y, int64_t ldy,
+                                hipStream_t s);
 // Xp [M][K] = X[:, perm] row-major (for the prefill GEMM's activations)
 hipError_t launch_gather_rows(const uint16_t* X, int64_t ldx, int M, int K, const int32_t* perm,
                               uint16_t* Xp, hipStream_t s);
