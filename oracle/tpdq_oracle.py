@@ -5,11 +5,13 @@ the tests, the smoke check and the CPU-baseline leg of the benchmark do. It is a
 plain, slow, obviously correct restatement of what the paper computes, written
 with numpy and sharing no code with the HIP kernels.
 
-Precision: dequantized weights are formed exactly in float64 (an fp16 scale
-times a small integer is exact), GEMMs accumulate in float64 (or float32 when
-asked), and every tensor the paper's experiments hold in FP16 (Y1, Y2) is
-rounded to fp16 with round-to-nearest-even (numpy's float64 -> float16 cast
-rounds once, correctly).
+Precision: dequantized weights are formed exactly in float64 (an fp16 or
+bf16 scale times a small integer is exact), GEMMs accumulate in float64 (or
+float32 when asked), and every tensor the paper's experiments hold in FP16
+(Y1, Y2) is rounded to fp16 with round-to-nearest-even (numpy's float64 ->
+float16 cast rounds once, correctly). With dtype="bf16" (not in the paper:
+the activations and scales are bfloat16) Y1 and Y2 are rounded to bfloat16
+instead, also once and to nearest even (to_bf16).
 
 Readings of the paper taken here (the paper is silent on them):
   * dequant is asymmetric: w = s * (q - z) with q, z the stored int4 codes;
@@ -214,15 +216,38 @@ def to_fp16(a) -> np.ndarray:
     return np.asarray(a).astype(np.float16)
 
 
+def to_bf16(a) -> np.ndarray:
+    """Round to bfloat16 (8 significant bits, ties to even), once, from the
+    float64 value; returned as float32, which holds every bfloat16 exactly.
+
+    With x = m * 2**e and 1/2 <= |m| < 1, the rounded value is
+    round(m * 2**8) * 2**(e - 8), numpy's round sending halves to the even
+    integer. Normal range only (|x| >= 2**-126): the values here are far
+    from both ends of it."""
+    x = np.asarray(a, dtype=np.float64)
+    m, e = np.frexp(x)
+    return np.ldexp(np.round(m * 256.0), e - 8).astype(np.float32)
+
+
+def round_to(a, dtype="fp16") -> np.ndarray:
+    """Round to the storage type of activations and outputs."""
+    if dtype == "fp16":
+        return to_fp16(a)
+    if dtype == "bf16":
+        return to_bf16(a)
+    raise ValueError(f"unknown dtype {dtype}")
+
+
 def w4a16_gemm(X, qweight, scales, qzeros, g_idx, x_perm=None, acc="f64", cols=None,
-               round_fp16=True):
+               round_fp16=True, dtype="fp16"):
     """Y[m][n] = sum_k X'[m][k] * W[k][n] with X' = X[:, x_perm] when a gather
-    is given (the X[:, P1] of Alg. 2 and Alg. 3), rounded to fp16."""
+    is given (the X[:, P1] of Alg. 2 and Alg. 3), rounded to fp16 (or to
+    bfloat16 with dtype="bf16"; round_fp16=False keeps the float64 sum)."""
     X = np.asarray(X)
     if x_perm is not None:
         X = X[:, np.asarray(x_perm, dtype=np.int64)]
     Y = matmul(X, dequant(qweight, scales, qzeros, g_idx, cols), acc)
-    return to_fp16(Y) if round_fp16 else Y
+    return round_to(Y, dtype) if round_fp16 else Y
 
 
 # ----------------------------------------------------------------------------
@@ -302,13 +327,15 @@ def _layer(w, g):
     return w["qweight"], w["scales"], w["qzeros"], g
 
 
-def mlp_reference(X, w1, g1, w2, g2, acc="f64", y1_fp16=True):
-    """Unsharded act-order MLP: Y2 = (X @ deq(W1)) @ deq(W2), Y1 in fp16."""
-    Y1 = w4a16_gemm(X, *_layer(w1, g1), acc=acc, round_fp16=y1_fp16)
-    return w4a16_gemm(Y1, *_layer(w2, g2), acc=acc)
+def mlp_reference(X, w1, g1, w2, g2, acc="f64", y1_fp16=True, dtype="fp16"):
+    """Unsharded act-order MLP: Y2 = (X @ deq(W1)) @ deq(W2), Y1 in fp16 (or
+    the dtype given)."""
+    Y1 = w4a16_gemm(X, *_layer(w1, g1), acc=acc, round_fp16=y1_fp16, dtype=dtype)
+    return w4a16_gemm(Y1, *_layer(w2, g2), acc=acc, dtype=dtype)
 
 
-def mlp_tp_aware_rank(X, P1, w1f_shard, w2f_shard, G, acc="f64", y1_fp16=True, round_y2=True):
+def mlp_tp_aware_rank(X, P1, w1f_shard, w2f_shard, G, acc="f64", y1_fp16=True, round_y2=True,
+                      dtype="fp16"):
     """Alg. 3 on one rank, up to its AllReduce:
       Y1_local = X[:, P1] @ W1_local   (W1_local a column shard of W1[P1, P2])
       Y2_local = Y1_local @ W2_local   (W2_local a row shard of W2[P2])
@@ -317,17 +344,19 @@ def mlp_tp_aware_rank(X, P1, w1f_shard, w2f_shard, G, acc="f64", y1_fp16=True, r
     K1 = w1f_shard["qweight"].shape[0] * 8
     K2 = w2f_shard["qweight"].shape[0] * 8
     Y1 = w4a16_gemm(X, *_layer(w1f_shard, g_idx_naive(K1, G)), x_perm=P1, acc=acc,
-                    round_fp16=y1_fp16)
-    Y2 = w4a16_gemm(Y1, *_layer(w2f_shard, g_idx_naive(K2, G)), acc=acc, round_fp16=round_y2)
+                    round_fp16=y1_fp16, dtype=dtype)
+    Y2 = w4a16_gemm(Y1, *_layer(w2f_shard, g_idx_naive(K2, G)), acc=acc, round_fp16=round_y2,
+                    dtype=dtype)
     return Y1, Y2
 
 
-def mlp_actorder_rank(X, w1_shard, g1, w2_shard, g2_shard, acc="f64", y1_fp16=True, round_y2=True):
+def mlp_actorder_rank(X, w1_shard, g1, w2_shard, g2_shard, acc="f64", y1_fp16=True, round_y2=True,
+                      dtype="fp16"):
     """The act-order (no reorder) MLP on one rank: column shard of W1 with its
     g_idx, row shard of W2 with the global g_idx values of its rows and the
     full metadata (Eq. 3 loads, Fig. 1)."""
-    Y1 = w4a16_gemm(X, *_layer(w1_shard, g1), acc=acc, round_fp16=y1_fp16)
-    Y2 = w4a16_gemm(Y1, *_layer(w2_shard, g2_shard), acc=acc, round_fp16=round_y2)
+    Y1 = w4a16_gemm(X, *_layer(w1_shard, g1), acc=acc, round_fp16=y1_fp16, dtype=dtype)
+    Y2 = w4a16_gemm(Y1, *_layer(w2_shard, g2_shard), acc=acc, round_fp16=round_y2, dtype=dtype)
     return Y1, Y2
 
 
@@ -388,7 +417,8 @@ def fold_sample(qweight, P_row, P_col, rows, cols):
     return ((words >> shift) & np.uint32(0xF)).astype(np.int64)
 
 
-def mlp_rank_from_global(X, l1, l2, rank, tp, ordered, P2=None, cols2=None, acc="f64"):
+def mlp_rank_from_global(X, l1, l2, rank, tp, ordered, P2=None, cols2=None, acc="f64",
+                         dtype="fp16"):
     """One rank's (Y1, Y2 partial[:, cols2]) computed from the unpermuted
     global layers l1 = (qweight, scales, qzeros, g_idx) and l2.
 
@@ -403,9 +433,9 @@ def mlp_rank_from_global(X, l1, l2, rank, tp, ordered, P2=None, cols2=None, acc=
     n = N1 // tp
     blk = np.arange(rank * n, (rank + 1) * n)
     sel = np.asarray(P2, dtype=np.int64)[blk] if ordered else blk
-    Y1 = to_fp16(matmul(X, dequant(*l1, cols=sel), acc))
+    Y1 = round_to(matmul(X, dequant(*l1, cols=sel), acc), dtype)
     W2 = dequant(*l2, cols=cols2)[sel]
-    Y2 = to_fp16(matmul(Y1, W2, acc))
+    Y2 = round_to(matmul(Y1, W2, acc), dtype)
     return Y1, Y2
 
 

@@ -14,7 +14,7 @@ K input channels and g_idx[i] = floor(phi(i) / G).
 
 Storage format (the library's, fixed here):
   qweight int32 [K/8][N]   nibble j (bits 4j..4j+3) of word [r][n] = row 8r+j
-  scales  fp16  [K/G][N]
+  scales  fp16  [K/G][N]   (or bfloat16 values, held in float32 arrays)
   qzeros  int32 [K/G][N/8] nibble j of word [g][c] = column 8c+j
 Uniform int4 codes packed eight to a word are exactly uniform 32-bit words, so
 qweight and qzeros are drawn as random words.
@@ -81,19 +81,32 @@ def random_words(shape, rng: np.random.Generator) -> np.ndarray:
     return rng.integers(0, 1 << 32, size=shape, dtype=np.uint64).astype(np.uint32).view(np.int32)
 
 
+BF16 = "bf16"  # dtype tag: bfloat16 values held in float32 arrays
+
+
+def _store(a: np.ndarray, dtype) -> np.ndarray:
+    """The drawn values in the storage type: numpy's cast for fp16; for
+    bfloat16, torch's CPU cast of the float32 values, kept in float32."""
+    if dtype == BF16:
+        import torch
+        t = torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).to(torch.bfloat16)
+        return t.to(torch.float32).numpy()
+    return a.astype(dtype)
+
+
 def random_scales(shape, rng: np.random.Generator, lo=0.002, hi=0.02, dtype=np.float16) -> np.ndarray:
-    return rng.uniform(lo, hi, size=shape).astype(dtype)
+    return _store(rng.uniform(lo, hi, size=shape), dtype)
 
 
 def random_activations(M: int, K: int, rng: np.random.Generator, dtype=np.float16) -> np.ndarray:
-    return rng.standard_normal((M, K)).astype(dtype)
+    return _store(rng.standard_normal((M, K)), dtype)
 
 
 @dataclasses.dataclass
 class QuantLinear:
     """One GPTQ-style act-order layer in the library's storage format."""
     qweight: np.ndarray   # int32 [K/8][N]
-    scales: np.ndarray    # fp16 [K/G][N]
+    scales: np.ndarray    # fp16 [K/G][N] (bf16 layers: float32 holding bf16 values)
     qzeros: np.ndarray    # int32 [K/G][N/8]
     g_idx: np.ndarray     # int32 [K]
     phi: np.ndarray       # int32 [K], the emulated act-order permutation
@@ -123,12 +136,12 @@ def make_layer(K: int, N: int, G: int, cfg_id: int, t_phi: int, t_qw: int, t_s: 
     )
 
 
-def make_workload(w: Workload, seed: int = BASE_SEED):
+def make_workload(w: Workload, seed: int = BASE_SEED, scale_dtype=np.float16):
     """Global (unsharded) layers of a workload: (W1, W2-or-None)."""
-    w1 = make_layer(w.K1, w.N1, w.G, w.cfg_id, T_PHI1, T_QW1, T_S1, T_Z1, seed)
+    w1 = make_layer(w.K1, w.N1, w.G, w.cfg_id, T_PHI1, T_QW1, T_S1, T_Z1, seed, scale_dtype)
     w2 = None
     if w.N2:
-        w2 = make_layer(w.K2, w.N2, w.G, w.cfg_id, T_PHI2, T_QW2, T_S2, T_Z2, seed)
+        w2 = make_layer(w.K2, w.N2, w.G, w.cfg_id, T_PHI2, T_QW2, T_S2, T_Z2, seed, scale_dtype)
     return w1, w2
 
 
@@ -137,10 +150,11 @@ def make_x(w: Workload, M: int, seed: int = BASE_SEED, dtype=np.float16) -> np.n
     return random_activations(M, w.K1, rng, dtype)
 
 
-def make_custom(K1: int, N1: int, N2: int, G: int, seed: int, cfg_id: int = 100, identity_phi=False):
+def make_custom(K1: int, N1: int, N2: int, G: int, seed: int, cfg_id: int = 100, identity_phi=False,
+                scale_dtype=np.float16):
     """Small ad-hoc layers for tests (ragged shapes, special cases)."""
-    w1 = make_layer(K1, N1, G, cfg_id, T_PHI1, T_QW1, T_S1, T_Z1, seed)
-    w2 = make_layer(N1, N2, G, cfg_id, T_PHI2, T_QW2, T_S2, T_Z2, seed) if N2 else None
+    w1 = make_layer(K1, N1, G, cfg_id, T_PHI1, T_QW1, T_S1, T_Z1, seed, scale_dtype)
+    w2 = make_layer(N1, N2, G, cfg_id, T_PHI2, T_QW2, T_S2, T_Z2, seed, scale_dtype) if N2 else None
     if identity_phi:
         for w in (w1, w2):
             if w is not None:

@@ -395,10 +395,52 @@ def pin_tiled_layout(o):
     assert np.all(qt2.view(np.uint32)[~used] == 0)
 
 
+
+# ------------------------------------------------------------- bfloat16 ---
+
+def pin_bf16_rounding(o, seed=21):
+    """to_bf16 against torch's CPU float32 -> bfloat16 cast (a library
+    routine) over a wide exponent range, and against hand-worked values:
+    ties go to the even significand, and a float64 value just above a tie
+    rounds up although its float32 rounding sits on the tie (one rounding,
+    not two)."""
+    import torch
+    rng = np.random.default_rng(seed)
+    x = (rng.standard_normal(4096) * np.exp2(rng.integers(-60, 60, 4096))).astype(np.float32)
+    ref = torch.from_numpy(x).to(torch.bfloat16).to(torch.float32).numpy()
+    assert np.array_equal(o.to_bf16(x).view(np.uint32), ref.view(np.uint32))
+    cases = [
+        (1.0 + 2.0 ** -8, 1.0),                        # tie -> even significand 1.0000000
+        (1.0 + 3 * 2.0 ** -8, 1.0 + 2.0 ** -6),        # tie -> even 1.0000010
+        (-(1.0 + 3 * 2.0 ** -8), -(1.0 + 2.0 ** -6)),
+        (255.5, 256.0),                                # 9 significant bits, tie -> 2^8
+        (1.0 + 2.0 ** -8 + 2.0 ** -30, 1.0 + 2.0 ** -7),  # just above the tie
+        (3.0, 3.0), (0.0, 0.0), (2.0 ** -100, 2.0 ** -100),
+    ]
+    for v, want in cases:
+        assert float(o.to_bf16(np.array([v]))[0]) == want, (v, want)
+
+
+def pin_bf16_gemm(o, seed=22):
+    """The bfloat16 GEMM's output is the exact product rounded once to
+    bfloat16: every value is a bfloat16 (low 16 bits of its float32 zero) and
+    lies within half a unit in the last place (2^-8 relative) of the float64
+    sum; an fp16 rounding would leave values bfloat16 cannot hold."""
+    w1, _ = inputs.make_custom(256, 64, 0, 32, seed, scale_dtype=inputs.BF16)
+    X = inputs.random_activations(5, 256, np.random.default_rng(seed), dtype=inputs.BF16)
+    args = (X, w1.qweight, w1.scales, w1.qzeros, w1.g_idx)
+    Y = o.w4a16_gemm(*args, dtype="bf16")
+    Y64 = o.w4a16_gemm(*args, round_fp16=False)
+    y = np.asarray(Y, dtype=np.float32)
+    assert np.all(y.view(np.uint32) & 0xFFFF == 0)
+    assert np.all(np.abs(y.astype(np.float64) - Y64) <= np.exp2(-8) * np.abs(Y64))
+    assert np.max(np.abs(Y64)) > 1.0  # a non-trivial product
+
+
 ALL_PINS = [
     pin_unpack_bruteforce, pin_pack_roundtrip, pin_golden_gemm_codes, pin_worked_reorder,
     pin_reorder_closed_form, pin_identity_phi, pin_check_groups, pin_golden_gemm,
     pin_gemm_bruteforce, pin_one_hot_rows, pin_special_cases, pin_ordered_equals_actorder,
     pin_tp_aware_mlp, pin_actorder_shard_mlp, pin_alg2_equals_alg3, pin_fold_elementwise,
-    pin_distinct_groups, pin_tiled_layout,
+    pin_distinct_groups, pin_tiled_layout, pin_bf16_rounding, pin_bf16_gemm,
 ]

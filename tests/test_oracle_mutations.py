@@ -92,12 +92,22 @@ def _row_shard_no_offset(w, rank, tp, G, keep_all_groups=False):
 
 
 def _gemm_ignores_perm(X, qweight, scales, qzeros, g_idx, x_perm=None, acc="f64", cols=None,
-                       round_fp16=True):
-    return _orig["w4a16_gemm"](X, qweight, scales, qzeros, g_idx, None, acc, cols, round_fp16)
+                       round_fp16=True, dtype="fp16"):
+    return _orig["w4a16_gemm"](X, qweight, scales, qzeros, g_idx, None, acc, cols, round_fp16, dtype)
 
 
 def _eq3_ceil(phi, G):
     return -(-np.asarray(phi, dtype=np.int64) // G)
+
+
+def _bf16_truncate(a):
+    x = np.asarray(a, dtype=np.float64)
+    m, e = np.frexp(x)
+    return np.ldexp(np.trunc(m * 256.0), e - 8).astype(np.float32)
+
+
+def _round_to_fp16_always(a, dtype="fp16"):
+    return np.asarray(a).astype(np.float16)
 
 
 MUTANTS = {
@@ -115,6 +125,8 @@ MUTANTS = {
     "row_shard:offset": _row_shard_no_offset,
     "w4a16_gemm:perm": _gemm_ignores_perm,
     "g_idx_actorder:ceil": _eq3_ceil,
+    "to_bf16:truncate": _bf16_truncate,
+    "round_to:fp16": _round_to_fp16_always,
 }
 
 
