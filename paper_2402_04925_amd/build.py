@@ -15,7 +15,7 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 BUILD = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libtpdq.so")
-SOURCES = ["abi.hip", "gemm_decode.hip", "gemm_prefill.hip", "reorder.hip"]
+SOURCES = ["abi.hip", "gemm_decode.hip", "gemm_decode_bf16.hip", "gemm_prefill.hip", "reorder.hip"]
 ARCH = "gfx950"
 
 HIPCC_FLAGS = [
@@ -46,7 +46,7 @@ def _compile(src: str) -> str:
 def build(verbose: bool = False) -> str:
     """Compile every HIP source for gfx950 and link libtpdq.so in the package."""
     os.makedirs(BUILD, exist_ok=True)
-    with concurrent.futures.ThreadPoolExecutor(max_workers=min(4, len(SOURCES))) as ex:
+    with concurrent.futures.ThreadPoolExecutor(max_workers=len(SOURCES)) as ex:
         objs = list(ex.map(_compile, SOURCES))
     tmp = LIB + ".tmp"
     cmd = [hipcc(), "-shared", f"--offload-arch={ARCH}", "-fPIC", *objs, "-o", tmp]

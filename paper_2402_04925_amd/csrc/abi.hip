@@ -85,19 +85,19 @@ size_t mtile_gather_bytes(int M, int K, bool perm) { return perm ? align_up((siz
 // The decode plan of one launch of mc <= 64 rows, as run_gemm makes it: with
 // a perm, the gather inside the kernel's LDS if it fits, else the prepared
 // operand (*prepared).
-bool decode_plan_for(int mc, bool perm, const tpdq_w4* w, int meta, DecodePlan* plan,
+bool decode_plan_for(int mc, bool perm, const tpdq_w4* w, int meta, int dt, DecodePlan* plan,
                      bool* prepared) {
   *prepared = false;
   if (perm) {
     if (plan_decode(mc, w->K, w->N, w->group_size, w->num_groups, w->layout, meta, kOperandGather,
-                    plan))
+                    dt, plan))
       return true;
     *prepared = true;
     return plan_decode(mc, w->K, w->N, w->group_size, w->num_groups, w->layout, meta,
-                       kOperandPrepared, plan);
+                       kOperandPrepared, dt, plan);
   }
   return plan_decode(mc, w->K, w->N, w->group_size, w->num_groups, w->layout, meta, kOperandPlain,
-                     plan);
+                     dt, plan);
 }
 
 // split-K partials of the wide decode kernel (0 when K is not split)
@@ -107,15 +107,16 @@ size_t decode_part_bytes(const DecodePlan& p, int mc, int N) {
 
 // Bytes the call (X with leading dimension ldx, optional perm) uses. Decode:
 // [prepared operand][wide kernel's partials], the partials after the
-// prepared-operand region whenever either is used.
-size_t gemm_ws_need(int M, int64_t ldx, bool perm, const tpdq_w4* w, int meta) {
+// prepared-operand region whenever either is used. The plans, and so the
+// bytes, are the same for both element types.
+size_t gemm_ws_need(int M, int64_t ldx, bool perm, const tpdq_w4* w, int meta, int dt = TPDQ_FP16) {
   MtilePlan p;
   if (plan_mtile(M, perm ? (int64_t)w->K : ldx, w, meta, &p))
     return mtile_gather_bytes(M, w->K, perm) + mtile_part_bytes(p, M, w->N);
   DecodePlan dp;
   bool prepared = false;
   const int mc = std::min(M, kDecodeMaxM);  // the largest launch
-  if (!decode_plan_for(mc, perm, w, meta, &dp, &prepared)) return perm ? decode_gather_bytes(M, w->K) : 0;
+  if (!decode_plan_for(mc, perm, w, meta, dt, &dp, &prepared)) return perm ? decode_gather_bytes(M, w->K) : 0;
   const size_t part = decode_part_bytes(dp, mc, w->N);
   return (prepared || part ? decode_gather_bytes(M, w->K) : 0) + part;
 }
@@ -131,7 +132,7 @@ int meta_mode(tpdq_path path) {
 // when it fits in LDS, else into the workspace first (already in operand
 // order).
 tpdq_status run_gemm(const uint16_t* X, int64_t ldx, int M, const int32_t* perm, const tpdq_w4* w,
-                     tpdq_path path, uint16_t* Y, int64_t ldy, char* ws, hipStream_t st) {
+                     tpdq_path path, int dt, uint16_t* Y, int64_t ldy, char* ws, hipStream_t st) {
   const int meta = meta_mode(path);
   const int32_t* gidx = path == TPDQ_PATH_ORDERED ? nullptr : w->g_idx;
   MtilePlan mp;
@@ -160,6 +161,7 @@ tpdq_status run_gemm(const uint16_t* X, int64_t ldx, int M, const int32_t* perm,
     a.N = w->N;
     a.G = w->group_size;
     a.num_groups = w->num_groups;
+    a.dt = dt;
     a.Y = Y;
     a.ldy = ldy;
     float* part = (float*)(ws + mtile_gather_bytes(M, w->K, perm != nullptr));
@@ -173,7 +175,7 @@ tpdq_status run_gemm(const uint16_t* X, int64_t ldx, int M, const int32_t* perm,
     int64_t ldc = ldx;
     DecodePlan plan;
     bool prepared = false;
-    const bool ok = decode_plan_for(mc, perm != nullptr, w, meta, &plan, &prepared);
+    const bool ok = decode_plan_for(mc, perm != nullptr, w, meta, dt, &plan, &prepared);
     int operand = perm ? (prepared ? kOperandPrepared : kOperandGather) : kOperandPlain;
     if (ok && prepared) {
       uint16_t* Xp = (uint16_t*)ws;
@@ -201,6 +203,7 @@ tpdq_status run_gemm(const uint16_t* X, int64_t ldx, int M, const int32_t* perm,
     a.N = w->N;
     a.G = w->group_size;
     a.num_groups = w->num_groups;
+    a.dt = dt;
     a.Y = Y + (int64_t)m0 * ldy;
     a.ldy = ldy;
     float* part = (float*)(ws + decode_gather_bytes(M, w->K));
@@ -216,8 +219,7 @@ tpdq_status check_common(int32_t M, tpdq_path path, tpdq_dtype dtype) {
   if (M < 1) return fail(TPDQ_ERR_SHAPE, "M=%d must be >= 1", M);
   if (path != TPDQ_PATH_ACTORDER && path != TPDQ_PATH_ORDERED && path != TPDQ_PATH_ACTORDER_GLOBAL)
     return fail(TPDQ_ERR_SHAPE, "unknown path %d", (int)path);
-  if (dtype == TPDQ_BF16) return fail(TPDQ_ERR_UNSUPPORTED, "bf16 activations are not built yet");
-  if (dtype != TPDQ_FP16) return fail(TPDQ_ERR_SHAPE, "unknown dtype %d", (int)dtype);
+  if (dtype != TPDQ_FP16 && dtype != TPDQ_BF16) return fail(TPDQ_ERR_SHAPE, "unknown dtype %d", (int)dtype);
   return TPDQ_OK;
 }
 
@@ -385,13 +387,13 @@ tpdq_status tpdq_w4a16_gemm(const void* X, int64_t ldx, int32_t M, const int32_t
   // a call that uses a workspace (a gather always does) takes the documented
   // tpdq_workspace_bytes(1, ...), an upper bound of what it uses
   const size_t bound = tpdq_workspace_bytes(1, M, w, nullptr);
-  const size_t need = gemm_ws_need(M, ldx, x_perm != nullptr, w, meta_mode(path));
+  const size_t need = gemm_ws_need(M, ldx, x_perm != nullptr, w, meta_mode(path), dtype);
   if ((x_perm || need) && (!workspace || ws_bytes < bound))
     return fail(TPDQ_ERR_WORKSPACE, "GEMM needs %zu workspace bytes, got %zu", bound, ws_bytes);
   if (workspace && !aligned(workspace, 16))
     return fail(TPDQ_ERR_ALIGN, "workspace needs 16-byte alignment");
-  return run_gemm((const uint16_t*)X, ldx, M, x_perm, w, path, (uint16_t*)Y, ldy, (char*)workspace,
-                  (hipStream_t)stream);
+  return run_gemm((const uint16_t*)X, ldx, M, x_perm, w, path, dtype, (uint16_t*)Y, ldy,
+                  (char*)workspace, (hipStream_t)stream);
 }
 
 tpdq_status tpdq_mlp_shard(const void* X, int64_t ldx, int32_t M, const int32_t* P1,
@@ -420,8 +422,8 @@ tpdq_status tpdq_mlp_shard(const void* X, int64_t ldx, int32_t M, const int32_t*
     return fail(TPDQ_ERR_ALIGN, "Y1 needs 16-byte and Y2_partial 8-byte alignment");
   const int meta = meta_mode(path);
   const size_t bound = tpdq_workspace_bytes(2, M, w1, w2);
-  const size_t need = std::max(gemm_ws_need(M, ldx, !act, w1, meta),
-                               gemm_ws_need(M, w1->N, false, w2, meta));
+  const size_t need = std::max(gemm_ws_need(M, ldx, !act, w1, meta, dtype),
+                               gemm_ws_need(M, w1->N, false, w2, meta, dtype));
   if ((!act || need) && (!workspace || ws_bytes < bound))
     return fail(TPDQ_ERR_WORKSPACE, "MLP needs %zu workspace bytes, got %zu", bound, ws_bytes);
   if (workspace && !aligned(workspace, 16))
@@ -429,10 +431,11 @@ tpdq_status tpdq_mlp_shard(const void* X, int64_t ldx, int32_t M, const int32_t*
 
   hipStream_t s = (hipStream_t)stream;
   char* ws = (char*)workspace;
-  st = run_gemm((const uint16_t*)X, ldx, M, act ? nullptr : P1, w1, path, (uint16_t*)Y1, w1->N, ws, s);
+  st = run_gemm((const uint16_t*)X, ldx, M, act ? nullptr : P1, w1, path, dtype, (uint16_t*)Y1, w1->N,
+                ws, s);
   if (st != TPDQ_OK) return st;
-  return run_gemm((const uint16_t*)Y1, w1->N, M, nullptr, w2, path, (uint16_t*)Y2_partial, w2->N, ws,
-                  s);
+  return run_gemm((const uint16_t*)Y1, w1->N, M, nullptr, w2, path, dtype, (uint16_t*)Y2_partial,
+                  w2->N, ws, s);
 }
 
 }  // extern "C"

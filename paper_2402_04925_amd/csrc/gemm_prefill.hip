@@ -26,7 +26,8 @@
 // Dequantizing to fp16 before the MFMA rounds each weight once (relative
 // error 2^-12); the decode kernels keep q - z exact and scale in fp32, but
 // here that would double the accumulator registers and the VALU work per
-// MFMA.
+// MFMA. With bf16 activations the weight is formed in fp32 and rounded once
+// to bf16 (relative error 2^-9), about four times the VALU work of fp16.
 #include "kernels_common.h"
 
 #include <algorithm>
@@ -55,12 +56,26 @@ __device__ __forceinline__ void dma_to_lds(__amdgpu_buffer_rsrc_t r, void* dst, 
     __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_ptr_t)dst, 4, off, 0, 0, 0);
 }
 
-__device__ __forceinline__ h8_t dequant_scaled(const UnpackConsts& kc, uint32_t w, uint32_t z1024,
+__device__ __forceinline__ u4_t dequant_scaled(const UnpackConsts<kF16>& kc, uint32_t w, uint32_t z1024,
                                                uint32_t z64, uint32_t s2) {
   const h8_t d = unpack_sub(kc, w, z1024, z64);
   const h2_t s = as_h2(s2);
   const h8_t sv = {s.x, s.y, s.x, s.y, s.x, s.y, s.x, s.y};
-  return d * sv;
+  return __builtin_bit_cast(u4_t, d * sv);
+}
+
+// bf16: s (q - z) = (128 + q) s - (128 + z) s with zs = (128 + z) s; both
+// products are exact in fp32 (8 significant bits each), so one FMA gives
+// s (q - z) exactly and the conversion rounds it once.
+__device__ __forceinline__ u4_t dequant_scaled_bf16(const UnpackConsts<kBF16>& kc, uint32_t w,
+                                                    float s, float zs) {
+  const u4_t b = unpack_bias_bf16(kc, w);
+  u4_t r;
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+    r[i] = pack2<kBF16>(__builtin_fmaf(as_f32(b[i] << 16), s, -zs),
+                        __builtin_fmaf(as_f32(b[i] & 0xFFFF0000u), s, -zs));
+  return r;
 }
 
 // RT row tiles (16 RT rows of Y per workgroup), NW waves (64 columns each),
@@ -71,7 +86,7 @@ __device__ __forceinline__ h8_t dequant_scaled(const UnpackConsts& kc, uint32_t 
 // Two waves per SIMD (the 8-wave workgroup, or two 4-wave workgroups per CU):
 // 256 registers per lane, with the accumulators in the architectural VGPRs
 // (no accumulator copies between loop iterations).
-template <int SPG, int NW, int ST, int RT>
+template <int SPG, int NW, int ST, int RT, int DT>
 __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2))) void k_prefill(GemmArgs a) {
   // groups per 128-row block: G = 32, 64, 128 -> 4, 2, 1; G = 256 -> one
   // group spans two blocks (each block loads it)
@@ -111,7 +126,7 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2))) vo
   const int kb1 = (int)((int64_t)nblk_all * (kidx + 1) / ks);
   const int ng = a.num_groups;
   const int ntiles = (a.N + kTileN - 1) / kTileN;
-  const UnpackConsts kc;
+  const UnpackConsts<DT> kc;
 
   // sources: rows past M, groups past the last one and tiles past N load
   // zeros from the resource bounds
@@ -193,6 +208,7 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2))) vo
 #pragma unroll
     for (int i = 0; i < kPWT; ++i) w[i] = wb[i * 64 + lane];
     uint32_t z1024[kPWT], z64[kPWT], s2[kPWT];
+    float sf[kPWT], zs[kPWT];  // bf16
 #pragma unroll
     for (int u = 0; u < 4; ++u) {
       const bool open = SPG >= 4 ? u == 0 : (u % SPG) == 0;
@@ -204,19 +220,28 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2))) vo
           const uint32_t sv = *(const uint16_t*)(mb + gi * 128 + 2 * c);
           const uint32_t zw = *(const uint32_t*)(mb + 512 + gi * 32 + 4 * (c >> 3));
           const uint32_t zc = (zw >> (4 * (c & 7))) & 0xFu;
-          z1024[i] = (0x6400u | zc) * 0x10001u;
-          z64[i] = (0x5400u | (zc << 4)) * 0x10001u;
-          s2[i] = sv * 0x10001u;
+          if constexpr (DT == kBF16) {
+            sf[i] = bits_to_float<kBF16>(sv);
+            zs[i] = (128.f + (float)zc) * sf[i];
+          } else {
+            z1024[i] = (0x6400u | zc) * 0x10001u;
+            z64[i] = (0x5400u | (zc << 4)) * 0x10001u;
+            s2[i] = sv * 0x10001u;
+          }
         }
       }
-      h8_t av[RT];
+      u4_t av[RT];
 #pragma unroll
-      for (int r = 0; r < RT; ++r) av[r] = as_h8(ab[(r * 4 + u) * 64 + lane]);
+      for (int r = 0; r < RT; ++r) av[r] = ab[(r * 4 + u) * 64 + lane];
 #pragma unroll
       for (int i = 0; i < kPWT; ++i) {
-        const h8_t bv = dequant_scaled(kc, w[i][u], z1024[i], z64[i], s2[i]);
+        u4_t bv;
+        if constexpr (DT == kBF16)
+          bv = dequant_scaled_bf16(kc, w[i][u], sf[i], zs[i]);
+        else
+          bv = dequant_scaled(kc, w[i][u], z1024[i], z64[i], s2[i]);
 #pragma unroll
-        for (int r = 0; r < RT; ++r) acc[r][i] = mfma16x16x32(av[r], bv, acc[r][i]);
+        for (int r = 0; r < RT; ++r) acc[r][i] = mfma_k32<DT>(av[r], bv, acc[r][i]);
         if (4 * u + i < LPB) dma_item(bnext, sn, 4 * u + i);
       }
     }
@@ -260,16 +285,17 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2))) vo
           if (ks > 1)
             part[(int64_t)row * a.N + c] = acc[r][i][e];
           else
-            a.Y[(int64_t)row * a.ldy + c] = float_to_half_bits(acc[r][i][e]);
+            a.Y[(int64_t)row * a.ldy + c] = float_to_bits<DT>(acc[r][i][e]);
         }
       }
     }
 }
 
-// Y[m][n] = fp16(sum over s of part[s][m][n]), the splits added in order s =
+// Y[m][n] = round(sum over s of part[s][m][n]) to the element type, the splits added in order s =
 // 0, 1, ... (the result does not depend on which split finished first). Four
 // columns per thread: one 16-byte load per split, one 8-byte store (N % 4 ==
 // 0 and 16-byte aligned rows; otherwise one column per thread).
+template <int DT>
 __global__ __launch_bounds__(256) void k_splitk_reduce(const float* __restrict__ part, int ks, int M,
                                                        int N, uint16_t* __restrict__ Y, int64_t ldy) {
   const int64_t plane = (int64_t)M * N;
@@ -283,8 +309,8 @@ __global__ __launch_bounds__(256) void k_splitk_reduce(const float* __restrict__
       const float* src = part + (int64_t)m * N + c0;
       f4_t v = *(const f4_t*)src;
       for (int s = 1; s < ks; ++s) v += *(const f4_t*)(src + s * plane);
-      const uint32_t lo = float_to_half_bits(v[0]) | ((uint32_t)float_to_half_bits(v[1]) << 16);
-      const uint32_t hi = float_to_half_bits(v[2]) | ((uint32_t)float_to_half_bits(v[3]) << 16);
+      const uint32_t lo = pack2<DT>(v[0], v[1]);
+      const uint32_t hi = pack2<DT>(v[2], v[3]);
       *(uint2*)(Y + (int64_t)m * ldy + c0) = make_uint2(lo, hi);
     }
     return;
@@ -295,7 +321,7 @@ __global__ __launch_bounds__(256) void k_splitk_reduce(const float* __restrict__
     const int c = (int)(i - (int64_t)m * N);
     float v = part[i];
     for (int s = 1; s < ks; ++s) v += part[s * plane + i];
-    Y[(int64_t)m * ldy + c] = float_to_half_bits(v);
+    Y[(int64_t)m * ldy + c] = float_to_bits<DT>(v);
   }
 }
 
@@ -373,15 +399,15 @@ size_t mtile_part_bytes(const MtilePlan& p, int M, int N) {
   return p.ks > 1 ? align_up((size_t)p.ks * M * N * 4) : 0;
 }
 
-template <int NW, int ST, int RT>
+template <int NW, int ST, int RT, int DT>
 hipError_t launch_mtile_t(const GemmArgs& a, int ks, hipStream_t s) {
   typedef void (*Kern)(GemmArgs);
   Kern k = nullptr;
   switch (a.G / 32) {
-    case 1: k = k_prefill<1, NW, ST, RT>; break;
-    case 2: k = k_prefill<2, NW, ST, RT>; break;
-    case 4: k = k_prefill<4, NW, ST, RT>; break;
-    case 8: k = k_prefill<8, NW, ST, RT>; break;
+    case 1: k = k_prefill<1, NW, ST, RT, DT>; break;
+    case 2: k = k_prefill<2, NW, ST, RT, DT>; break;
+    case 4: k = k_prefill<4, NW, ST, RT, DT>; break;
+    case 8: k = k_prefill<8, NW, ST, RT, DT>; break;
   }
   if (!k) return hipErrorInvalidValue;
   const int lds = ST * pf_stage(RT, NW);
@@ -398,21 +424,25 @@ hipError_t launch_mtile(const GemmArgs& a0, const MtilePlan& p, float* part, hip
   a.part = part;
   if (p.ks > 1 && !part) return hipErrorInvalidValue;
   hipError_t e;
+  const bool bf = a.dt == kBF16;
   if (p.rt == 8 && p.nw == 8 && p.st == 2)
-    e = launch_mtile_t<8, 2, 8>(a, p.ks, s);
+    e = bf ? launch_mtile_t<8, 2, 8, kBF16>(a, p.ks, s) : launch_mtile_t<8, 2, 8, kF16>(a, p.ks, s);
   else if (p.rt == 4 && p.nw == 4 && p.st == 2)
-    e = launch_mtile_t<4, 2, 4>(a, p.ks, s);
+    e = bf ? launch_mtile_t<4, 2, 4, kBF16>(a, p.ks, s) : launch_mtile_t<4, 2, 4, kF16>(a, p.ks, s);
   else
     return hipErrorInvalidValue;
   if (e != hipSuccess || p.ks == 1) return e;
-  return launch_splitk_reduce(part, p.ks, a.M, a.N, a.Y, a.ldy, s);
+  return launch_splitk_reduce(part, p.ks, a.M, a.N, a.Y, a.ldy, a.dt, s);
 }
 
 hipError_t launch_splitk_reduce(const float* part, int ks, int M, int N, uint16_t* Y, int64_t ldy,
-                                hipStream_t s) {
+                                int dt, hipStream_t s) {
   const int64_t total = (int64_t)M * N / 4 + 1;
   const int blocks = (int)std::min<int64_t>((total + 255) / 256, 16384);
-  hipLaunchKernelGGL(k_splitk_reduce, dim3(blocks), dim3(256), 0, s, part, ks, M, N, Y, ldy);
+  if (dt == kBF16)
+    hipLaunchKernelGGL(k_splitk_reduce<kBF16>, dim3(blocks), dim3(256), 0, s, part, ks, M, N, Y, ldy);
+  else
+    hipLaunchKernelGGL(k_splitk_reduce<kF16>, dim3(blocks), dim3(256), 0, s, part, ks, M, N, Y, ldy);
   return hipGetLastError();
 }
 

@@ -1,5 +1,5 @@
-// Device helpers shared by the GEMM kernels of libtpdq (gfx950): fp16
-// vector types, the exact int4 unpack, MFMA and wait-count wrappers, and
+// Device helpers shared by the GEMM kernels of libtpdq (gfx950): fp16 and
+// bf16 vector types, the exact int4 unpack, MFMA and wait-count wrappers, and
 // raw buffer loads. Included by the .hip translation units only.
 #pragma once
 
@@ -10,6 +10,8 @@ namespace {
 
 typedef _Float16 h2_t __attribute__((ext_vector_type(2)));
 typedef _Float16 h8_t __attribute__((ext_vector_type(8)));
+typedef __bf16 b2_t __attribute__((ext_vector_type(2)));
+typedef __bf16 b8_t __attribute__((ext_vector_type(8)));
 typedef float f4_t __attribute__((ext_vector_type(4)));
 typedef uint32_t u4_t __attribute__((ext_vector_type(4)));
 
@@ -28,6 +30,34 @@ __device__ __forceinline__ uint16_t float_to_half_bits(float f) {
   return __builtin_bit_cast(uint16_t, (_Float16)f);  // round to nearest even
 }
 
+// Element type of activations, scales and outputs (tpdq_dtype).
+constexpr int kF16 = TPDQ_FP16;
+constexpr int kBF16 = TPDQ_BF16;
+
+template <int DT>
+__device__ __forceinline__ float bits_to_float(uint32_t bits16) {
+  if constexpr (DT == kBF16) return as_f32(bits16 << 16);  // bf16 is the top half of an fp32
+  else return half_bits_to_float(bits16);
+}
+
+template <int DT>
+__device__ __forceinline__ uint16_t float_to_bits(float f) {
+  if constexpr (DT == kBF16) return __builtin_bit_cast(uint16_t, (__bf16)f);  // nearest even
+  else return float_to_half_bits(f);
+}
+
+// {a, b} rounded to the element type, a in the low half-word
+template <int DT>
+__device__ __forceinline__ uint32_t pack2(float a, float b) {
+  if constexpr (DT == kBF16) {
+    const b2_t v = {(__bf16)a, (__bf16)b};
+    return __builtin_bit_cast(uint32_t, v);
+  } else {
+    const h2_t v = {(_Float16)a, (_Float16)b};
+    return as_u32(v);
+  }
+}
+
 // Packed word -> 8 fp16 values (q - z) of one column, exact.
 // OR-ing a nibble into the mantissa of 1024.0 (0x6400) gives 1024 + q; the
 // nibbles at bits 4..7 land as 1024 + 16 q and are rescaled by 1/16 inside
@@ -39,16 +69,23 @@ __device__ __forceinline__ uint16_t float_to_half_bits(float f) {
 // high one), so the values come out as k0 .. k7 and A is used as loaded.
 // The masks live in VGPRs (v_and_or_b32 takes no two literals and reads one
 // SGPR at most on this ISA), so each pair costs one v_and_or_b32.
+// For bf16 the magic number is 128.0 (0x4300): 128 + q is exact (bf16 holds
+// the integers 128 .. 255), and the zero is not subtracted per element (see
+// unpack_bias_bf16).
+template <int DT = kF16>
 struct UnpackConsts {
   uint32_t lo, hi, magic;
   __device__ __forceinline__ UnpackConsts() {
     asm volatile("v_mov_b32 %0, 0x000f000f" : "=v"(lo));
     asm volatile("v_mov_b32 %0, 0x00f000f0" : "=v"(hi));
-    asm volatile("v_mov_b32 %0, 0x64006400" : "=v"(magic));
+    if constexpr (DT == kBF16)
+      asm volatile("v_mov_b32 %0, 0x43004300" : "=v"(magic));
+    else
+      asm volatile("v_mov_b32 %0, 0x64006400" : "=v"(magic));
   }
 };
 
-__device__ __forceinline__ h8_t unpack_sub(const UnpackConsts& k, uint32_t w, uint32_t z1024,
+__device__ __forceinline__ h8_t unpack_sub(const UnpackConsts<kF16>& k, uint32_t w, uint32_t z1024,
                                            uint32_t z64) {
   const uint32_t lo = k.lo, hi = k.hi, magic = k.magic;
   const uint32_t w8 = w >> 8;
@@ -61,13 +98,40 @@ __device__ __forceinline__ h8_t unpack_sub(const UnpackConsts& k, uint32_t w, ui
   return as_h8(r);
 }
 
+// Packed word -> 8 bf16 values 128 + q of one column, exact, in the order of
+// unpack_sub (nibble positions (0, 4), (1, 5), (2, 6), (3, 7)). bf16 has no
+// packed arithmetic here to subtract the zero per element, so the zero is
+// applied once per group instead: sum_k x (q - z) = sum_k x (128 + q) -
+// (128 + z) sum_k x, with sum_k x taken by the same MFMA against ones.
+__device__ __forceinline__ u4_t unpack_bias_bf16(const UnpackConsts<kBF16>& k, uint32_t w) {
+  const uint32_t lo = k.lo, magic = k.magic;
+  u4_t r;
+  r.x = (w & lo) | magic;
+  r.y = ((w >> 4) & lo) | magic;
+  r.z = ((w >> 8) & lo) | magic;
+  r.w = ((w >> 12) & lo) | magic;
+  return r;
+}
+
+// bf16 ones: the B operand whose product with A sums A's 32 columns
+constexpr uint32_t kBf16OnePair = 0x3F803F80u;
+
+// The B operand of one 32-row step: fp16 q - z (the zero subtracted per
+// element), or bf16 128 + q (the zero applied per group).
+template <int DT>
+__device__ __forceinline__ u4_t unpack_step(const UnpackConsts<DT>& k, uint32_t w, uint32_t z1024,
+                                            uint32_t z64) {
+  if constexpr (DT == kBF16) return unpack_bias_bf16(k, w);
+  else return __builtin_bit_cast(u4_t, unpack_sub(k, w, z1024, z64));
+}
+
 
 // Per-row dequant of one word: row r (0..7) has zero z[r] and scale bits
 // s[r]; returns fp16(s * (q - z)) in the unpack order of the word's layout
 // (NAT: a tiled word, rows k0 .. k7; else k0, k4, k1, k5, k2, k6, k3, k7).
 template <bool NAT>
-__device__ __forceinline__ h8_t dequant_rows(const UnpackConsts& k, uint32_t w,
-                                             const uint32_t (&z)[8], const uint32_t (&s)[8]) {
+__device__ __forceinline__ h8_t dequant_rows_f16(const UnpackConsts<kF16>& k, uint32_t w,
+                                                 const uint32_t (&z)[8], const uint32_t (&s)[8]) {
   const uint32_t lo = k.lo, hi = k.hi, magic = k.magic;
   const uint32_t w8 = w >> 8;
   const h2_t inv16 = {(_Float16)0.0625f, (_Float16)0.0625f};
@@ -84,6 +148,27 @@ __device__ __forceinline__ h8_t dequant_rows(const UnpackConsts& k, uint32_t w,
   r.z = as_u32((as_h2((w8 & lo) | magic) - as_h2(z26)) * as_h2(s[r2] | (s[r6] << 16)));
   r.w = as_u32((as_h2((w8 & hi) | magic) * inv16 - as_h2(z37)) * as_h2(s[r3] | (s[r7] << 16)));
   return as_h8(r);
+}
+
+// The same for bf16: s * (q - z) formed in fp32 (exact: an 8-bit scale times
+// a small integer) and rounded once to bf16.
+template <bool NAT, int DT>
+__device__ __forceinline__ u4_t dequant_rows(const UnpackConsts<DT>& k, uint32_t w,
+                                             const uint32_t (&z)[8], const uint32_t (&s)[8]) {
+  if constexpr (DT == kF16) {
+    return __builtin_bit_cast(u4_t, dequant_rows_f16<NAT>(k, w, z, s));
+  } else {
+    // nibble position p holds row p (GPTQ) or row 2p, 2 (p - 4) + 1 (tiled)
+    auto val = [&](int p) {
+      const int r = NAT ? (p < 4 ? 2 * p : 2 * (p - 4) + 1) : p;
+      const int q = (int)((w >> (4 * p)) & 0xFu);
+      return (float)(q - (int)z[r]) * bits_to_float<kBF16>(s[r]);
+    };
+    u4_t out;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) out[i] = pack2<kBF16>(val(i), val(i + 4));
+    return out;
+  }
 }
 
 // 8 consecutive fp16 activations x0..x7 -> x0, x4, x1, x5, x2, x6, x3, x7.
@@ -115,6 +200,16 @@ __device__ __forceinline__ void wait_vmcnt() {
 
 __device__ __forceinline__ f4_t mfma16x16x32(h8_t a, h8_t b, f4_t c) {
   return __builtin_amdgcn_mfma_f32_16x16x32_f16(a, b, c, 0, 0, 0);
+}
+
+// v_mfma_f32_16x16x32_{f16,bf16} on raw operand bits
+template <int DT>
+__device__ __forceinline__ f4_t mfma_k32(u4_t a, u4_t b, f4_t c) {
+  if constexpr (DT == kBF16)
+    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(b8_t, a),
+                                                   __builtin_bit_cast(b8_t, b), c, 0, 0, 0);
+  else
+    return __builtin_amdgcn_mfma_f32_16x16x32_f16(as_h8(a), as_h8(b), c, 0, 0, 0);
 }
 
 // Workgroups are dispatched round-robin over the 8 XCDs. Neighbouring

@@ -60,6 +60,7 @@ struct GemmArgs {
   int K, N, G, num_groups;
   int ks;        // M-tiled kernel: K splits (<= 1: none)
   float* part;   // M-tiled kernel: fp32 partials [ks][M][N] when ks > 1
+  int dt;        // tpdq_dtype of X, scales and Y (the kernels take it as a template argument)
   uint16_t* Y;            // [M][ldy]
   int64_t ldy;
   int meta_rows;          // metadata rows staged in LDS
@@ -69,6 +70,7 @@ struct GemmArgs {
 
 // Host-side plan of one decode launch.
 struct DecodePlan {
+  int dt;       // tpdq_dtype
   int layout;   // tpdq_layout of qweight
   int meta;     // MetaMode
   int amode;    // AMode
@@ -95,7 +97,11 @@ constexpr int kWideTargetWgs = 200;
 // covers the request (for kOperandGather: the gather does not fit in LDS, the
 // caller then runs launch_gather_prep and plans with kOperandPrepared).
 bool plan_decode(int M, int K, int N, int G, int num_groups, int layout, int meta_pref, int operand,
-                 DecodePlan* p);
+                 int dt, DecodePlan* p);
+// the kernel of a plan, per element type (gemm_decode.hip, gemm_decode_bf16.hip)
+typedef void (*DecodeKernel)(GemmArgs);
+DecodeKernel decode_kernel_f16(const DecodePlan& p);
+DecodeKernel decode_kernel_bf16(const DecodePlan& p);
 // part: the workspace for k_wide's split-K partials (ks x M x N floats)
 hipError_t launch_decode(const GemmArgs& a, const DecodePlan& p, float* part, hipStream_t s);
 // Xp [M][K] = X[:, perm] (perm may be NULL), each octet in operand order.
@@ -123,7 +129,7 @@ size_t mtile_part_bytes(const MtilePlan& p, int M, int N);
 // part: the partials (ignored when p.ks == 1)
 hipError_t launch_mtile(const GemmArgs& a, const MtilePlan& p, float* part, hipStream_t s);
 hipError_t launch_splitk_reduce(const float* part, int ks, int M, int N, uint16_t* Y, int64_t ldy,
-                                hipStream_t s);
+                                int dt, hipStream_t s);
 // Xp [M][K] = X[:, perm] row-major (for the prefill GEMM's activations)
 hipError_t launch_gather_rows(const uint16_t* X, int64_t ldx, int M, int K, const int32_t* perm,
                               uint16_t* Xp, hipStream_t s);

@@ -80,7 +80,7 @@ def test_gemm_validation(lib):
     assert gemm(lib, w, perm=1 << 27, ws=None) == _abi.ERR_WORKSPACE        # a gather needs workspace
     nog = fake_layer(gidx=False)
     assert gemm(lib, nog, path=_abi.PATH_ACTORDER) == _abi.ERR_NULL          # act-order needs g_idx
-    assert gemm(lib, w, dtype=_abi.BF16) == _abi.ERR_UNSUPPORTED
+    assert gemm(lib, w, dtype=2) == _abi.ERR_SHAPE                         # unknown dtype
     assert gemm(lib, w, path=7) == _abi.ERR_SHAPE
     assert gemm(lib, nog, path=_abi.PATH_ACTORDER_GLOBAL) == _abi.ERR_NULL
     need = lib.tpdq_workspace_bytes(_abi.OP_GEMM, 4, ctypes.byref(w), None)
