@@ -59,7 +59,7 @@ def gemm_bytes(M, K, N, G, ng=None, gidx=False, xperm=False):
 
 def kernel_source_hash():
     h = hashlib.sha256()
-    for f in ("gemm_decode.hip", "kernels_common.h", "tpdq_internal.h"):
+    for f in ("decode_kernels.h", "gemm_decode.hip", "kernels_common.h", "tpdq_internal.h"):
         with open(os.path.join(ROOT, "paper_2402_04925_amd", "csrc", f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()[:16]
@@ -87,22 +87,27 @@ def read_traffic(workload, M):
 
 
 class Setup:
-    """Device-resident shards (rank 0) of one workload, replicated for rotation."""
+    """Device-resident shards (rank 0) of one workload, replicated for rotation.
+    bf16: bfloat16 scales (and activations, in Calls)."""
 
-    def __init__(self, wl, dev, min_bytes=ROTATE_MIN_BYTES):
+    def __init__(self, wl, dev, min_bytes=ROTATE_MIN_BYTES, bf16=False):
         import torch
         import paper_2402_04925_amd as tpdq
         from paper_2402_04925_amd import inputs
 
         self.wl = wl
+        self.bf16 = bf16
         t0 = time.time()
-        L1, L2 = inputs.make_workload(wl)
+        L1, L2 = inputs.make_workload(wl, scale_dtype=inputs.BF16 if bf16 else np.float16)
         self.L1, self.L2 = L1, L2
-        eprint(f"[bench] generated {wl.name} layers in {time.time() - t0:.1f}s")
+        eprint(f"[bench] generated {wl.name} layers{' (bf16 scales)' if bf16 else ''} in {time.time() - t0:.1f}s")
 
         def dev_layer(L):
+            sc = torch.from_numpy(L.scales)
+            if bf16:
+                sc = sc.to(torch.bfloat16)
             return tpdq.QuantWeight.from_tensors(
-                torch.from_numpy(L.qweight).to(dev), torch.from_numpy(L.scales).to(dev),
+                torch.from_numpy(L.qweight).to(dev), sc.to(dev),
                 torch.from_numpy(L.qzeros).to(dev), torch.from_numpy(L.g_idx.astype(np.int32)).to(dev),
                 L.G)
 
@@ -209,9 +214,13 @@ class Calls:
         self.st, self.M, self.dev = st, M, dev
         self.tpdq = tpdq
         self.lib = tpdq._abi.lib()
-        self.X = torch.from_numpy(inputs.make_x(wl, M)).to(dev)
-        self.y1 = torch.empty(M, wl.N1 // wl.tp, dtype=torch.float16, device=dev)
-        self.y2 = torch.empty(M, wl.N2, dtype=torch.float16, device=dev)
+        if st.bf16:
+            self.X = torch.from_numpy(inputs.make_x(wl, M, dtype=inputs.BF16)).to(torch.bfloat16).to(dev)
+        else:
+            self.X = torch.from_numpy(inputs.make_x(wl, M)).to(dev)
+        self.dt = tpdq.BF16 if st.bf16 else tpdq.FP16
+        self.y1 = torch.empty(M, wl.N1 // wl.tp, dtype=self.X.dtype, device=dev)
+        self.y2 = torch.empty(M, wl.N2, dtype=self.X.dtype, device=dev)
         self.xg = self.X[:, st.P1.long()].contiguous()   # X[:, P1] for the single-GEMM timings
         self.ws = tpdq.Workspace(dev)
         self.paths = {"ordered": tpdq.PATH_ORDERED, "actorder": tpdq.PATH_ACTORDER,
@@ -236,7 +245,7 @@ class Calls:
         def call():
             tpdq._abi.check(lib.tpdq_mlp_shard(
                 X.data_ptr(), X.stride(0), M, P1, ctypes.byref(c1), ctypes.byref(c2), path,
-                tpdq.FP16, y1.data_ptr(), y2.data_ptr(), buf.data_ptr(), buf.numel(), self._stream()))
+                self.dt, y1.data_ptr(), y2.data_ptr(), buf.data_ptr(), buf.numel(), self._stream()))
         return call
 
     def gemm(self, rep, which, pname):
@@ -251,7 +260,7 @@ class Calls:
 
         def call():
             tpdq._abi.check(lib.tpdq_w4a16_gemm(
-                xin.data_ptr(), xin.stride(0), M, None, ctypes.byref(c), path, tpdq.FP16,
+                xin.data_ptr(), xin.stride(0), M, None, ctypes.byref(c), path, self.dt,
                 out.data_ptr(), out.stride(0), buf.data_ptr(), buf.numel(), self._stream()))
         return call
 
@@ -371,6 +380,36 @@ def config_lines(dev, steps, warmup):
     return out
 
 
+def bf16_line(dev, steps, warmup):
+    """The headline workload (Llama-70B TP = 8 rank-0 shard) with bfloat16
+    activations, scales and outputs: ordered and act-order MLPs and the
+    ordered GEMMs' achieved GB/s at each M, timed like the fp16 line."""
+    import torch
+    from paper_2402_04925_amd import inputs
+    wl = inputs.WORKLOADS["llama70b_tp8"]
+    st = Setup(wl, dev, bf16=True)
+    N1, K2 = wl.N1 // wl.tp, wl.K2 // wl.tp
+    res = {}
+    for M in wl.Ms:
+        c = Calls(st, M, dev)
+        mo, _ = capture_and_time([c.mlp(rep, "ordered") for rep in st.reps], steps, warmup, dev)
+        ma, _ = capture_and_time([c.mlp(rep, "actorder") for rep in st.reps], steps, warmup, dev)
+        g1, _ = capture_and_time([c.gemm(rep, 0, "ordered") for rep in st.reps], steps, warmup, dev)
+        g2, _ = capture_and_time([c.gemm(rep, 1, "ordered") for rep in st.reps], steps, warmup, dev)
+        gbs = (gemm_bytes(M, wl.K1, N1, wl.G) + gemm_bytes(M, K2, wl.N2, wl.G)) / ((g1 + g2) * 1e-3) / 1e9
+        res[str(M)] = dict(ordered_mlp_us=round(mo * 1e3, 3), actorder_mlp_us=round(ma * 1e3, 3),
+                           speedup_ordered_vs_actorder=round(ma / mo, 3),
+                           ordered_gemm_us=[round(g1 * 1e3, 3), round(g2 * 1e3, 3)],
+                           ordered_gemm_gbs=round(gbs, 1), ordered_gemm_hbm_frac=round(gbs / HBM_PEAK_GBS, 4))
+        eprint(f"[bench] bf16 {wl.name} M={M}: ordered mlp {mo*1e3:.2f} us (gemms {g1*1e3:.2f} + {g2*1e3:.2f} us, "
+               f"{gbs:.0f} GB/s), actorder mlp {ma*1e3:.2f} us")
+        del c
+    del st
+    torch.cuda.synchronize()
+    return dict(workload=f"{wl.name}: rank-0 TP-aware MLP shard, W1 {wl.K1}x{N1}, W2 {K2}x{wl.N2}, int4 G={wl.G}, "
+                         f"bf16 X, scales and outputs", by_M=res)
+
+
 def prefill_line(dev, steps=10):
     """The Llama-70B TP = 2 prefill shard (M = 2048): the ordered MLP shard
     and its two GEMMs (graph replay), TFLOP/s against the dense fp16 MFMA
@@ -420,6 +459,8 @@ def main():
                     help="skip the Granite-20B TP=4 and Llama-70B TP=1 decode lines")
     ap.add_argument("--no-prefill", action="store_true",
                     help="skip the Llama-70B TP=2 prefill shard (M=2048, MFMA-bound) line")
+    ap.add_argument("--no-bf16", action="store_true",
+                    help="skip the bf16 line (the headline shard with bf16 activations and scales)")
     ap.add_argument("--profile-run", action="store_true",
                     help="eager launches for rocprofv3 (kernel trace or counters); no JSON")
     args = ap.parse_args()
@@ -475,6 +516,7 @@ def main():
     eprint(f"[bench] 1 GiB device copy: {copy_gbs:.0f} GB/s (read + write)")
     configs = None if args.no_configs else config_lines(dev, args.steps, args.warmup)
     prefill = None if args.no_prefill else prefill_line(dev)
+    bf16 = None if args.no_bf16 else bf16_line(dev, args.steps, args.warmup)
 
     M = args.M
     r = results[M]
@@ -527,7 +569,7 @@ def main():
         hbm_frac=round(b["mlp"] / (mlp_us * 1e-6) / 1e9 / HBM_PEAK_GBS, 4),
         tflops=round(r["flops"] / (mlp_us * 1e-6) / 1e12, 3),
         speedup_vs_actorder=round(r["actorder"]["mlp_us"] / mlp_us, 3),
-        roofline=roof, cpu_baseline=cpu, configs=configs, prefill=prefill,
+        roofline=roof, cpu_baseline=cpu, configs=configs, prefill=prefill, bf16=bf16,
         copy_1gib_gbs=round(copy_gbs, 1),
         roofline_frac_of_copy=round(achieved / copy_gbs, 4),
         sweep=sweep,

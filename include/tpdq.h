@@ -29,7 +29,7 @@
  * GPTQ layout: group quantization of a K x N weight, section 1.1):
  *   qweight int32 [K/8][ld_q]   nibble j (bits 4j..4j+3) of word [r][n] is
  *                               the unsigned 4-bit code q of row 8r+j, col n
- *   scales  fp16  [num_groups][ld_s]     one scale s per (group, column)
+ *   scales  fp16 or bf16 [num_groups][ld_s]  one scale s per (group, column)
  *   qzeros  int32 [num_groups][ld_z]     nibble j of word [g][c] is the
  *                               4-bit zero code z of group g, column 8c+j
  *   g_idx   int32 [K]           group of row k
@@ -58,6 +58,15 @@ typedef enum {
   TPDQ_ERR_HIP = 7          /* a HIP runtime call or a kernel launch failed             */
 } tpdq_status;
 
+/* Element type of X, the scales and the outputs (one type per call; the
+ * paper's experiments use fp16, bf16 is the second type of the same
+ * method). Both accumulate in fp32 and round the output to nearest even.
+ * fp16: the ordered kernels subtract the zero exactly per element; the
+ * act-order and prefill-sized kernels round each dequantized weight to fp16.
+ * bf16: the ordered decode kernels keep q - z exact (the zero is applied per
+ * group against the group's sum of X, so a product that is exactly 0 comes
+ * out at fp32 rounding level, not 0); the act-order and prefill-sized
+ * kernels round each dequantized weight to bf16. */
 typedef enum { TPDQ_FP16 = 0, TPDQ_BF16 = 1 } tpdq_dtype;
 
 /* Storage order of qweight.
