@@ -127,12 +127,22 @@ int meta_mode(tpdq_path path) {
   return kMetaRowLds;
 }
 
+// Extra inputs and outputs of one GEMM inside the MLP (decode kernels, one
+// launch of M <= 64 rows): yp receives a second copy of Y in the prepared
+// operand layout of the next GEMM; x_prepared says X already is one.
+struct GemmIO {
+  uint16_t* yp = nullptr;
+  int yp_natural = 0;
+  bool x_prepared = false;
+};
+
 // One GEMM through the decode kernels, M cut into launches of <= 64 rows.
 // perm != NULL: the operand is X[:, perm]; it is gathered inside the kernel
 // when it fits in LDS, else into the workspace first (already in operand
 // order).
 tpdq_status run_gemm(const uint16_t* X, int64_t ldx, int M, const int32_t* perm, const tpdq_w4* w,
-                     tpdq_path path, int dt, uint16_t* Y, int64_t ldy, char* ws, hipStream_t st) {
+                     tpdq_path path, int dt, uint16_t* Y, int64_t ldy, char* ws, hipStream_t st,
+                     const GemmIO& io = GemmIO()) {
   const int meta = meta_mode(path);
   const int32_t* gidx = path == TPDQ_PATH_ORDERED ? nullptr : w->g_idx;
   MtilePlan mp;
@@ -175,7 +185,10 @@ tpdq_status run_gemm(const uint16_t* X, int64_t ldx, int M, const int32_t* perm,
     int64_t ldc = ldx;
     DecodePlan plan;
     bool prepared = false;
-    const bool ok = decode_plan_for(mc, perm != nullptr, w, meta, dt, &plan, &prepared);
+    const bool ok = io.x_prepared
+                        ? plan_decode(mc, w->K, w->N, w->group_size, w->num_groups, w->layout, meta,
+                                      kOperandPrepared, dt, &plan)
+                        : decode_plan_for(mc, perm != nullptr, w, meta, dt, &plan, &prepared);
     int operand = perm ? (prepared ? kOperandPrepared : kOperandGather) : kOperandPlain;
     if (ok && prepared) {
       uint16_t* Xp = (uint16_t*)ws;
@@ -206,6 +219,8 @@ tpdq_status run_gemm(const uint16_t* X, int64_t ldx, int M, const int32_t* perm,
     a.dt = dt;
     a.Y = Y + (int64_t)m0 * ldy;
     a.ldy = ldy;
+    a.Yp = io.yp;
+    a.yp_natural = io.yp_natural;
     float* part = (float*)(ws + decode_gather_bytes(M, w->K));
     hipError_t e = launch_decode(a, plan, part, st);
     if (e != hipSuccess) return hip_fail(e, "decode GEMM launch");
@@ -214,6 +229,28 @@ tpdq_status run_gemm(const uint16_t* X, int64_t ldx, int M, const int32_t* perm,
 }
 
 bool is_actorder(tpdq_path p) { return p == TPDQ_PATH_ACTORDER || p == TPDQ_PATH_ACTORDER_GLOBAL; }
+
+// The MLP's GEMM2 reads Y1 from global memory when Y1 does not fit in LDS;
+// row-major, every load of 16 rows touches 16 rows a row apart (address
+// translation and L1 tag stalls), so GEMM1 then also writes Y1 in GEMM2's
+// operand order (one contiguous KiB per load) into the workspace. Both
+// GEMMs must be single decode launches of the tile kernels (not k_wide, not
+// the M-tiled kernel), and N1 a multiple of 128 (no padding to fill).
+bool mlp_prepared_y1(int M, int64_t ldx, bool perm, const tpdq_w4* w1, const tpdq_w4* w2, int meta,
+                     int dt) {
+  if (M > kDecodeMaxM || w1->N % 128 != 0) return false;
+  MtilePlan mp;
+  if (plan_mtile(M, perm ? (int64_t)w1->K : ldx, w1, meta, &mp) || plan_mtile(M, w1->N, w2, meta, &mp))
+    return false;
+  DecodePlan p1, p2;
+  bool prepared = false;
+  if (!decode_plan_for(M, perm, w1, meta, dt, &p1, &prepared) || p1.wide) return false;
+  if (!decode_plan_for(M, false, w2, meta, dt, &p2, &prepared) || p2.wide || p2.amode != kAGlobal)
+    return false;
+  DecodePlan p3;
+  return plan_decode(M, w2->K, w2->N, w2->group_size, w2->num_groups, w2->layout, meta,
+                     kOperandPrepared, dt, &p3) && !p3.wide;
+}
 
 tpdq_status check_common(int32_t M, tpdq_path path, tpdq_dtype dtype) {
   if (M < 1) return fail(TPDQ_ERR_SHAPE, "M=%d must be >= 1", M);
@@ -265,7 +302,9 @@ size_t tpdq_workspace_bytes(int op, int32_t M, const tpdq_w4* a, const tpdq_w4* 
   if (op == 1) return gemm_max(a, true);
   if (op == 2) {
     if (!b) return 0;
-    return std::max(gemm_max(a, true), gemm_max(b, false));
+    // GEMM1's region, then Y1 in GEMM2's operand order (mlp_prepared_y1)
+    const size_t y1p = M <= kDecodeMaxM ? decode_gather_bytes(M, a->N) : 0;
+    return std::max(gemm_max(a, true) + y1p, gemm_max(b, false));
   }
   return 0;
 }
@@ -431,9 +470,19 @@ tpdq_status tpdq_mlp_shard(const void* X, int64_t ldx, int32_t M, const int32_t*
 
   hipStream_t s = (hipStream_t)stream;
   char* ws = (char*)workspace;
+  GemmIO io1, io2;
+  if (workspace && ws_bytes >= bound && mlp_prepared_y1(M, ldx, !act, w1, w2, meta, dtype)) {
+    const size_t off = gemm_ws_need(M, ldx, !act, w1, meta, dtype);
+    io1.yp = (uint16_t*)(ws + off);
+    io1.yp_natural = w2->layout == TPDQ_LAYOUT_TILED ? 1 : 0;
+    io2.x_prepared = true;
+  }
   st = run_gemm((const uint16_t*)X, ldx, M, act ? nullptr : P1, w1, path, dtype, (uint16_t*)Y1, w1->N,
-                ws, s);
+                ws, s, io1);
   if (st != TPDQ_OK) return st;
+  if (io2.x_prepared)
+    return run_gemm(io1.yp, w1->N, M, nullptr, w2, path, dtype, (uint16_t*)Y2_partial, w2->N, ws, s,
+                    io2);
   return run_gemm((const uint16_t*)Y1, w1->N, M, nullptr, w2, path, dtype, (uint16_t*)Y2_partial,
                   w2->N, ws, s);
 }

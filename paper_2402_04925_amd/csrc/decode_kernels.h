@@ -230,8 +230,20 @@ struct XStage {
   }
 };
 
+// Offset (in elements) of Y[row][c] in the prepared-operand layout of a
+// following GEMM whose K is this GEMM's N (the records of k_gather_prep:
+// [row tile][step][lane] x 8 values, rows 8 (4 step + lane / 16) .. +7 of
+// the operand for row 16 tile + lane % 16, in natural order for tiled
+// weights, else x0, x4, x1, x5, ...).
+__device__ __forceinline__ int64_t prepared_offset(int row, int c, int nsteps, int natural) {
+  const int r = c >> 3, e = c & 7;
+  const int64_t rec = ((int64_t)(row >> 4) * nsteps + (r >> 2)) * 64 + 16 * (r & 3) + (row & 15);
+  return rec * 8 + (natural ? e : (e & 3) * 2 + (e >> 2));
+}
+
 // Sum the NW waves' partial tiles (TN tiles of 16 columns from n0) in LDS
-// and write Y in the element type. acc[t][n] of lane l holds rows t*16 + 4*(l/16) + e, column
+// and write Y in the element type; with a.Yp, Y is also written in the next
+// GEMM's prepared-operand layout (a.N a multiple of 128: no padding). acc[t][n] of lane l holds rows t*16 + 4*(l/16) + e, column
 // n0 + 16 n + l % 16.
 template <int MT, int NW, int TN, int DT>
 __device__ __forceinline__ void reduce_store(const GemmArgs& a, f4_t (&acc)[MT][TN], int n0,
@@ -258,7 +270,11 @@ __device__ __forceinline__ void reduce_store(const GemmArgs& a, f4_t (&acc)[MT][
     for (int w = 0; w < NW; ++w) s += red[((w * MT * TN + tn) * 4 + e) * 64 + ln];
     const int row = (tn / TN) * kTileM + 4 * (ln >> 4) + e;
     const int c = n0 + (tn % TN) * kTileN + (ln & 15);
-    if (row < a.M && c < a.N) a.Y[(int64_t)row * a.ldy + c] = float_to_bits<DT>(s);
+    if (row < a.M && c < a.N) {
+      const uint16_t v = float_to_bits<DT>(s);
+      a.Y[(int64_t)row * a.ldy + c] = v;
+      if (a.Yp) a.Yp[prepared_offset(row, c, a.N >> 5, a.yp_natural)] = v;
+    }
   }
 }
 

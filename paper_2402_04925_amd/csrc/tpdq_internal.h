@@ -63,6 +63,11 @@ struct GemmArgs {
   int dt;        // tpdq_dtype of X, scales and Y (the kernels take it as a template argument)
   uint16_t* Y;            // [M][ldy]
   int64_t ldy;
+  // optional second copy of Y in the prepared-operand layout of a GEMM whose K
+  // is this N (k_ordered and k_rowmeta; N % 128 == 0), natural order when
+  // that GEMM's weights are tiled
+  uint16_t* Yp;
+  int yp_natural;
   int meta_rows;          // metadata rows staged in LDS
   int lds_x_off;          // byte offset of the staged X in LDS
   int lds_xr_off;         // kALdsGather: byte offset of the LDS copy of X's rows
