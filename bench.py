@@ -113,9 +113,12 @@ class Setup:
 
         d1, d2 = dev_layer(L1), dev_layer(L2)
         P1, _, P2, _, w1o, w2o = tpdq.reorder(d1, d2)
+        # Alg. 2's local data flow at TP = 1 needs W1[P1] with its columns in place
+        w1u = tpdq.reorder(d1)[4] if wl.tp == 1 else None
         torch.cuda.synchronize()
         tp = wl.tp
         self.P1 = P1
+        self.P2 = P2
         # rank-0 shards, materialised densely (what a deployment would ship)
         ord1 = w1o.column_shard(0, tp)
         ord2 = w2o.row_shard(0, tp, sorted_rows=True)
@@ -129,6 +132,8 @@ class Setup:
 
         a1, a2 = dense(act1, True), dense(act2, True)
         base = [dense(ord1, False), dense(ord2, False), a1, a2, tpdq.pack_tiled(a1), tpdq.pack_tiled(a2)]
+        if w1u is not None:
+            base.append(dense(w1u, False))   # index 6: W1[P1] (Alg. 2 at TP = 1)
         per = sum(t.qweight.numel() * 4 + t.scales.numel() * 2 + t.qzeros.numel() * 4 for t in base[:2])
         self.R = max(2, -(-min_bytes // per))
         self.reps = [base]
@@ -137,7 +142,7 @@ class Setup:
                                                q.g_idx.clone() if q.g_idx is not None else None,
                                                q.K, q.N, q.G, q.num_groups, q.layout) for q in base])
         torch.cuda.synchronize()
-        del d1, d2, w1o, w2o
+        del d1, d2, w1o, w2o, w1u
         eprint(f"[bench] {self.R} weight replicas of {per / 1e6:.1f} MB (ordered pair)")
 
 
@@ -248,6 +253,27 @@ class Calls:
                 self.dt, y1.data_ptr(), y2.data_ptr(), buf.data_ptr(), buf.numel(), self._stream()))
         return call
 
+    def alg2_mlp(self, rep):
+        """Alg. 2's local data flow at TP = 1: Y1 = X[:, P1] @ W1[P1] (columns in
+        place), then Y2 = Y1[:, P2] @ W2[P2], the gather inside GEMM2 (x_perm)."""
+        import ctypes
+        tpdq, lib, M = self.tpdq, self.lib, self.M
+        c1, c2 = rep[6].c_struct(), rep[1].c_struct()
+        nb = max(lib.tpdq_workspace_bytes(tpdq.OP_GEMM, M, ctypes.byref(c1), None),
+                 lib.tpdq_workspace_bytes(tpdq.OP_GEMM, M, ctypes.byref(c2), None))
+        buf = self.ws.get(nb)
+        X, y1, y2 = self.X, self.y1, self.y2
+        P1, P2 = self.st.P1.data_ptr(), self.st.P2.data_ptr()
+
+        def call():
+            tpdq._abi.check(lib.tpdq_w4a16_gemm(
+                X.data_ptr(), X.stride(0), M, P1, ctypes.byref(c1), tpdq.PATH_ORDERED, self.dt,
+                y1.data_ptr(), y1.stride(0), buf.data_ptr(), buf.numel(), self._stream()))
+            tpdq._abi.check(lib.tpdq_w4a16_gemm(
+                y1.data_ptr(), y1.stride(0), M, P2, ctypes.byref(c2), tpdq.PATH_ORDERED, self.dt,
+                y2.data_ptr(), y2.stride(0), buf.data_ptr(), buf.numel(), self._stream()))
+        return call
+
     def gemm(self, rep, which, pname):
         import ctypes
         tpdq, lib, M = self.tpdq, self.lib, self.M
@@ -356,6 +382,12 @@ def config_lines(dev, steps, warmup):
                      ordered_gemm_us=[round(g1 * 1e3, 3), round(g2 * 1e3, 3)],
                      ordered_gemm_gbs=round(gbs, 1), ordered_gemm_hbm_frac=round(gbs / HBM_PEAK_GBS, 4),
                      ordered_mlp_tflops=round(flops / (mo * 1e-3) / 1e12, 2))
+            if wl.tp == 1:
+                m2, _ = capture_and_time([c.alg2_mlp(rep) for rep in st.reps], steps, warmup, dev)
+                r["alg2_local_mlp_us"] = round(m2 * 1e3, 3)
+                r["alg2_local_over_alg3"] = round(m2 / mo, 4)
+                eprint(f"[bench] {name} M={M}: Alg. 2 local data flow {m2*1e3:.2f} us "
+                       f"(Alg. 3 {mo*1e3:.2f} us, ratio {m2 / mo:.3f})")
             if dense is not None:
                 X = c.X
                 y1 = torch.empty(M, N1, dtype=torch.float16, device=dev)
