@@ -405,6 +405,73 @@ def mlp_tp_aware(X, P1, w1f, w2f, G, tp, acc="f64"):
     return all_reduce_sum(partials), partials
 
 
+# ----------------------------------------------------------------------------
+# Gated MLP (the experiments section notes that the method carries over to an
+# MLP with a gate projection): Y1 = silu(X W_gate) * (X W_up), Y2 = Y1 W_down.
+# Readings: gate and up take the same input, hence the same act-order
+# permutation (one g_idx, one P1); P2 (from W_down) is folded into the columns
+# of both; both products stay unrounded until Y1, which is rounded once.
+# ----------------------------------------------------------------------------
+
+
+def silu(x) -> np.ndarray:
+    """x * sigma(x) = x / (1 + exp(-x)) in float64."""
+    x = np.asarray(x, dtype=np.float64)
+    return x / (1.0 + np.exp(-x))
+
+
+def gated_y1(X, gate, up, g_idx, x_perm=None, acc="f64", cols=None, round_fp16=True, dtype="fp16"):
+    """Y1 = silu(X' @ deq(W_gate)) * (X' @ deq(W_up)), X' = X[:, x_perm] when
+    given; gate and up are (qweight, scales, qzeros) of the same shape sharing
+    g_idx. Rounded once to the storage type (round_fp16=False: float64)."""
+    yg = w4a16_gemm(X, *gate, g_idx, x_perm=x_perm, acc=acc, cols=cols, round_fp16=False)
+    yu = w4a16_gemm(X, *up, g_idx, x_perm=x_perm, acc=acc, cols=cols, round_fp16=False)
+    y = silu(yg) * yu
+    return round_to(y, dtype) if round_fp16 else y
+
+
+def _triple(w):
+    return w["qweight"], w["scales"], w["qzeros"]
+
+
+def gated_mlp_reference(X, gate, up, g1, down, g2, acc="f64", y1_fp16=True, dtype="fp16"):
+    """Unsharded act-order gated MLP (dicts of packed arrays; g1 shared by
+    gate and up)."""
+    Y1 = gated_y1(X, _triple(gate), _triple(up), g1, acc=acc, round_fp16=y1_fp16, dtype=dtype)
+    return w4a16_gemm(Y1, *_triple(down), g2, acc=acc, dtype=dtype)
+
+
+def gated_mlp_tp_aware_rank(X, P1, gate_f, up_f, down_f, G, acc="f64", y1_fp16=True, round_y2=True,
+                            dtype="fp16"):
+    """Alg. 3 for the gated MLP on one rank: gate_f and up_f are column shards
+    of W_gate[P1, P2] and W_up[P1, P2], down_f a row shard of W_down[P2]; all
+    hold sorted rows, so their local group of row k is floor(k / G)."""
+    K1 = gate_f["qweight"].shape[0] * 8
+    K2 = down_f["qweight"].shape[0] * 8
+    Y1 = gated_y1(X, _triple(gate_f), _triple(up_f), g_idx_naive(K1, G), x_perm=P1, acc=acc,
+                  round_fp16=y1_fp16, dtype=dtype)
+    Y2 = w4a16_gemm(Y1, *_triple(down_f), g_idx_naive(K2, G), acc=acc, round_fp16=round_y2, dtype=dtype)
+    return Y1, Y2
+
+
+def gated_rank_from_global(X, lg, lu, l2, rank, tp, ordered, P2=None, cols2=None, acc="f64",
+                           dtype="fp16"):
+    """One rank's (Y1, Y2 partial[:, cols2]) of the gated MLP from the
+    unpermuted global layers lg, lu = (qweight, scales, qzeros, g_idx) with a
+    shared g_idx, and l2; column block `rank` of gate and up (original columns
+    P2[block] when ordered), as in mlp_rank_from_global."""
+    N1 = np.asarray(lg[0]).shape[1]
+    n = N1 // tp
+    blk = np.arange(rank * n, (rank + 1) * n)
+    sel = np.asarray(P2, dtype=np.int64)[blk] if ordered else blk
+    yg = matmul(X, dequant(*lg, cols=sel), acc)
+    yu = matmul(X, dequant(*lu, cols=sel), acc)
+    Y1 = round_to(silu(yg) * yu, dtype)
+    W2 = dequant(*l2, cols=cols2)[sel]
+    Y2 = round_to(matmul(Y1, W2, acc), dtype)
+    return Y1, Y2
+
+
 def fold_sample(qweight, P_row, P_col, rows, cols):
     """Codes of W[P_row, P_col] at rows x cols (P_col None: columns in place),
     read from the source words element by element; for layers too large to

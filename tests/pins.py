@@ -437,10 +437,107 @@ def pin_bf16_gemm(o, seed=22):
     assert np.max(np.abs(Y64)) > 1.0  # a non-trivial product
 
 
+
+# ------------------------------------------------------------- gated MLP ---
+
+def pin_silu(o, seed=23):
+    """silu against scipy's logistic function (a library routine), the
+    identity silu(x) - silu(-x) = x, and hand values: silu(0) = 0,
+    silu(1) = 1 / (1 + e^-1), silu(x) -> x for large x and -> 0 for very
+    negative x."""
+    from scipy.special import expit
+    x = np.random.default_rng(seed).standard_normal(1000) * 8
+    assert np.allclose(o.silu(x), x * expit(x), rtol=1e-14, atol=0)
+    assert np.allclose(o.silu(x) - o.silu(-x), x, rtol=1e-13, atol=1e-13)
+    assert o.silu(np.array([0.0]))[0] == 0.0
+    assert abs(o.silu(np.array([1.0]))[0] - 0.7310585786300049) < 1e-15
+    assert abs(o.silu(np.array([40.0]))[0] - 40.0) < 1e-12
+    assert abs(o.silu(np.array([-40.0]))[0]) < 1e-15
+
+
+def _gated_case(seed):
+    K1, N1, N2, G = 256, 512, 128, 32
+    gate, down = inputs.make_custom(K1, N1, N2, G, seed)
+    up, _ = inputs.make_custom(K1, N1, 0, G, seed + 1000)
+    up.g_idx = gate.g_idx          # one input, one act-order permutation
+    X = inputs.random_activations(6, K1, np.random.default_rng(seed))
+    d = lambda w: dict(qweight=w.qweight, scales=w.scales, qzeros=w.qzeros)
+    return gate, up, down, d(gate), d(up), d(down), X, G
+
+
+def pin_gated_tp_aware_mlp(o, seed=24, tps=(1, 2, 4)):
+    """The gated MLP under the TP-aware fold: P2 folded into the columns of
+    both gate and up (W[P1, P2]) and into the rows of down; the sum over ranks
+    equals the unsharded act-order gated MLP (float64), for each TP degree;
+    with fp16 activations within 2e-3. The elementwise silu(gate) * up
+    commutes with the column permutation, which is why the fold carries over."""
+    gate, up, down, dg, du, dd, X, G = _gated_case(seed)
+    ref64 = o.w4a16_gemm(o.gated_y1(X, o._triple(dg), o._triple(du), gate.g_idx, round_fp16=False),
+                         *o._triple(dd), down.g_idx, round_fp16=False)
+    P1, _ = o.reorder(gate.g_idx)
+    P2, _ = o.reorder(down.g_idx)
+    gf, df = o.fold(dg, dd, P1, P2)
+    uf, _ = o.fold(du, None, P1, P2)
+    for tp in tps:
+        parts, parts16 = [], []
+        for r in range(tp):
+            sg, su = o.column_shard(gf, r, tp), o.column_shard(uf, r, tp)
+            sd = o.row_shard(df, r, tp, G)
+            _, y2 = o.gated_mlp_tp_aware_rank(X, P1, sg, su, sd, G, y1_fp16=False, round_y2=False)
+            parts.append(y2)
+            parts16.append(o.gated_mlp_tp_aware_rank(X, P1, sg, su, sd, G)[1])
+        tot = o.all_reduce_sum(parts, round_fp16=False)
+        assert np.max(np.abs(tot - ref64)) <= 1e-12 * np.max(np.abs(ref64)), tp
+        ref16 = o.gated_mlp_reference(X, dg, du, gate.g_idx, dd, down.g_idx)
+        assert o.rel_err(o.all_reduce_sum(parts16), ref16) <= 2e-3, tp
+
+
+def pin_gated_special_cases(o, seed=25):
+    """q == z in W_up (up = 0) gives Y1 = 0 whatever the gate; q == z in
+    W_gate (gate = 0, silu(0) = 0) gives Y1 = 0 whatever up."""
+    gate, up, down, dg, du, dd, X, G = _gated_case(seed)
+    for which in ("up", "gate"):
+        dz = dict(dg if which == "gate" else du)
+        z = o.unpack_cols(dz["qzeros"])
+        dz["qweight"] = o.pack_rows(z[gate.g_idx])   # every code equals its zero
+        a, b = (dz, du) if which == "gate" else (dg, dz)
+        y1 = o.gated_y1(X, o._triple(a), o._triple(b), gate.g_idx, round_fp16=False)
+        assert np.all(y1 == 0), which
+
+
+
+def pin_gated_bruteforce(o, seed=26):
+    """gated_y1 against scalar loops on a tiny layer pair: every weight read
+    off the hex spelling of its word, both dot products summed term by term,
+    silu from math.exp, so a swap of gate and up, or a dropped zero, shows."""
+    import math
+    K, N, G, M = 16, 8, 8, 2
+    gate, _ = inputs.make_custom(K, N, 0, G, seed)
+    up, _ = inputs.make_custom(K, N, 0, G, seed + 7)
+    up.g_idx = gate.g_idx
+    X = inputs.random_activations(M, K, np.random.default_rng(seed))
+
+    def w(layer, k, n):
+        q = nibble_by_hex(int(layer.qweight.view(np.uint32)[k // 8, n]), k % 8)
+        g = int(gate.g_idx[k])
+        z = nibble_by_hex(int(layer.qzeros.view(np.uint32)[g, n // 8]), n % 8)
+        return float(layer.scales[g, n]) * (q - z)
+
+    d = lambda L: (L.qweight, L.scales, L.qzeros)
+    y = o.gated_y1(X, d(gate), d(up), gate.g_idx, round_fp16=False)
+    for m in range(M):
+        for n in range(N):
+            yg = sum(float(X[m, k]) * w(gate, k, n) for k in range(K))
+            yu = sum(float(X[m, k]) * w(up, k, n) for k in range(K))
+            want = yg / (1.0 + math.exp(-yg)) * yu
+            assert abs(y[m, n] - want) <= 1e-12 * max(1.0, abs(want)), (m, n)
+
+
 ALL_PINS = [
     pin_unpack_bruteforce, pin_pack_roundtrip, pin_golden_gemm_codes, pin_worked_reorder,
     pin_reorder_closed_form, pin_identity_phi, pin_check_groups, pin_golden_gemm,
     pin_gemm_bruteforce, pin_one_hot_rows, pin_special_cases, pin_ordered_equals_actorder,
     pin_tp_aware_mlp, pin_actorder_shard_mlp, pin_alg2_equals_alg3, pin_fold_elementwise,
-    pin_distinct_groups, pin_tiled_layout, pin_bf16_rounding, pin_bf16_gemm,
+    pin_distinct_groups, pin_tiled_layout, pin_bf16_rounding, pin_bf16_gemm, pin_silu,
+    pin_gated_tp_aware_mlp, pin_gated_special_cases, pin_gated_bruteforce,
 ]

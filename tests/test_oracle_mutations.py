@@ -110,6 +110,16 @@ def _round_to_fp16_always(a, dtype="fp16"):
     return np.asarray(a).astype(np.float16)
 
 
+def _silu_is_sigmoid(x):
+    x = np.asarray(x, dtype=np.float64)
+    return 1.0 / (1.0 + np.exp(-x))
+
+
+def _gated_silu_on_up(X, gate, up, g_idx, x_perm=None, acc="f64", cols=None, round_fp16=True,
+                      dtype="fp16"):
+    return _orig["gated_y1"](X, up, gate, g_idx, x_perm, acc, cols, round_fp16, dtype)
+
+
 MUTANTS = {
     "unpack_rows": _unpack_rows_reversed,
     "unpack_cols": _unpack_cols_reversed,
@@ -127,6 +137,8 @@ MUTANTS = {
     "g_idx_actorder:ceil": _eq3_ceil,
     "to_bf16:truncate": _bf16_truncate,
     "round_to:fp16": _round_to_fp16_always,
+    "silu:sigmoid": _silu_is_sigmoid,
+    "gated_y1:swapped": _gated_silu_on_up,
 }
 
 
