@@ -217,9 +217,38 @@ tpdq_status tpdq_mlp_shard(const void* X, int64_t ldx, int32_t M, const int32_t*
                            tpdq_dtype dtype, void* Y1, void* Y2_partial,
                            void* workspace, size_t ws_bytes, void* stream);
 
+/*
+ * tpdq_gated_mlp_shard - one rank's share of an MLP with a gate projection,
+ * up to its AllReduce: Y1 = silu(X' W_gate) * (X' W_up) (silu(x) =
+ * x / (1 + e^-x), both products in fp32, one rounding), Y2_partial = Y1 @
+ * W_down. The experiments section notes that the method carries over to
+ * this MLP: P2 (from W_down) is folded into the columns of both W_gate and
+ * W_up, since the elementwise silu(gate) * up commutes with a column
+ * permutation.
+ *
+ * Gate and up take the same input, so act-order gives them one permutation:
+ * TPDQ_PATH_ORDERED: w_gate and w_up are the rank's column shards of
+ *   W_gate[P1, P2] and W_up[P1, P2] (tpdq_reorder(w_gate, w_down) and
+ *   tpdq_reorder(w_up, w_down) give the same P1 when their g_idx agree),
+ *   w_down its row shard of W_down[P2]; X' = X[:, P1], P1 required.
+ * TPDQ_PATH_ACTORDER / TPDQ_PATH_ACTORDER_GLOBAL: w_gate, w_up and w_down as
+ *   for tpdq_mlp_shard; w_gate->g_idx serves both gate and up (w_up->g_idx
+ *   is not read); P1 must be NULL.
+ * w_up must have w_gate's K, N, group size, num_groups, layout and leading
+ * dimensions (TPDQ_ERR_SHAPE otherwise); w_down->K == w_gate->N.
+ * X, Y1, Y2_partial, alignment and workspace as for tpdq_mlp_shard, with
+ * tpdq_workspace_bytes(3, M, w_gate, w_down). Runs the decode kernels at
+ * every M (batches of more than 64 rows in launches of 64).
+ */
+tpdq_status tpdq_gated_mlp_shard(const void* X, int64_t ldx, int32_t M, const int32_t* P1,
+                                 const tpdq_w4* w_gate, const tpdq_w4* w_up, const tpdq_w4* w_down,
+                                 tpdq_path path, tpdq_dtype dtype, void* Y1, void* Y2_partial,
+                                 void* workspace, size_t ws_bytes, void* stream);
+
 /* Workspace bytes for op 0 (tpdq_reorder: a = w1, b = w2 or NULL),
- * 1 (tpdq_w4a16_gemm: a = w) or 2 (tpdq_mlp_shard: a = w1, b = w2) at batch
- * M. Returns 0 when the arguments are invalid. */
+ * 1 (tpdq_w4a16_gemm: a = w), 2 (tpdq_mlp_shard: a = w1, b = w2) or
+ * 3 (tpdq_gated_mlp_shard: a = w_gate, b = w_down) at batch M. Returns 0
+ * when the arguments are invalid. */
 size_t tpdq_workspace_bytes(int op, int32_t M, const tpdq_w4* a, const tpdq_w4* b);
 
 /* Static description of a status code. */

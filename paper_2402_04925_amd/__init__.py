@@ -12,11 +12,12 @@ import dataclasses
 from typing import Optional
 
 from . import _abi
-from ._abi import (BF16, FP16, LAYOUT_GPTQ, LAYOUT_TILED, OP_GEMM, OP_MLP, OP_REORDER,
+from ._abi import (BF16, FP16, LAYOUT_GPTQ, LAYOUT_TILED, OP_GATED_MLP, OP_GEMM, OP_MLP, OP_REORDER,
                    PATH_ACTORDER, PATH_ACTORDER_GLOBAL, PATH_ORDERED, TpdqError)
 
 __all__ = [
-    "QuantWeight", "reorder", "pack_tiled", "w4a16_gemm", "mlp_shard", "workspace_bytes", "Workspace",
+    "QuantWeight", "reorder", "pack_tiled", "w4a16_gemm", "mlp_shard", "gated_mlp_shard",
+    "workspace_bytes", "Workspace",
     "LAYOUT_GPTQ", "LAYOUT_TILED", "tiled_ld",
     "TpdqError", "PATH_ACTORDER", "PATH_ORDERED", "PATH_ACTORDER_GLOBAL", "FP16", "BF16", "version",
 ]
@@ -261,4 +262,28 @@ def mlp_shard(X, w1: QuantWeight, w2: QuantWeight, path: int, P1=None, y1=None, 
         _ptr(X), X.stride(0), M, _ptr(P1), ctypes.byref(c1), ctypes.byref(c2), path,
         _dtype_code(X.dtype), _ptr(y1), _ptr(y2), _ptr(buf), buf.numel(),
         _stream_handle(X.device)))
+    return y1, y2
+
+
+def gated_mlp_shard(X, w_gate: QuantWeight, w_up: QuantWeight, w_down: QuantWeight, path: int, P1=None,
+                    y1=None, y2=None, workspace: Optional[Workspace] = None):
+    """One rank's gated MLP share up to the AllReduce: Y1 = silu(X' W_gate) *
+    (X' W_up), Y2_partial = Y1 @ W_down (X' = X[:, P1] on the ordered path,
+    where gate and up are column shards of W[P1, P2] and down a row shard of
+    W_down[P2]). Returns (Y1, Y2_partial)."""
+    torch = _torch()
+    if X.dim() != 2 or X.stride(1) != 1:
+        raise ValueError("X must be 2-D with unit column stride")
+    M = X.shape[0]
+    if y1 is None:
+        y1 = torch.empty(M, w_gate.N, dtype=X.dtype, device=X.device)
+    if y2 is None:
+        y2 = torch.empty(M, w_down.N, dtype=X.dtype, device=X.device)
+    cg, cu, cd = w_gate.c_struct(), w_up.c_struct(), w_down.c_struct()
+    lib = _abi.lib()
+    nbytes = lib.tpdq_workspace_bytes(OP_GATED_MLP, M, ctypes.byref(cg), ctypes.byref(cd))
+    buf = _workspace(X.device, nbytes, workspace)
+    _abi.check(lib.tpdq_gated_mlp_shard(
+        _ptr(X), X.stride(0), M, _ptr(P1), ctypes.byref(cg), ctypes.byref(cu), ctypes.byref(cd), path,
+        _dtype_code(X.dtype), _ptr(y1), _ptr(y2), _ptr(buf), buf.numel(), _stream_handle(X.device)))
     return y1, y2

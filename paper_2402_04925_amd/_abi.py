@@ -10,11 +10,12 @@ LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libtpdq.so"
 OK, ERR_NULL, ERR_SHAPE, ERR_ALIGN, ERR_GIDX, ERR_WORKSPACE, ERR_UNSUPPORTED, ERR_HIP = range(8)
 FP16, BF16 = 0, 1
 PATH_ACTORDER, PATH_ORDERED, PATH_ACTORDER_GLOBAL = 0, 1, 2
-OP_REORDER, OP_GEMM, OP_MLP = 0, 1, 2
+OP_REORDER, OP_GEMM, OP_MLP, OP_GATED_MLP = 0, 1, 2, 3
 LAYOUT_GPTQ, LAYOUT_TILED = 0, 1
 
 EXPORTED = (
-    "tpdq_reorder", "tpdq_pack_tiled", "tpdq_w4a16_gemm", "tpdq_mlp_shard", "tpdq_workspace_bytes",
+    "tpdq_reorder", "tpdq_pack_tiled", "tpdq_w4a16_gemm", "tpdq_mlp_shard", "tpdq_gated_mlp_shard",
+    "tpdq_workspace_bytes",
     "tpdq_status_string", "tpdq_last_error", "tpdq_version",
 )
 
@@ -50,6 +51,9 @@ def _declare(lib):
     lib.tpdq_mlp_shard.argtypes = [vp, i64, i32, vp, pw, pw, ctypes.c_int, ctypes.c_int, vp, vp, vp,
                                    sz, vp]
     lib.tpdq_mlp_shard.restype = ctypes.c_int
+    lib.tpdq_gated_mlp_shard.argtypes = [vp, i64, i32, vp, pw, pw, pw, ctypes.c_int, ctypes.c_int, vp,
+                                         vp, vp, sz, vp]
+    lib.tpdq_gated_mlp_shard.restype = ctypes.c_int
     lib.tpdq_workspace_bytes.argtypes = [ctypes.c_int, i32, pw, pw]
     lib.tpdq_workspace_bytes.restype = sz
     lib.tpdq_status_string.argtypes = [ctypes.c_int]

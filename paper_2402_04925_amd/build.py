@@ -15,7 +15,8 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 BUILD = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libtpdq.so")
-SOURCES = ["abi.hip", "gemm_decode.hip", "gemm_decode_bf16.hip", "gemm_prefill.hip", "reorder.hip"]
+SOURCES = ["abi.hip", "gemm_decode.hip", "gemm_decode_bf16.hip", "gemm_gated.hip", "gemm_gated_bf16.hip",
+           "gemm_prefill.hip", "reorder.hip"]
 ARCH = "gfx950"
 
 HIPCC_FLAGS = [

@@ -86,18 +86,18 @@ size_t mtile_gather_bytes(int M, int K, bool perm) { return perm ? align_up((siz
 // a perm, the gather inside the kernel's LDS if it fits, else the prepared
 // operand (*prepared).
 bool decode_plan_for(int mc, bool perm, const tpdq_w4* w, int meta, int dt, DecodePlan* plan,
-                     bool* prepared) {
+                     bool* prepared, bool gated = false) {
   *prepared = false;
   if (perm) {
     if (plan_decode(mc, w->K, w->N, w->group_size, w->num_groups, w->layout, meta, kOperandGather,
-                    dt, plan))
+                    dt, plan, gated))
       return true;
     *prepared = true;
     return plan_decode(mc, w->K, w->N, w->group_size, w->num_groups, w->layout, meta,
-                       kOperandPrepared, dt, plan);
+                       kOperandPrepared, dt, plan, gated);
   }
   return plan_decode(mc, w->K, w->N, w->group_size, w->num_groups, w->layout, meta, kOperandPlain,
-                     dt, plan);
+                     dt, plan, gated);
 }
 
 // split-K partials of the wide decode kernel (0 when K is not split)
@@ -109,14 +109,17 @@ size_t decode_part_bytes(const DecodePlan& p, int mc, int N) {
 // [prepared operand][wide kernel's partials], the partials after the
 // prepared-operand region whenever either is used. The plans, and so the
 // bytes, are the same for both element types.
-size_t gemm_ws_need(int M, int64_t ldx, bool perm, const tpdq_w4* w, int meta, int dt = TPDQ_FP16) {
+// The gated GEMM (gated = true) runs the decode kernels only.
+size_t gemm_ws_need(int M, int64_t ldx, bool perm, const tpdq_w4* w, int meta, int dt = TPDQ_FP16,
+                    bool gated = false) {
   MtilePlan p;
-  if (plan_mtile(M, perm ? (int64_t)w->K : ldx, w, meta, &p))
+  if (!gated && plan_mtile(M, perm ? (int64_t)w->K : ldx, w, meta, &p))
     return mtile_gather_bytes(M, w->K, perm) + mtile_part_bytes(p, M, w->N);
   DecodePlan dp;
   bool prepared = false;
   const int mc = std::min(M, kDecodeMaxM);  // the largest launch
-  if (!decode_plan_for(mc, perm, w, meta, dt, &dp, &prepared)) return perm ? decode_gather_bytes(M, w->K) : 0;
+  if (!decode_plan_for(mc, perm, w, meta, dt, &dp, &prepared, gated))
+    return perm ? decode_gather_bytes(M, w->K) : 0;
   const size_t part = decode_part_bytes(dp, mc, w->N);
   return (prepared || part ? decode_gather_bytes(M, w->K) : 0) + part;
 }
@@ -134,6 +137,7 @@ struct GemmIO {
   uint16_t* yp = nullptr;
   int yp_natural = 0;
   bool x_prepared = false;
+  const tpdq_w4* up = nullptr;  // gated GEMM: Y = silu(X' W) * (X' W_up), decode kernels only
 };
 
 // One GEMM through the decode kernels, M cut into launches of <= 64 rows.
@@ -146,7 +150,8 @@ tpdq_status run_gemm(const uint16_t* X, int64_t ldx, int M, const int32_t* perm,
   const int meta = meta_mode(path);
   const int32_t* gidx = path == TPDQ_PATH_ORDERED ? nullptr : w->g_idx;
   MtilePlan mp;
-  if (plan_mtile(M, perm ? (int64_t)w->K : ldx, w, meta, &mp)) {
+  const bool gated = io.up != nullptr;
+  if (!gated && plan_mtile(M, perm ? (int64_t)w->K : ldx, w, meta, &mp)) {
     // M-tiled MFMA GEMM over all rows, the activations gathered first
     const uint16_t* Xa = X;
     int64_t lda = ldx;
@@ -187,8 +192,8 @@ tpdq_status run_gemm(const uint16_t* X, int64_t ldx, int M, const int32_t* perm,
     bool prepared = false;
     const bool ok = io.x_prepared
                         ? plan_decode(mc, w->K, w->N, w->group_size, w->num_groups, w->layout, meta,
-                                      kOperandPrepared, dt, &plan)
-                        : decode_plan_for(mc, perm != nullptr, w, meta, dt, &plan, &prepared);
+                                      kOperandPrepared, dt, &plan, gated)
+                        : decode_plan_for(mc, perm != nullptr, w, meta, dt, &plan, &prepared, gated);
     int operand = perm ? (prepared ? kOperandPrepared : kOperandGather) : kOperandPlain;
     if (ok && prepared) {
       uint16_t* Xp = (uint16_t*)ws;
@@ -221,6 +226,11 @@ tpdq_status run_gemm(const uint16_t* X, int64_t ldx, int M, const int32_t* perm,
     a.ldy = ldy;
     a.Yp = io.yp;
     a.yp_natural = io.yp_natural;
+    if (gated) {
+      a.qw_up = (const uint32_t*)io.up->qweight;
+      a.sc_up = (const uint16_t*)io.up->scales;
+      a.qz_up = (const uint32_t*)io.up->qzeros;
+    }
     float* part = (float*)(ws + decode_gather_bytes(M, w->K));
     hipError_t e = launch_decode(a, plan, part, st);
     if (e != hipSuccess) return hip_fail(e, "decode GEMM launch");
@@ -237,14 +247,15 @@ bool is_actorder(tpdq_path p) { return p == TPDQ_PATH_ACTORDER || p == TPDQ_PATH
 // GEMMs must be single decode launches of the tile kernels (not k_wide, not
 // the M-tiled kernel), and N1 a multiple of 128 (no padding to fill).
 bool mlp_prepared_y1(int M, int64_t ldx, bool perm, const tpdq_w4* w1, const tpdq_w4* w2, int meta,
-                     int dt) {
+                     int dt, bool gated = false) {
   if (M > kDecodeMaxM || w1->N % 128 != 0) return false;
   MtilePlan mp;
-  if (plan_mtile(M, perm ? (int64_t)w1->K : ldx, w1, meta, &mp) || plan_mtile(M, w1->N, w2, meta, &mp))
+  if ((!gated && plan_mtile(M, perm ? (int64_t)w1->K : ldx, w1, meta, &mp)) ||
+      plan_mtile(M, w1->N, w2, meta, &mp))
     return false;
   DecodePlan p1, p2;
   bool prepared = false;
-  if (!decode_plan_for(M, perm, w1, meta, dt, &p1, &prepared) || p1.wide) return false;
+  if (!decode_plan_for(M, perm, w1, meta, dt, &p1, &prepared, gated) || p1.wide) return false;
   if (!decode_plan_for(M, false, w2, meta, dt, &p2, &prepared) || p2.wide || p2.amode != kAGlobal)
     return false;
   DecodePlan p3;
@@ -300,11 +311,19 @@ size_t tpdq_workspace_bytes(int op, int32_t M, const tpdq_w4* a, const tpdq_w4* 
     return n;
   };
   if (op == 1) return gemm_max(a, true);
-  if (op == 2) {
+  if (op == 2 || op == 3) {
     if (!b) return 0;
-    // GEMM1's region, then Y1 in GEMM2's operand order (mlp_prepared_y1)
+    // GEMM1's region, then Y1 in GEMM2's operand order (mlp_prepared_y1);
+    // op 3: GEMM1 is the gated GEMM (a = w_gate)
     const size_t y1p = M <= kDecodeMaxM ? decode_gather_bytes(M, a->N) : 0;
-    return std::max(gemm_max(a, true) + y1p, gemm_max(b, false));
+    size_t g1 = gemm_max(a, true);
+    if (op == 3) {
+      g1 = decode_gather_bytes(M, a->K);
+      for (int pm = 0; pm <= 1; ++pm)
+        for (int meta : {kMetaGroup, kMetaRowLds, kMetaRowGlobal})
+          g1 = std::max(g1, gemm_ws_need(M, a->K, pm == 1, a, meta, TPDQ_FP16, true));
+    }
+    return std::max(g1 + y1p, gemm_max(b, false));
   }
   return 0;
 }
@@ -485,6 +504,65 @@ tpdq_status tpdq_mlp_shard(const void* X, int64_t ldx, int32_t M, const int32_t*
                     io2);
   return run_gemm((const uint16_t*)Y1, w1->N, M, nullptr, w2, path, dtype, (uint16_t*)Y2_partial,
                   w2->N, ws, s);
+}
+
+tpdq_status tpdq_gated_mlp_shard(const void* X, int64_t ldx, int32_t M, const int32_t* P1,
+                                 const tpdq_w4* w_gate, const tpdq_w4* w_up, const tpdq_w4* w_down,
+                                 tpdq_path path, tpdq_dtype dtype, void* Y1, void* Y2_partial,
+                                 void* workspace, size_t ws_bytes, void* stream) {
+  tpdq_status st = check_common(M, path, dtype);
+  if (st != TPDQ_OK) return st;
+  const bool act = is_actorder(path);
+  st = check_layer(w_gate, "w_gate", act, !act);
+  if (st != TPDQ_OK) return st;
+  st = check_layer(w_up, "w_up", false, !act);
+  if (st != TPDQ_OK) return st;
+  st = check_layer(w_down, "w_down", act, !act);
+  if (st != TPDQ_OK) return st;
+  if (w_up->K != w_gate->K || w_up->N != w_gate->N || w_up->group_size != w_gate->group_size ||
+      w_up->num_groups != w_gate->num_groups || w_up->layout != w_gate->layout ||
+      w_up->ld_q != w_gate->ld_q || w_up->ld_s != w_gate->ld_s || w_up->ld_z != w_gate->ld_z)
+    return fail(TPDQ_ERR_SHAPE, "w_up must match w_gate in shape, groups, layout and leading dimensions");
+  if (w_down->K != w_gate->N)
+    return fail(TPDQ_ERR_SHAPE, "w_down->K=%d != w_gate->N=%d", w_down->K, w_gate->N);
+  if (!X || !Y1 || !Y2_partial) return fail(TPDQ_ERR_NULL, "X, Y1 and Y2_partial are required");
+  if (act && P1) return fail(TPDQ_ERR_SHAPE, "the act-order paths take no P1");
+  if (!act && !P1) return fail(TPDQ_ERR_NULL, "the ordered path needs P1");
+  if (ldx < w_gate->K) return fail(TPDQ_ERR_SHAPE, "ldx=%lld < K1=%d", (long long)ldx, w_gate->K);
+  if (act) {
+    if (!aligned(X, 16) || ldx % 8)
+      return fail(TPDQ_ERR_ALIGN, "X needs 16-byte alignment and ldx %% 8 == 0");
+  } else if (!aligned(X, 2)) {
+    return fail(TPDQ_ERR_ALIGN, "X needs 2-byte alignment");
+  }
+  if (!aligned(Y1, 16) || !aligned(Y2_partial, 8))
+    return fail(TPDQ_ERR_ALIGN, "Y1 needs 16-byte and Y2_partial 8-byte alignment");
+  const int meta = meta_mode(path);
+  const size_t bound = tpdq_workspace_bytes(3, M, w_gate, w_down);
+  const size_t need = std::max(gemm_ws_need(M, ldx, !act, w_gate, meta, dtype, true),
+                               gemm_ws_need(M, w_gate->N, false, w_down, meta, dtype));
+  if ((!act || need) && (!workspace || ws_bytes < bound))
+    return fail(TPDQ_ERR_WORKSPACE, "gated MLP needs %zu workspace bytes, got %zu", bound, ws_bytes);
+  if (workspace && !aligned(workspace, 16))
+    return fail(TPDQ_ERR_ALIGN, "workspace needs 16-byte alignment");
+
+  hipStream_t s = (hipStream_t)stream;
+  char* ws = (char*)workspace;
+  GemmIO io1, io2;
+  io1.up = w_up;
+  if (workspace && ws_bytes >= bound && mlp_prepared_y1(M, ldx, !act, w_gate, w_down, meta, dtype, true)) {
+    io1.yp = (uint16_t*)(ws + gemm_ws_need(M, ldx, !act, w_gate, meta, dtype, true));
+    io1.yp_natural = w_down->layout == TPDQ_LAYOUT_TILED ? 1 : 0;
+    io2.x_prepared = true;
+  }
+  st = run_gemm((const uint16_t*)X, ldx, M, act ? nullptr : P1, w_gate, path, dtype, (uint16_t*)Y1,
+                w_gate->N, ws, s, io1);
+  if (st != TPDQ_OK) return st;
+  if (io2.x_prepared)
+    return run_gemm(io1.yp, w_gate->N, M, nullptr, w_down, path, dtype, (uint16_t*)Y2_partial,
+                    w_down->N, ws, s, io2);
+  return run_gemm((const uint16_t*)Y1, w_gate->N, M, nullptr, w_down, path, dtype,
+                  (uint16_t*)Y2_partial, w_down->N, ws, s);
 }
 
 }  // extern "C"

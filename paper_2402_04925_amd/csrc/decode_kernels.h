@@ -66,8 +66,9 @@ __device__ __forceinline__ void load_groups(const GemmArgs& a, bool ok, int wr, 
 // ---------------------------------------------------------------------------
 
 // Metadata of the 16-column tile (kMetaRowLds), one 16-byte entry per
-// (group, column): the scale's bits | z << 16 in the first word.
-template <int NT, int R>
+// (group, column): the scale's bits | z << 16 in word COMP (0; the gated
+// kernel's up projection in word 1).
+template <int NT, int R, int COMP = 0>
 struct MetaStage {
   uint32_t s[R], z[R];
   // Entry idx = 16 g + c: group g, column n0 + c. The loads are branch-free:
@@ -88,7 +89,7 @@ struct MetaStage {
   __device__ __forceinline__ static void put(u4_t* meta, int idx, int n, uint32_t sbits,
                                              uint32_t zw) {
     const uint32_t zc = (zw >> (4 * (n & 7))) & 0xFu;
-    meta[idx] = u4_t{sbits | (zc << 16), 0u, 0u, 0u};
+    ((uint32_t*)&meta[idx])[COMP] = sbits | (zc << 16);
   }
   // Entries past the last group go to the spare entry meta[items], so every
   // value loaded in load() is consumed on every path (a value used only
@@ -243,9 +244,11 @@ __device__ __forceinline__ int64_t prepared_offset(int row, int c, int nsteps, i
 
 // Sum the NW waves' partial tiles (TN tiles of 16 columns from n0) in LDS
 // and write Y in the element type; with a.Yp, Y is also written in the next
-// GEMM's prepared-operand layout (a.N a multiple of 128: no padding). acc[t][n] of lane l holds rows t*16 + 4*(l/16) + e, column
-// n0 + 16 n + l % 16.
-template <int MT, int NW, int TN, int DT>
+// GEMM's prepared-operand layout (a.N a multiple of 128: no padding).
+// acc[t][n] of lane l holds rows t*16 + 4*(l/16) + e, column n0 + 16 n +
+// l % 16. GATED: tiles 0 and 1 are the gate and up products of the same 16
+// columns, and Y = silu(gate) * up (in fp32, rounded once).
+template <int MT, int NW, int TN, int DT, bool GATED = false>
 __device__ __forceinline__ void reduce_store(const GemmArgs& a, f4_t (&acc)[MT][TN], int n0,
                                              unsigned char* smem) {
   const int tid = threadIdx.x;
@@ -261,6 +264,28 @@ __device__ __forceinline__ void reduce_store(const GemmArgs& a, f4_t (&acc)[MT][
       for (int e = 0; e < 4; ++e)
         red[(((wave * MT + t) * TN + n) * 4 + e) * 64 + lane] = acc[t][n][e];
   __syncthreads();
+  if constexpr (GATED) {
+    // tile 0 holds X W_gate, tile 1 X W_up, both for columns n0 .. n0 + 15
+    for (int idx = tid; idx < MT * 256; idx += NW * 64) {
+      const int t = idx >> 8;
+      const int e = (idx >> 6) & 3;
+      const int ln = idx & 63;
+      float g = 0.f, u = 0.f;
+#pragma unroll
+      for (int w = 0; w < NW; ++w) {
+        g += red[((w * MT * TN + t * TN + 0) * 4 + e) * 64 + ln];
+        u += red[((w * MT * TN + t * TN + 1) * 4 + e) * 64 + ln];
+      }
+      const int row = t * kTileM + 4 * (ln >> 4) + e;
+      const int c = n0 + (ln & 15);
+      if (row < a.M && c < a.N) {
+        const uint16_t v = float_to_bits<DT>(g / (1.f + __expf(-g)) * u);  // silu(g) * u
+        a.Y[(int64_t)row * a.ldy + c] = v;
+        if (a.Yp) a.Yp[prepared_offset(row, c, a.N >> 5, a.yp_natural)] = v;
+      }
+    }
+    return;
+  }
   for (int idx = tid; idx < MT * TN * 256; idx += NW * 64) {
     const int tn = idx >> 8;  // t * TN + n
     const int e = (idx >> 6) & 3;
@@ -496,8 +521,11 @@ struct ChunkMeta {
 // first block. Block ranges and the loop are wave-uniform (scalar); group
 // boundaries inside a chunk sit at compile-time positions for G <= 128.
 // ---------------------------------------------------------------------------
-template <int MT, int NW, int SPG, int AM, int LAYOUT, int TN, int DT>
+template <int MT, int NW, int SPG, int AM, int LAYOUT, int TN, int DT, bool GATED = false>
 __global__ __launch_bounds__(NW * 64) void k_ordered(GemmArgs a) {
+  // GATED: one 16-column tile, its TN = 2 weight streams are the gate and up
+  // projections (same shape and leading dimensions), Y = silu(gate) * up
+  static_assert(!GATED || TN == 2, "the gated kernel streams gate and up");
   extern __shared__ __align__(16) unsigned char smem[];
   constexpr int NT = NW * 64;
   constexpr bool AG = a_global(AM);
@@ -509,13 +537,20 @@ __global__ __launch_bounds__(NW * 64) void k_ordered(GemmArgs a) {
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int j = lane & 15;
   const int kq = lane >> 4;
-  const int tile0 = xcd_tile(blockIdx.x, gridDim.x) * TN;
+  const int tile0 = xcd_tile(blockIdx.x, gridDim.x) * (GATED ? 1 : TN);
   const int ntiles = (a.N + kTileN - 1) / kTileN;
   const int kw = a.K >> 3;
   const int ng = a.K / (32 * SPG);
   const int nblk = (a.K + 127) >> 7;
   const int b0 = (int)((int64_t)nblk * wave / NW);
   const int b1 = (int)((int64_t)nblk * (wave + 1) / NW);
+  GemmArgs au = a;  // stream n's weights: the up projection's for n = 1 when GATED
+  if constexpr (GATED) {
+    au.qw = a.qw_up;
+    au.sc = a.sc_up;
+    au.qz = a.qz_up;
+  }
+  auto tile_of = [&](int n) { return GATED ? tile0 : tile0 + n; };
   u4_t* xs = (u4_t*)(smem + a.lds_x_off);
   u4_t* xr = (u4_t*)(smem + a.lds_xr_off);
   const int zero_slot = a.M * 16 * nblk;  // the zero entry after the staged X
@@ -531,14 +566,15 @@ __global__ __launch_bounds__(NW * 64) void k_ordered(GemmArgs a) {
   ChunkMeta<SPG, DT> cm[TN];
 #pragma unroll
   for (int n = 0; n < TN; ++n) {
-    cm[n].init(a, ng, (tile0 + n) * kTileN + j, kq);
+    cm[n].init(GATED && n == 1 ? au : a, ng, tile_of(n) * kTileN + j, kq);
     cm[n].load((4 * b0) / SPG, b0 < b1, ng, kq);
   }
   __builtin_amdgcn_sched_barrier(0);
   WeightStream<LAYOUT> wsrc[TN];
 #pragma unroll
   for (int n = 0; n < TN; ++n)
-    wsrc[n].init(a, tile0 + n, tile0 + n < ntiles, lane, kq, (tile0 + n) * kTileN + j, nblk);
+    wsrc[n].init(GATED && n == 1 ? au : a, tile_of(n), tile_of(n) < ntiles, lane, kq,
+                 tile_of(n) * kTileN + j, nblk);
   const AStream<MT, AM> asrc(a, j, lane);
   u4_t wb[D][TN];
   u4_t ab[AG ? D : 1][4][MT];
@@ -663,7 +699,7 @@ __global__ __launch_bounds__(NW * 64) void k_ordered(GemmArgs a) {
       __builtin_amdgcn_sched_barrier(0);
     }
   }
-  reduce_store<MT, NW, TN, DT>(a, acc, tile0 * kTileN, smem);
+  reduce_store<MT, NW, TN, DT, GATED>(a, acc, tile0 * kTileN, smem);
 }
 
 
@@ -895,8 +931,10 @@ __global__ __launch_bounds__(NW * 64) void k_wide(GemmArgs a) {
 // (g_idx, or floor(k / G) when g_idx is NULL) and is dequantized on its own.
 // One 128-row block of weights (and of g_idx) is prefetched ahead.
 // ---------------------------------------------------------------------------
-template <int MT, int NW, int META, int AM, int LAYOUT, int DT>
+template <int MT, int NW, int META, int AM, int LAYOUT, int DT, bool GATED = false>
 __global__ __launch_bounds__(NW * 64) void k_rowmeta(GemmArgs a) {
+  // GATED: a second weight stream and metadata (the up projection, same
+  // shape, leading dimensions and g_idx), Y = silu(X W) * (X W_up)
   extern __shared__ __align__(16) unsigned char smem[];
   constexpr int NT = NW * 64;
   constexpr bool AG = a_global(AM);
@@ -920,9 +958,19 @@ __global__ __launch_bounds__(NW * 64) void k_rowmeta(GemmArgs a) {
   const uint32_t* qtile = a.qw + (int64_t)tile * a.ldq;
   const bool wok = LAYOUT == TPDQ_LAYOUT_TILED ? true : col_ok;
   const UnpackConsts<DT> kc;
+  GemmArgs au = a;
+  if constexpr (GATED) {
+    au.qw = a.qw_up;
+    au.sc = a.sc_up;
+    au.qz = a.qz_up;
+  }
+  const uint32_t* qcol_u = au.qw + col;
+  const uint32_t* qtile_u = au.qw + (int64_t)tile * a.ldq;
 
   MetaStage<NT, 8> ms;
+  MetaStage<NT, 8, 1> msu;
   if constexpr (META == kMetaRowLds) ms.load(a, n0, a.meta_rows, tid);
+  if constexpr (META == kMetaRowLds && GATED) msu.load(au, n0, a.meta_rows, tid);
   XStage<NT, false, LAYOUT> xst;
   if constexpr (!AG) xst.load(a, tid);
 
@@ -934,30 +982,38 @@ __global__ __launch_bounds__(NW * 64) void k_rowmeta(GemmArgs a) {
     }
   };
   u4_t wb = load_block<LAYOUT>(a, qcol, qtile, lane, kq, b0, b0 < b1 && wok, kw);
+  u4_t wbu = u4_t{0u, 0u, 0u, 0u};
+  if constexpr (GATED) wbu = load_block<LAYOUT>(a, qcol_u, qtile_u, lane, kq, b0, b0 < b1 && wok, kw);
   u4_t gb[4][2];
   load_g(b0, gb);
   u4_t ab[4][MT];
   if constexpr (AG) load_a_block<MT, AM, LAYOUT>(a, j, kq, b0, b0 < b1, kw, ab);
 
   if constexpr (META == kMetaRowLds) ms.store(a, meta, n0, a.meta_rows, tid);
+  if constexpr (META == kMetaRowLds && GATED) msu.store(au, meta, n0, a.meta_rows, tid);
   if constexpr (!AG) xst.store(a, xs, nullptr, tid);
   if constexpr (META == kMetaRowLds || !AG) __syncthreads();
   AAddr aa[MT];
 #pragma unroll
   for (int t = 0; t < MT; ++t) aa[t].init(a.M, j, kq, t, zero_slot);
 
-  f4_t acc[MT];
+  f4_t acc[MT], accu[MT];
 #pragma unroll
-  for (int t = 0; t < MT; ++t) acc[t] = f4_t{0.f, 0.f, 0.f, 0.f};
+  for (int t = 0; t < MT; ++t) {
+    acc[t] = f4_t{0.f, 0.f, 0.f, 0.f};
+    accu[t] = f4_t{0.f, 0.f, 0.f, 0.f};
+  }
   const uint32_t gmax = (uint32_t)(a.num_groups - 1);
   const int zshift = 4 * (col & 7);
   for (int b = b0; b < b1; ++b) {
     const bool more = b + 1 < b1;
     u4_t wn = u4_t{0u, 0u, 0u, 0u};
+    u4_t wnu = u4_t{0u, 0u, 0u, 0u};
     u4_t gn[4][2];
     u4_t an[4][MT];
     if (more) {
       wn = load_block<LAYOUT>(a, qcol, qtile, lane, kq, b + 1, wok, kw);
+      if constexpr (GATED) wnu = load_block<LAYOUT>(a, qcol_u, qtile_u, lane, kq, b + 1, wok, kw);
       load_g(b + 1, gn);
       if constexpr (AG) load_a_block<MT, AM, LAYOUT>(a, j, kq, b + 1, true, kw, an);
     }
@@ -972,25 +1028,43 @@ __global__ __launch_bounds__(NW * 64) void k_rowmeta(GemmArgs a) {
         else
           av[t] = xs[aa[t].base + aa[t].stride * (4 * b + u)];
       }
-      uint32_t zr[8], sr[8];
+      uint32_t zr[8], sr[8], zru[8], sru[8];
 #pragma unroll
       for (int r = 0; r < 8; ++r) {
         const uint32_t g = min(r < 4 ? gb[u][0][r] : gb[u][1][r - 4], gmax);
         if constexpr (META == kMetaRowLds) {
-          const uint32_t v = meta[g * kTileN + j].x;
-          zr[r] = v >> 16;
-          sr[r] = v & 0xFFFFu;
+          if constexpr (GATED) {
+            const uint2 v = *(const uint2*)&meta[g * kTileN + j];
+            zr[r] = v.x >> 16;
+            sr[r] = v.x & 0xFFFFu;
+            zru[r] = v.y >> 16;
+            sru[r] = v.y & 0xFFFFu;
+          } else {
+            const uint32_t v = meta[g * kTileN + j].x;
+            zr[r] = v >> 16;
+            sr[r] = v & 0xFFFFu;
+          }
         } else {
           sr[r] = col_ok ? (uint32_t)a.sc[(int64_t)g * a.lds + col] : 0u;
           zr[r] = col_ok ? (a.qz[(int64_t)g * a.ldz + (col >> 3)] >> zshift) & 0xFu : 0u;
+          if constexpr (GATED) {
+            sru[r] = col_ok ? (uint32_t)au.sc[(int64_t)g * a.lds + col] : 0u;
+            zru[r] = col_ok ? (au.qz[(int64_t)g * a.ldz + (col >> 3)] >> zshift) & 0xFu : 0u;
+          }
         }
       }
       const u4_t bv = dequant_rows<LAYOUT == TPDQ_LAYOUT_TILED, DT>(kc, wb[u], zr, sr);
 #pragma unroll
       for (int t = 0; t < MT; ++t) acc[t] = mfma_k32<DT>(av[t], bv, acc[t]);
+      if constexpr (GATED) {
+        const u4_t bvu = dequant_rows<LAYOUT == TPDQ_LAYOUT_TILED, DT>(kc, wbu[u], zru, sru);
+#pragma unroll
+        for (int t = 0; t < MT; ++t) accu[t] = mfma_k32<DT>(av[t], bvu, accu[t]);
+      }
     }
     if (more) {
       wb = wn;
+      if constexpr (GATED) wbu = wnu;
 #pragma unroll
       for (int u = 0; u < 4; ++u) {
         gb[u][0] = gn[u][0];
@@ -1004,10 +1078,20 @@ __global__ __launch_bounds__(NW * 64) void k_rowmeta(GemmArgs a) {
       }
     }
   }
-  f4_t acc1[MT][1];
+  if constexpr (GATED) {
+    f4_t acc2[MT][2];
 #pragma unroll
-  for (int t = 0; t < MT; ++t) acc1[t][0] = acc[t];
-  reduce_store<MT, NW, 1, DT>(a, acc1, n0, smem);
+    for (int t = 0; t < MT; ++t) {
+      acc2[t][0] = acc[t];
+      acc2[t][1] = accu[t];
+    }
+    reduce_store<MT, NW, 2, DT, true>(a, acc2, n0, smem);
+  } else {
+    f4_t acc1[MT][1];
+#pragma unroll
+    for (int t = 0; t < MT; ++t) acc1[t][0] = acc[t];
+    reduce_store<MT, NW, 1, DT>(a, acc1, n0, smem);
+  }
 }
 
 // Kernel selection for a plan (DecodeKernel is declared with DecodePlan).
@@ -1110,6 +1194,70 @@ DecodeKernel pick_wide(const DecodePlan& p) {
     case 4: return prep ? pick_wide_spg<4, 1, true, DT>(p.spg) : pick_wide_spg<4, 1, false, DT>(p.spg);
   }
   return nullptr;
+}
+
+// Gated kernels (silu(X W_gate) * (X W_up)): the ordered kernel with the
+// two projections as its two weight streams (4 waves with X from global
+// memory, 4 or 8 with X in LDS, as plan_decode gives), and the per-row kernel
+// with a second stream. Instantiated in their own translation units.
+template <int MT, int NW, int SPG, int L, int DT>
+DecodeKernel pick_gated_ordered_am(int am) {
+  switch (am) {
+    case kAGlobal:
+      if constexpr (NW == 4) return k_ordered<MT, NW, SPG, kAGlobal, L, 2, DT, true>;
+      return nullptr;
+    case kAGlobalPrep:
+      if constexpr (NW == 4) return k_ordered<MT, NW, SPG, kAGlobalPrep, L, 2, DT, true>;
+      return nullptr;
+    case kALds: return k_ordered<MT, NW, SPG, kALds, L, 2, DT, true>;
+    case kALdsGather: return k_ordered<MT, NW, SPG, kALdsGather, L, 2, DT, true>;
+  }
+  return nullptr;
+}
+
+template <int MT, int NW, int L, int DT>
+DecodeKernel pick_gated_mt_nw(const DecodePlan& p) {
+  if (p.meta == kMetaGroup) {
+    switch (p.spg) {
+      case 1: return pick_gated_ordered_am<MT, NW, 1, L, DT>(p.amode);
+      case 2: return pick_gated_ordered_am<MT, NW, 2, L, DT>(p.amode);
+      case 4: return pick_gated_ordered_am<MT, NW, 4, L, DT>(p.amode);
+      case 8: return pick_gated_ordered_am<MT, NW, 8, L, DT>(p.amode);
+    }
+    return nullptr;
+  }
+  if constexpr (!(MT == 4 && NW > 4)) {
+    const bool lds = p.meta == kMetaRowLds;
+    switch (p.amode) {
+      case kAGlobal:
+        return lds ? k_rowmeta<MT, NW, kMetaRowLds, kAGlobal, L, DT, true>
+                   : k_rowmeta<MT, NW, kMetaRowGlobal, kAGlobal, L, DT, true>;
+      case kAGlobalPrep:
+        return lds ? k_rowmeta<MT, NW, kMetaRowLds, kAGlobalPrep, L, DT, true>
+                   : k_rowmeta<MT, NW, kMetaRowGlobal, kAGlobalPrep, L, DT, true>;
+      case kALds:
+        return lds ? k_rowmeta<MT, NW, kMetaRowLds, kALds, L, DT, true>
+                   : k_rowmeta<MT, NW, kMetaRowGlobal, kALds, L, DT, true>;
+    }
+  }
+  return nullptr;
+}
+
+template <int L, int DT>
+DecodeKernel pick_gated_layout(const DecodePlan& p) {
+  const int nw = p.nw;
+  switch (p.mt) {
+    case 1: return nw == 4 ? pick_gated_mt_nw<1, 4, L, DT>(p) : nw == 8 ? pick_gated_mt_nw<1, 8, L, DT>(p) : nullptr;
+    case 2: return nw == 4 ? pick_gated_mt_nw<2, 4, L, DT>(p) : nw == 8 ? pick_gated_mt_nw<2, 8, L, DT>(p) : nullptr;
+    case 4: return nw == 4 ? pick_gated_mt_nw<4, 4, L, DT>(p) : nw == 8 ? pick_gated_mt_nw<4, 8, L, DT>(p) : nullptr;
+  }
+  return nullptr;
+}
+
+template <int DT>
+DecodeKernel pick_gated_dt(const DecodePlan& p) {
+  if (p.layout == TPDQ_LAYOUT_TILED) return pick_gated_layout<TPDQ_LAYOUT_TILED, DT>(p);
+  return pick_gated_layout<TPDQ_LAYOUT_GPTQ, DT>(p);
 }
 
 // the kernel of a plan: k_wide, or the tile kernel of its layout

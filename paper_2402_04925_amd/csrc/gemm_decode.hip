@@ -61,12 +61,13 @@ DecodeKernel decode_kernel_f16(const DecodePlan& p) { return pick_kernel_dt<kF16
 
 namespace {
 DecodeKernel decode_kernel(const DecodePlan& p) {
+  if (p.gated) return p.dt == kBF16 ? decode_kernel_gated_bf16(p) : decode_kernel_gated_f16(p);
   return p.dt == kBF16 ? decode_kernel_bf16(p) : decode_kernel_f16(p);
 }
 }  // namespace
 
 bool plan_decode(int M, int K, int N, int G, int num_groups, int layout, int meta_pref, int operand,
-                 int dt, DecodePlan* p) {
+                 int dt, DecodePlan* p, bool gated) {
   if (M < 1 || M > kDecodeMaxM) return false;
   const int mt = M <= 16 ? 1 : (M <= 32 ? 2 : 4);
   const int ntiles = (N + kTileN - 1) / kTileN;
@@ -83,10 +84,11 @@ bool plan_decode(int M, int K, int N, int G, int num_groups, int layout, int met
     meta = kMetaRowLds;  // sorted rows of another G: per-row groups floor(k / G)
   if ((meta != kMetaGroup || mt == 4) && nw > 8) nw = 8;
   if (meta != kMetaGroup && mt == 4) nw = 4;  // four row tiles of per-row dequant: registers
+  if (gated && nw > 8) nw = 8;                 // two weight streams per wave
   // tile metadata in LDS: the per-row act-order kernel only (the ordered
   // kernel's travels with its weight stream)
   int meta_rows = meta == kMetaRowLds ? num_groups : 0;
-  const size_t red = (size_t)nw * mt * 1024;
+  const size_t red = (size_t)nw * mt * (gated ? 2 : 1) * 1024;
   size_t meta_bytes =
       meta_rows ? align_up(((size_t)meta_rows * kTileN + 1) * 16, 16) : 0;  // + a spare entry
   if (meta_bytes > kLdsMax - red) {
@@ -122,11 +124,12 @@ bool plan_decode(int M, int K, int N, int G, int num_groups, int layout, int met
     nw = (!a_global(am) && nblk >= 48 && ntiles <= 256) ? 8 : 4;
     if (a_global(am) && ntiles >= 512) tn = 2;
   }
+  if (gated) tn = 2;  // the gate and up streams of one 16-column tile
   // the wide kernel when X is read from global memory and the weights are
   // large (the decode kernel re-reads X for every 16 columns): 8 waves over
   // 128 columns share X through LDS, K split until about kWideTargetWgs
   // workgroups stream
-  p->wide = meta == kMetaGroup && layout == TPDQ_LAYOUT_TILED && a_global(am) &&
+  p->wide = !gated && meta == kMetaGroup && layout == TPDQ_LAYOUT_TILED && a_global(am) &&
             (int64_t)K * N >= kWideMinWeights;
   p->ks = 1;
   if (p->wide) {
@@ -135,6 +138,7 @@ bool plan_decode(int M, int K, int N, int G, int num_groups, int layout, int met
     p->ks = std::max(1, std::min((kWideTargetWgs + wgs - 1) / wgs, std::max(1, nblk / 4)));
   }
   p->tn = tn;
+  p->gated = gated;
   p->dt = dt;
   p->layout = layout;
   p->meta = meta;
@@ -186,7 +190,8 @@ hipError_t launch_decode(const GemmArgs& a0, const DecodePlan& p, float* part, h
     if (e != hipSuccess) return e;
   }
   const int ntiles = (a.N + kTileN - 1) / kTileN;
-  hipLaunchKernelGGL(k, dim3((ntiles + p.tn - 1) / p.tn), dim3(p.nw * 64), p.lds_bytes, s, a);
+  const int grid = p.gated ? ntiles : (ntiles + p.tn - 1) / p.tn;  // gated: both streams, one tile
+  hipLaunchKernelGGL(k, dim3(grid), dim3(p.nw * 64), p.lds_bytes, s, a);
   return hipGetLastError();
 }
 

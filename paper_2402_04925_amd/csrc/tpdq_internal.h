@@ -68,6 +68,11 @@ struct GemmArgs {
   // that GEMM's weights are tiled
   uint16_t* Yp;
   int yp_natural;
+  // gated GEMM (plan.gated): the up projection's weights and metadata, with
+  // the same shape, leading dimensions, g_idx and layout as qw, sc, qz
+  const uint32_t* qw_up;
+  const uint16_t* sc_up;
+  const uint32_t* qz_up;
   int meta_rows;          // metadata rows staged in LDS
   int lds_x_off;          // byte offset of the staged X in LDS
   int lds_xr_off;         // kALdsGather: byte offset of the LDS copy of X's rows
@@ -75,6 +80,7 @@ struct GemmArgs {
 
 // Host-side plan of one decode launch.
 struct DecodePlan {
+  bool gated;   // Y = silu(X W) * (X W_up): two weight streams, tn = 2
   int dt;       // tpdq_dtype
   int layout;   // tpdq_layout of qweight
   int meta;     // MetaMode
@@ -102,11 +108,13 @@ constexpr int kWideTargetWgs = 200;
 // covers the request (for kOperandGather: the gather does not fit in LDS, the
 // caller then runs launch_gather_prep and plans with kOperandPrepared).
 bool plan_decode(int M, int K, int N, int G, int num_groups, int layout, int meta_pref, int operand,
-                 int dt, DecodePlan* p);
+                 int dt, DecodePlan* p, bool gated = false);
 // the kernel of a plan, per element type (gemm_decode.hip, gemm_decode_bf16.hip)
 typedef void (*DecodeKernel)(GemmArgs);
 DecodeKernel decode_kernel_f16(const DecodePlan& p);
 DecodeKernel decode_kernel_bf16(const DecodePlan& p);
+DecodeKernel decode_kernel_gated_f16(const DecodePlan& p);   // gemm_gated.hip
+DecodeKernel decode_kernel_gated_bf16(const DecodePlan& p);  // gemm_gated_bf16.hip
 // part: the workspace for k_wide's split-K partials (ks x M x N floats)
 hipError_t launch_decode(const GemmArgs& a, const DecodePlan& p, float* part, hipStream_t s);
 // Xp [M][K] = X[:, perm] (perm may be NULL), each octet in operand order.

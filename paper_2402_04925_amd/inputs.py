@@ -27,8 +27,10 @@ import numpy as np
 
 BASE_SEED = 20240207
 
-# tensor ids for the per-tensor streams
+# tensor ids for the per-tensor streams (T_*U: the up projection of a gated
+# MLP, whose act-order permutation is W1's: both read the same input)
 T_PHI1, T_PHI2, T_QW1, T_QW2, T_S1, T_S2, T_Z1, T_Z2, T_X = range(9)
+T_QWU, T_SU, T_ZU = 9, 10, 11
 
 
 @dataclasses.dataclass(frozen=True)
@@ -143,6 +145,15 @@ def make_workload(w: Workload, seed: int = BASE_SEED, scale_dtype=np.float16):
     if w.N2:
         w2 = make_layer(w.K2, w.N2, w.G, w.cfg_id, T_PHI2, T_QW2, T_S2, T_Z2, seed, scale_dtype)
     return w1, w2
+
+
+def make_gated_workload(w: Workload, seed: int = BASE_SEED, scale_dtype=np.float16):
+    """Global layers of the gated form of a workload: (gate, up, down). gate
+    and down are make_workload's W1 and W2; up has gate's shape and act-order
+    permutation (hence its g_idx) and codes, scales and zeros of its own."""
+    gate, down = make_workload(w, seed, scale_dtype)
+    up = make_layer(w.K1, w.N1, w.G, w.cfg_id, T_PHI1, T_QWU, T_SU, T_ZU, seed, scale_dtype)
+    return gate, up, down
 
 
 def make_x(w: Workload, M: int, seed: int = BASE_SEED, dtype=np.float16) -> np.ndarray:
