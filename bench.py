@@ -442,6 +442,83 @@ def bf16_line(dev, steps, warmup):
                          f"bf16 X, scales and outputs", by_M=res)
 
 
+def gated_line(dev, steps, warmup):
+    """The gated form of the headline workload (Llama-70B TP = 8 rank 0:
+    gate and up 8192 x 3584 each, down 3584 x 8192): tpdq_gated_mlp_shard on
+    the ordered path (P2 folded into gate and up) and the act-order path, at
+    each M, weights rotating over replicas of at least ROTATE_MIN_BYTES."""
+    import ctypes
+    import torch
+    import paper_2402_04925_amd as tpdq
+    from paper_2402_04925_amd import inputs
+    wl = inputs.WORKLOADS["llama70b_tp8"]
+    gate, up, down = inputs.make_gated_workload(wl)
+
+    def dl(L):
+        return tpdq.QuantWeight.from_tensors(
+            torch.from_numpy(L.qweight).to(dev), torch.from_numpy(L.scales).to(dev),
+            torch.from_numpy(L.qzeros).to(dev), torch.from_numpy(L.g_idx.astype(np.int32)).to(dev), L.G)
+
+    dg, du, dd = dl(gate), dl(up), dl(down)
+    P1, _, _, _, gf, do = tpdq.reorder(dg, dd)
+    _, _, _, _, uf, _ = tpdq.reorder(du, dd)
+    tp = wl.tp
+
+    def dense(q, with_g):
+        return tpdq.QuantWeight(q.qweight.contiguous(), q.scales.contiguous(), q.qzeros.contiguous(),
+                                q.g_idx.contiguous() if with_g and q.g_idx is not None else None,
+                                q.K, q.N, q.G, q.num_groups, q.layout)
+
+    base = [dense(gf.column_shard(0, tp), False), dense(uf.column_shard(0, tp), False),
+            dense(do.row_shard(0, tp, True), False), dense(dg.column_shard(0, tp), True),
+            dense(du.column_shard(0, tp), True), dense(dd.row_shard(0, tp, False), True)]
+    per = sum(t.qweight.numel() * 4 + t.scales.numel() * 2 + t.qzeros.numel() * 4 for t in base[:3])
+    R = max(2, -(-ROTATE_MIN_BYTES // per))
+    reps = [base] + [[tpdq.QuantWeight(q.qweight.clone(), q.scales.clone(), q.qzeros.clone(),
+                                       q.g_idx.clone() if q.g_idx is not None else None,
+                                       q.K, q.N, q.G, q.num_groups, q.layout) for q in base]
+                     for _ in range(R - 1)]
+    del dg, du, dd, gf, uf, do
+    torch.cuda.synchronize()
+    eprint(f"[bench] gated {wl.name}: {R} weight replicas of {per / 1e6:.1f} MB (ordered triple)")
+    lib = tpdq._abi.lib()
+    ws = tpdq.Workspace(dev)
+    N1, K2 = wl.N1 // tp, wl.K2 // tp
+    res = {}
+    for M in wl.Ms:
+        X = torch.from_numpy(inputs.make_x(wl, M)).to(dev)
+        y1 = torch.empty(M, N1, dtype=torch.float16, device=dev)
+        y2 = torch.empty(M, wl.N2, dtype=torch.float16, device=dev)
+
+        def mk(rep, ordered):
+            g, u, d = (rep[0], rep[1], rep[2]) if ordered else (rep[3], rep[4], rep[5])
+            cg, cu, cd = g.c_struct(), u.c_struct(), d.c_struct()
+            nb = lib.tpdq_workspace_bytes(tpdq.OP_GATED_MLP, M, ctypes.byref(cg), ctypes.byref(cd))
+            buf = ws.get(nb)
+            path = tpdq.PATH_ORDERED if ordered else tpdq.PATH_ACTORDER
+            p1 = P1.data_ptr() if ordered else None
+
+            def call():
+                tpdq._abi.check(lib.tpdq_gated_mlp_shard(
+                    X.data_ptr(), X.stride(0), M, p1, ctypes.byref(cg), ctypes.byref(cu), ctypes.byref(cd),
+                    path, tpdq.FP16, y1.data_ptr(), y2.data_ptr(), buf.data_ptr(), buf.numel(),
+                    torch.cuda.current_stream(dev).cuda_stream))
+            return call
+
+        mo, _ = capture_and_time([mk(rep, True) for rep in reps], steps, warmup, dev)
+        ma, _ = capture_and_time([mk(rep, False) for rep in reps], steps, warmup, dev)
+        b = 2 * shard_bytes(wl.K1, N1, wl.G) + M * wl.K1 * 2 + M * N1 * 2 + gemm_bytes(M, K2, wl.N2, wl.G)
+        res[str(M)] = dict(ordered_mlp_us=round(mo * 1e3, 3), actorder_mlp_us=round(ma * 1e3, 3),
+                           speedup_ordered_vs_actorder=round(ma / mo, 3),
+                           ordered_mlp_gbs=round(b / (mo * 1e-3) / 1e9, 1))
+        eprint(f"[bench] gated {wl.name} M={M}: ordered mlp {mo*1e3:.2f} us ({b / (mo * 1e-3) / 1e9:.0f} GB/s), "
+               f"actorder mlp {ma*1e3:.2f} us")
+    del reps, base
+    torch.cuda.synchronize()
+    return dict(workload=f"{wl.name} gated: rank-0 shard, gate and up {wl.K1}x{N1}, down {K2}x{wl.N2}, "
+                         f"int4 G={wl.G}, fp16 X, Y1 = silu(X W_gate) * (X W_up)", weight_replicas=R, by_M=res)
+
+
 def prefill_line(dev, steps=10):
     """The Llama-70B TP = 2 prefill shard (M = 2048): the ordered MLP shard
     and its two GEMMs (graph replay), TFLOP/s against the dense fp16 MFMA
@@ -493,6 +570,8 @@ def main():
                     help="skip the Llama-70B TP=2 prefill shard (M=2048, MFMA-bound) line")
     ap.add_argument("--no-bf16", action="store_true",
                     help="skip the bf16 line (the headline shard with bf16 activations and scales)")
+    ap.add_argument("--no-gated", action="store_true",
+                    help="skip the gated-MLP line (the headline shard with a gate projection)")
     ap.add_argument("--profile-run", action="store_true",
                     help="eager launches for rocprofv3 (kernel trace or counters); no JSON")
     args = ap.parse_args()
@@ -549,6 +628,7 @@ def main():
     configs = None if args.no_configs else config_lines(dev, args.steps, args.warmup)
     prefill = None if args.no_prefill else prefill_line(dev)
     bf16 = None if args.no_bf16 else bf16_line(dev, args.steps, args.warmup)
+    gated = None if args.no_gated else gated_line(dev, args.steps, args.warmup)
 
     M = args.M
     r = results[M]
@@ -601,7 +681,7 @@ def main():
         hbm_frac=round(b["mlp"] / (mlp_us * 1e-6) / 1e9 / HBM_PEAK_GBS, 4),
         tflops=round(r["flops"] / (mlp_us * 1e-6) / 1e12, 3),
         speedup_vs_actorder=round(r["actorder"]["mlp_us"] / mlp_us, 3),
-        roofline=roof, cpu_baseline=cpu, configs=configs, prefill=prefill, bf16=bf16,
+        roofline=roof, cpu_baseline=cpu, configs=configs, prefill=prefill, bf16=bf16, gated=gated,
         copy_1gib_gbs=round(copy_gbs, 1),
         roofline_frac_of_copy=round(achieved / copy_gbs, 4),
         sweep=sweep,
