@@ -157,3 +157,32 @@ def test_workspace_sizes(lib):
     assert r >= 4 * (64 + 28)
     assert lib.tpdq_workspace_bytes(_abi.OP_MLP, 4, ctypes.byref(w1), None) == 0
     assert lib.tpdq_workspace_bytes(_abi.OP_GEMM, 0, ctypes.byref(w1), None) == 0
+
+
+@needs_no_gpu
+def test_gated_mlp_validation(lib):
+    wg = fake_layer(K=256, N=512)
+    wu = fake_layer(K=256, N=512, base=1 << 23)
+    wd = fake_layer(K=512, N=128, base=1 << 22)
+    wu_bad = fake_layer(K=256, N=256, base=1 << 23)
+    wu_ld = fake_layer(K=256, N=512, base=1 << 23)
+    wu_ld.ld_q = 520
+    wd_bad = fake_layer(K=256, N=128, base=1 << 22)
+
+    def f(g, u, d, P1=1 << 27, path=_abi.PATH_ORDERED, ws=None, nb=0, dtype=_abi.FP16):
+        return lib.tpdq_gated_mlp_shard(
+            1 << 24, 256, 4, P1, ctypes.byref(g) if g is not None else None,
+            ctypes.byref(u) if u is not None else None, ctypes.byref(d), path, dtype, 1 << 25, 1 << 26,
+            ws, nb, None)
+    assert f(None, wu, wd) == _abi.ERR_NULL                                  # gate required
+    assert f(wg, None, wd) == _abi.ERR_NULL                                  # up required
+    assert f(wg, wu_bad, wd) == _abi.ERR_SHAPE                               # up != gate shape
+    assert f(wg, wu_ld, wd) == _abi.ERR_SHAPE                                # up != gate leading dims
+    assert f(wg, wu, wd_bad) == _abi.ERR_SHAPE                               # down K != N1
+    assert f(wg, wu, wd, P1=None) == _abi.ERR_NULL                           # ordered needs P1
+    assert f(wg, wu, wd, path=_abi.PATH_ACTORDER) == _abi.ERR_SHAPE          # act-order takes no P1
+    assert f(wg, wu, wd, dtype=2) == _abi.ERR_SHAPE                          # unknown dtype
+    assert f(wg, wu, wd) == _abi.ERR_WORKSPACE                               # the gather needs one
+    for M in (1, 16, 64, 200):
+        n = lib.tpdq_workspace_bytes(_abi.OP_GATED_MLP, M, ctypes.byref(wg), ctypes.byref(wd))
+        assert n > 0 and n % 256 == 0
