@@ -118,11 +118,13 @@ bool plan_decode(int M, int K, int N, int G, int num_groups, int layout, int met
     // the ordered kernel streams best with 8 waves (about 8 blocks of 128
     // rows each) when the grid has no more workgroups than CUs, else with 4
     // (measured on the Llama-70B and Granite-20B shapes); with X read from
-    // global memory, 4 waves, and two tiles per workgroup when that still
-    // leaves a workgroup per CU
+    // global memory, 4 waves, and two tiles per workgroup (half the re-reads
+    // of X) from 384 tiles on: Granite-20B TP=4 at M = 16 (384 tiles, 192
+    // workgroups) 14.7 -> 9.7 us per GEMM, while the Llama-70B TP=8 GEMM1
+    // (224 tiles) is slower paired (10.5 -> 11.1 us)
     const int nblk = (K + 127) / 128;
     nw = (!a_global(am) && nblk >= 48 && ntiles <= 256) ? 8 : 4;
-    if (a_global(am) && ntiles >= 512) tn = 2;
+    if (a_global(am) && ntiles >= 384) tn = 2;
   }
   if (gated) tn = 2;  // the gate and up streams of one 16-column tile
   // the wide kernel when X is read from global memory and the weights are
