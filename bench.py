@@ -544,6 +544,15 @@ def prefill_line(dev, steps=10):
            f"gemm2 {g2*1e3:.1f} us; actorder mlp {ma*1e3:.1f} us")
     del c, st
     torch.cuda.synchronize()
+    # the same ordered MLP with bf16 activations and scales (bf16 MFMA; the
+    # weights are dequantized in fp32 and rounded to bf16)
+    st = Setup(wl, dev, min_bytes=0, bf16=True)
+    c = Calls(st, M, dev)
+    mb, _ = capture_and_time([c.mlp(rep, "ordered") for rep in st.reps[:1]], steps, 2, dev)
+    tfb = flops / (mb * 1e-3) / 1e12
+    eprint(f"[bench] prefill M={M} bf16: ordered mlp {mb*1e3:.1f} us ({tfb:.0f} TFLOP/s)")
+    del c, st
+    torch.cuda.synchronize()
     return dict(
         workload=f"{wl.name}: rank-0 TP-aware MLP shard, W1 {wl.K1}x{N1}, W2 {K2}x{wl.N2}, "
                  f"int4 G={wl.G}, fp16 X, M={M}",
@@ -552,6 +561,8 @@ def prefill_line(dev, steps=10):
         tflops=round(tf, 1), gemm_tflops=[round(t, 1) for t in tf_g],
         peak_tflops=MFMA_F16_PEAK_TFLOPS, frac=round(tf / MFMA_F16_PEAK_TFLOPS, 4),
         actorder_mlp_us=round(ma * 1e3, 1), speedup_vs_actorder=round(ma / ms, 2),
+        bf16_ordered_mlp_us=round(mb * 1e3, 1), bf16_tflops=round(tfb, 1),
+        bf16_frac=round(tfb / MFMA_F16_PEAK_TFLOPS, 4),
         timing="HIP graph replay, events, median of 5")
 
 
