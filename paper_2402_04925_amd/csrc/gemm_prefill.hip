@@ -378,15 +378,18 @@ bool plan_mtile(int M, int64_t ldx, const tpdq_w4* w, int meta, MtilePlan* p) {
     // below prefill sizes the weight stream bounds the product; worth it
     // only when the weights are large enough that the decode kernels'
     // per-workgroup re-reads of X dominate: 64-row tiles, 4 waves (two
-    // workgroups per CU), K split so that about kMtileTargetWgs workgroups
-    // stream
+    // workgroups per CU, i.e. two waves per SIMD), K split as far as the
+    // workgroups still fit those kMtileSlots slots in one round (Llama-70B
+    // TP=1 at M = 64: GEMM1 448 workgroups 56.8 -> 51.9 us, GEMM2 512
+    // workgroups 54.9 -> 51.0 us, against about 256 before: one wave per
+    // SIMD left the loads' latency exposed)
     if ((int64_t)K * N < kMtileMinWeights) return false;
     q.rt = 4;
     q.nw = 4;
     q.st = 2;
     const int nblk = (K + 127) / 128;
     const int tiles = ((M + 63) / 64) * ((N + 255) / 256);
-    int ks = (kMtileTargetWgs + tiles - 1) / tiles;
+    int ks = kMtileSlots / tiles;
     ks = std::max(1, std::min(ks, nblk / 4));
     if ((int64_t)ks * M * N * 4 >= lim) ks = 1;
     q.ks = ks;

@@ -132,7 +132,7 @@ hipError_t launch_gather_prep(const uint16_t* X, int64_t ldx, int M, int K, cons
 constexpr int kPrefillMinM = 256;
 constexpr int kMtileMinM = 33;
 constexpr int64_t kMtileMinWeights = (int64_t)64 << 20;
-constexpr int kMtileTargetWgs = 256;
+constexpr int kMtileSlots = 512;  // two workgroups per CU on 256 CUs
 struct MtilePlan {
   int rt, nw, st, ks;  // row tiles and waves per workgroup, LDS stages, K splits
 };
