@@ -29,11 +29,15 @@ def _run(tpdq, Xd, dev, gate, up, down, rank, tp, variant):
         P1, _, P2, _, gf, do = tpdq.reorder(dg, dd, layout=lay)
         P1u, _, _, _, uf, _ = tpdq.reorder(du, dd, layout=lay)
         assert bool((P1 == P1u).all())
+        if tp == 1:   # the whole layers (a tiled shard must cover whole 16-column tiles)
+            return tpdq.gated_mlp_shard(Xd, gf, uf, do, tpdq.PATH_ORDERED, P1=P1)
         return tpdq.gated_mlp_shard(Xd, gf.column_shard(rank, tp), uf.column_shard(rank, tp),
                                     do.row_shard(rank, tp, True), tpdq.PATH_ORDERED, P1=P1)
     if variant == "actorder-tiled":
         dg, du, dd = tpdq.pack_tiled(dg), tpdq.pack_tiled(du), tpdq.pack_tiled(dd)
     path = tpdq.PATH_ACTORDER_GLOBAL if variant == "actorder-global" else tpdq.PATH_ACTORDER
+    if tp == 1:
+        return tpdq.gated_mlp_shard(Xd, dg, du, dd, path)
     return tpdq.gated_mlp_shard(Xd, dg.column_shard(rank, tp), du.column_shard(rank, tp),
                                 dd.row_shard(rank, tp, False), path)
 
@@ -117,3 +121,38 @@ def test_gated_full_size(name, M, dtype):
         W2 = o.dequant(*_l(down), cols=c2)[sel]
         e2 = o.round_to(o.matmul(np_of(y1).astype(np.float64), W2), dtype)
         assert o.rel_err(np_of(y2)[:, c2], e2) <= tol, variant
+
+
+@pytest.mark.parametrize("M", [3, 17])
+@pytest.mark.parametrize("variant", ["ordered", "actorder"])
+def test_gated_ragged(M, variant):
+    """Ragged K and N (not multiples of 128 or 16) and G = 8: the ordered path
+    takes the per-row gated kernel with groups floor(k / G)."""
+    import torch
+    import paper_2402_04925_amd as tpdq
+    dev = torch_dev()
+    K1, N1, N2, G = 288, 200, 72, 8
+    log(f"gated ragged {variant} M={M}")
+    gate, up, down = _custom(K1, N1, N2, G, 60 + M)
+    X = inputs.random_activations(M, K1, np.random.default_rng(M + 60))
+    y1, y2 = _run(tpdq, to_dev(X, dev), dev, gate, up, down, 0, 1, variant)
+    torch.cuda.synchronize()
+    eP2, _ = o.reorder(down.g_idx)
+    e1, e2 = o.gated_rank_from_global(X, _l(gate), _l(up, gate.g_idx), _l(down), 0, 1,
+                                      variant == "ordered", P2=eP2)
+    assert o.rel_err(np_of(y1), e1) <= TOL_FP16
+    assert o.rel_err(np_of(y2), e2) <= TOL_FP16
+
+
+def test_gated_deterministic():
+    """Two calls give bit-identical outputs."""
+    import torch
+    import paper_2402_04925_amd as tpdq
+    dev = torch_dev()
+    gate, up, down = _custom(1024, 512, 256, 128, 3)
+    X = to_dev(inputs.random_activations(16, 1024, np.random.default_rng(3)), dev)
+    a = [np_of(t) for t in _run(tpdq, X, dev, gate, up, down, 0, 1, "ordered")]
+    b = [np_of(t) for t in _run(tpdq, X, dev, gate, up, down, 0, 1, "ordered")]
+    torch.cuda.synchronize()
+    for x, y in zip(a, b):
+        assert np.array_equal(x.view(np.uint16), y.view(np.uint16))
