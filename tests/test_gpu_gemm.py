@@ -197,3 +197,32 @@ def test_gemm_interleaved_shapes_share_workspace():
         ref = o.w4a16_gemm(X, w1.qweight, w1.scales, w1.qzeros, w1.g_idx)
         assert o.rel_err(np_of(Yo), ref) <= TOL_FP16
         assert o.rel_err(np_of(Ya), ref) <= TOL_FP16
+
+
+# degenerate shapes: one group (G = K), the smallest N (half a 16-column
+# tile), the smallest K (one 8-row word), a single row
+DEGENERATE = [(256, 64, 256, 5), (128, 8, 128, 1), (8, 8, 8, 1), (8, 24, 8, 3), (512, 8, 32, 16)]
+
+
+@pytest.mark.parametrize("K,N,G,M", DEGENERATE)
+def test_gemm_degenerate(K, N, G, M):
+    """Every path and layout on degenerate shapes, against the oracle."""
+    import torch
+    import paper_2402_04925_amd as tpdq
+    dev = torch_dev()
+    log(f"gemm degenerate K={K} N={N} G={G} M={M}")
+    w1, _ = inputs.make_custom(K, N, 0, G, seed=K * 7 + N + G)
+    X = inputs.random_activations(M, K, np.random.default_rng(K + M))
+    Xd = to_dev(X, dev)
+    dw = layer_to_dev(w1, dev)
+    ref = o.w4a16_gemm(X, w1.qweight, w1.scales, w1.qzeros, w1.g_idx)
+    for path in (tpdq.PATH_ACTORDER, tpdq.PATH_ACTORDER_GLOBAL):
+        for w in (dw, tpdq.pack_tiled(dw)):
+            Y = tpdq.w4a16_gemm(Xd, w, path)
+            torch.cuda.synchronize()
+            assert o.rel_err(np_of(Y), ref) <= TOL_FP16, path
+    for lay in (tpdq.LAYOUT_TILED, tpdq.LAYOUT_GPTQ):
+        P, _, _, _, wo, _ = tpdq.reorder(dw, layout=lay)
+        Y = tpdq.w4a16_gemm(Xd, wo, tpdq.PATH_ORDERED, x_perm=P)
+        torch.cuda.synchronize()
+        assert o.rel_err(np_of(Y), ref) <= TOL_FP16, lay
