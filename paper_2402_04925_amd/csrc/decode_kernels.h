@@ -1019,7 +1019,6 @@ __global__ __launch_bounds__(NW * 64) void k_rowmeta(GemmArgs a) {
     }
 #pragma unroll
     for (int u = 0; u < 4; ++u) {
-      const int wr = 4 * (4 * b + u) + kq;
       u4_t av[MT];
 #pragma unroll
       for (int t = 0; t < MT; ++t) {
