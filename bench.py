@@ -205,6 +205,71 @@ def cpu_baseline(wl, M, L1, L2, budget_s=20.0):
                        f"ordered, float64 dequant + GEMM), median")
 
 
+def cpu_model() -> str:
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def cpu_detail():
+    """The oracle on the host beyond the headline sample (reported only):
+    Alg. 1 (the stable argsort of both g_idx) and the rank-0 MLP shard of
+    every decode workload at its largest decode M, with the BLAS thread pool
+    at its default size and at one thread, and the tiny single GEMM on both
+    paths. One run per item except the tiny GEMM (median of 20); the
+    unsharded Llama-70B shard computes 512 of the 8192 GEMM2 columns."""
+    from threadpoolctl import threadpool_info, threadpool_limits
+    from oracle import tpdq_oracle as o
+    from paper_2402_04925_amd import inputs
+
+    def timed(fn, runs=1):
+        ts = []
+        for _ in range(runs):
+            t0 = time.perf_counter()
+            fn()
+            ts.append(time.perf_counter() - t0)
+        return float(np.median(ts)) * 1e6
+
+    pool = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
+    out = dict(cpu_model=cpu_model(), logical_cpus=os.cpu_count(), blas_threads=int(pool),
+               unit="us", kind="oracle", items={})
+    w = inputs.WORKLOADS["tiny_gemm"]
+    L, _ = inputs.make_workload(w)
+    X = inputs.make_x(w, 4)
+    P, g = o.reorder(L.g_idx)
+    l_act = (L.qweight, L.scales, L.qzeros, L.g_idx)
+    qo = o.permute_rows(dict(qweight=L.qweight, scales=L.scales, qzeros=L.qzeros), P)["qweight"]
+    out["items"]["tiny_gemm"] = dict(
+        M=4, reorder_us=round(timed(lambda: o.reorder(L.g_idx), 20), 1),
+        actorder_gemm_us=round(timed(lambda: o.w4a16_gemm(X, *l_act), 20), 1),
+        ordered_gemm_us=round(timed(lambda: o.w4a16_gemm(X, qo, L.scales, L.qzeros, g, x_perm=P), 20), 1))
+    for name, M, sample in (("llama70b_tp8", 16, None), ("granite20b_tp4", 16, None),
+                            ("llama70b_tp1", 64, 512)):
+        w = inputs.WORKLOADS[name]
+        L1, L2 = inputs.make_workload(w)
+        X = inputs.make_x(w, M)
+        P2, _ = o.reorder(L2.g_idx)
+        l1 = (L1.qweight, L1.scales, L1.qzeros, L1.g_idx)
+        l2 = (L2.qweight, L2.scales, L2.qzeros, L2.g_idx)
+        cols = None if sample is None else np.arange(0, w.N2, w.N2 // sample)
+        mlp = lambda: o.mlp_rank_from_global(X, l1, l2, 0, w.tp, True, P2=P2, cols2=cols)
+        it = dict(M=M, reorder_us=round(timed(lambda: (o.reorder(L1.g_idx), o.reorder(L2.g_idx))), 1),
+                  mlp_shard_us=round(timed(mlp), 1))
+        with threadpool_limits(limits=1):
+            it["mlp_shard_us_1thread"] = round(timed(mlp), 1)
+        if sample is not None:
+            it["gemm2_columns"] = f"{sample} of {w.N2}"
+        out["items"][name] = it
+        eprint(f"[bench] oracle on the host, {name} M={M}: {it}")
+        del L1, L2
+    return out
+
+
 class Calls:
     """Library calls of one batch size M on the rank-0 shards: the MLP shard
     and each GEMM on its own, for every path, one closure per weight replica."""
@@ -652,9 +717,10 @@ def main():
     roof = dict(bound="hbm", achieved=round(achieved, 1), peak=HBM_PEAK_GBS, unit="GB/s",
                 frac=round(achieved / HBM_PEAK_GBS, 4), traffic=traffic,
                 kernel="k_ordered (its GEMM1 and GEMM2 launches averaged)")
-    cpu = None
+    cpu = cpu_host = None
     if not args.no_cpu_baseline:
         cpu = cpu_baseline(wl, M, st.L1, st.L2)
+        cpu_host = cpu_detail()
 
     sweep = {}
     for m, rr in results.items():
@@ -692,7 +758,7 @@ def main():
         hbm_frac=round(b["mlp"] / (mlp_us * 1e-6) / 1e9 / HBM_PEAK_GBS, 4),
         tflops=round(r["flops"] / (mlp_us * 1e-6) / 1e12, 3),
         speedup_vs_actorder=round(r["actorder"]["mlp_us"] / mlp_us, 3),
-        roofline=roof, cpu_baseline=cpu, configs=configs, prefill=prefill, bf16=bf16, gated=gated,
+        roofline=roof, cpu_baseline=cpu, cpu_detail=cpu_host, configs=configs, prefill=prefill, bf16=bf16, gated=gated,
         copy_1gib_gbs=round(copy_gbs, 1),
         roofline_frac_of_copy=round(achieved / copy_gbs, 4),
         sweep=sweep,
