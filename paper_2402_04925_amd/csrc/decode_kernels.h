@@ -120,10 +120,13 @@ struct MetaStage {
 // GPTQ weights, as they are for tiled ones), for r < 16 * ceil(K / 128)
 // (zero past K). One more zero entry follows (see
 // AAddr), then a spare entry. With GATHER the operand column k is X column
-// perm[k] (X[:, perm]): the rows of X are first copied to LDS as they are
-// (at xr, [M][K]) and gathered from there, so no global load waits on
-// another. Global loads are buffer loads: octets past K load zeros at no
-// cost and go to a spare entry.
+// perm[k] (X[:, perm]): the rows of X are first copied to LDS (at xr) and
+// gathered from there, so no global load waits on another. With 2 <= M <= 4
+// (and every piece of X held in registers) the copy is column-major, four
+// halves per column (rows 0..3, zero past M), so one 8-byte LDS read
+// fetches a column of every row; otherwise it is row-major, [M][K].
+// Global loads are buffer loads: octets past K load zeros at no cost and go
+// to a spare entry.
 template <int NT, bool GATHER, int LAYOUT>
 struct XStage {
   static constexpr int R = 8;
@@ -167,6 +170,33 @@ struct XStage {
     else
       xs[r < kw ? r * M + m : spare] = to_operand<LAYOUT>(x);
   }
+  // column-major copy of X: octet r = tid + I NT of rows 0..3 (pieces in
+  // slots m P + I, zeros past M) as eight 8-byte columns at xr + 4 r
+  template <int SL>
+  __device__ __forceinline__ u4_t slot(bool on) const {
+    if constexpr (SL < R) return on ? v[SL] : u4_t{0u, 0u, 0u, 0u};
+    return u4_t{0u, 0u, 0u, 0u};
+  }
+  template <int P, int I>
+  __device__ __forceinline__ void store_colmajor(u4_t* xr, int M, int kw, int tid) const {
+    if constexpr (I < P) {
+      const u4_t row[4] = {slot<I>(true), slot<P + I>(M > 1), slot<2 * P + I>(M > 2),
+                           slot<3 * P + I>(M > 3)};
+      const int r = tid + I * NT;
+      u4_t* dst = xr + 4 * (r < kw ? r : kw);  // octets past K: the spare columns
+#pragma unroll
+      for (int w = 0; w < 4; ++w)  // columns 2w, 2w + 1
+        dst[w] = u4_t{__builtin_amdgcn_perm(row[1][w], row[0][w], 0x05040100u),
+                      __builtin_amdgcn_perm(row[3][w], row[2][w], 0x05040100u),
+                      __builtin_amdgcn_perm(row[1][w], row[0][w], 0x07060302u),
+                      __builtin_amdgcn_perm(row[3][w], row[2][w], 0x07060302u)};
+      store_colmajor<P, I + 1>(xr, M, kw, tid);
+    }
+  }
+  static __device__ __forceinline__ bool colmajor(int M, int kw) {
+    const int P = (kw + NT - 1) / NT;
+    return GATHER && M >= 2 && M <= 4 && M * P <= R;
+  }
   __device__ __forceinline__ void store(const GemmArgs& a, u4_t* xs, u4_t* xr, int tid) {
     const int kw = a.K >> 3;
     const int M = a.M;
@@ -174,6 +204,44 @@ struct XStage {
     const int kwp = 16 * ((a.K + 127) >> 7);
     const int spare = kwp * M + 1;  // after the zero entry
     for (int e = kw * M + tid; e <= kwp * M; e += NT) xs[e] = u4_t{0u, 0u, 0u, 0u};
+    if (GATHER && colmajor(M, kw)) {
+      switch (P) {
+        case 1: store_colmajor<1, 0>(xr, M, kw, tid); break;
+        case 2: store_colmajor<2, 0>(xr, M, kw, tid); break;
+        case 3: store_colmajor<3, 0>(xr, M, kw, tid); break;
+        default: store_colmajor<4, 0>(xr, M, kw, tid); break;
+      }
+      __syncthreads();  // the copy of X is complete
+      const uint32_t kmax = (uint32_t)(a.K - 1);
+      const unsigned char* xb = (const unsigned char*)xr;
+      for (int r = tid; r < kw; r += NT) {
+        u4_t p0 = p[0], p1 = p[1];
+        if (r != tid) {
+          p0 = *(const u4_t*)(a.perm + r * 8);
+          p1 = *(const u4_t*)(a.perm + r * 8 + 4);
+          wait_vmcnt<0>();
+        }
+        uint32_t q[8][2];  // column perm[8 r + e]: rows 0, 1 in q[e][0], rows 2, 3 in q[e][1]
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const uint32_t c = min(e < 4 ? p0[e] : p1[e - 4], kmax);
+          const uint2 t = *(const uint2*)(xb + 8u * c);
+          q[e][0] = t.x;
+          q[e][1] = t.y;
+        }
+#pragma unroll
+        for (int mr = 0; mr < 4; ++mr) {
+          if (mr >= M) break;
+          const uint32_t sel = (mr & 1) ? 0x07060302u : 0x05040100u;
+          const int h = mr >> 1;
+          xs[r * M + mr] = to_operand<LAYOUT>(u4_t{__builtin_amdgcn_perm(q[1][h], q[0][h], sel),
+                                                   __builtin_amdgcn_perm(q[3][h], q[2][h], sel),
+                                                   __builtin_amdgcn_perm(q[5][h], q[4][h], sel),
+                                                   __builtin_amdgcn_perm(q[7][h], q[6][h], sel)});
+        }
+      }
+      return;
+    }
     int m = 0, i = 0;
 #pragma unroll
     for (int sl = 0; sl < R; ++sl) {

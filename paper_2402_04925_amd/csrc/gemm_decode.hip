@@ -98,7 +98,10 @@ bool plan_decode(int M, int K, int N, int G, int num_groups, int layout, int met
   }
   // padded X + the zero entry + a spare entry
   const size_t x_bytes = ((size_t)M * 16 * ((K + 127) / 128) + 2) * 16;
-  const size_t xr_bytes = align_up((size_t)M * K * 2, 16) + 16;  // the gather's copy of X + spare
+  // the gather's copy of X + spare: row-major, or column-major with four
+  // halves per column for 2 <= M <= 4 (see XStage)
+  const size_t xr_bytes = (M >= 2 && M <= 4) ? (size_t)(K / 8 + 1) * 64
+                                             : align_up((size_t)M * K * 2, 16) + 16;
   // stage X in LDS when it leaves room for two workgroups per CU (or one,
   // when the grid has no more workgroups than CUs)
   const size_t budget = ntiles <= 256 ? kLdsMax : kLdsMax / 2;

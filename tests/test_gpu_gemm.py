@@ -41,6 +41,27 @@ def test_gemm_actorder(K, N, G, M, variant):
     assert o.rel_err(np_of(Y), ref) <= TOL_FP16
 
 
+@pytest.mark.parametrize("K,N,G,M", [(K, N, G, M) for (K, N, G) in SHAPES for M in (2, 3)] +
+                         [(8192, 256, 128, M) for M in (2, 3, 4)] + [(6144, 4352, 128, 2)])
+@pytest.mark.parametrize("layout", ["tiled", "gptq"])
+def test_gemm_ordered_gather_rows(K, N, G, M, layout):
+    """The X[:, P] gather from the column-major LDS copy of X (2 <= M <= 4):
+    ragged shapes, the Llama-70B K with one and two octets per thread, and
+    4 waves with three octets per thread (over 256 column tiles)."""
+    import torch
+    import paper_2402_04925_amd as tpdq
+    dev = torch_dev()
+    log(f"gemm ordered gather K={K} N={N} G={G} M={M} {layout}")
+    w1, _ = inputs.make_custom(K, N, 0, G, seed=K + N + G + M)
+    X = inputs.random_activations(M, K, np.random.default_rng(M + 7))
+    lay = tpdq.LAYOUT_TILED if layout == "tiled" else tpdq.LAYOUT_GPTQ
+    P, _, _, _, wo, _ = tpdq.reorder(layer_to_dev(w1, dev), layout=lay)
+    Y = tpdq.w4a16_gemm(to_dev(X, dev), wo, tpdq.PATH_ORDERED, x_perm=P)
+    torch.cuda.synchronize()
+    ref = o.w4a16_gemm(X, w1.qweight, w1.scales, w1.qzeros, w1.g_idx)
+    assert o.rel_err(np_of(Y), ref) <= TOL_FP16
+
+
 @pytest.mark.parametrize("K,N,G", SHAPES)
 @pytest.mark.parametrize("M", MS)
 @pytest.mark.parametrize("layout", ["tiled", "gptq"])
