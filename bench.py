@@ -381,6 +381,23 @@ def copy_ceiling(dev, reps=10):
     return 2 * COPY_BYTES / sec / 1e9
 
 
+def copy_shard(dev, nbytes, steps, warmup):
+    """Graph-timed device copy of one buffer the size of a weight shard
+    (torch's copy kernel, one launch per step, rotating over enough buffers
+    that every step reads HBM): what one launch that moves this many bytes
+    costs on the part, for comparison with the GEMMs of the same size."""
+    import torch
+    n = nbytes // 2
+    reps = max(2, -(-ROTATE_MIN_BYTES // nbytes))
+    pairs = [(torch.ones(n, dtype=torch.float16, device=dev), torch.empty(n, dtype=torch.float16, device=dev))
+             for _ in range(reps)]
+    fns = [(lambda s=s_, d=d_: d.copy_(s)) for s_, d_ in pairs]
+    ms, _ = capture_and_time(fns, steps, warmup, dev)
+    del pairs, fns
+    torch.cuda.synchronize()
+    return ms * 1e3
+
+
 def profile_run(st, Ms, launches, dev):
     """Eager launches for rocprofv3 (kernel trace or counters): every path's
     GEMM1 and GEMM2 and the ordered MLP shard at each M, `launches` times
@@ -701,6 +718,9 @@ def main():
         torch.cuda.synchronize()
     copy_gbs = copy_ceiling(dev)
     eprint(f"[bench] 1 GiB device copy: {copy_gbs:.0f} GB/s (read + write)")
+    shard_bytes_w1 = wl.K1 * (wl.N1 // wl.tp) // 2
+    copy_shard_us = copy_shard(dev, shard_bytes_w1, args.steps, args.warmup)
+    eprint(f"[bench] device copy of {shard_bytes_w1 / 1e6:.1f} MB (one launch): {copy_shard_us:.2f} us")
     configs = None if args.no_configs else config_lines(dev, args.steps, args.warmup)
     prefill = None if args.no_prefill else prefill_line(dev)
     bf16 = None if args.no_bf16 else bf16_line(dev, args.steps, args.warmup)
@@ -760,6 +780,10 @@ def main():
         speedup_vs_actorder=round(r["actorder"]["mlp_us"] / mlp_us, 3),
         roofline=roof, cpu_baseline=cpu, cpu_detail=cpu_host, configs=configs, prefill=prefill, bf16=bf16, gated=gated,
         copy_1gib_gbs=round(copy_gbs, 1),
+        copy_w1_shard=dict(bytes=shard_bytes_w1, us=round(copy_shard_us, 3),
+                           gbs=round(2 * shard_bytes_w1 / (copy_shard_us * 1e-6) / 1e9, 1),
+                           what="one device-copy launch of a buffer the size of the packed W1 shard "
+                                "(read + write), graph-timed like the GEMMs"),
         roofline_frac_of_copy=round(achieved / copy_gbs, 4),
         sweep=sweep,
         paper_context="paper: up to 1.81x (Llama-70B) / 1.78x (Granite-20B) Alg. 3 vs Alg. 2 on "
