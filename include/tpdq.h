@@ -54,7 +54,9 @@ typedef enum {
   TPDQ_ERR_ALIGN = 3,       /* a pointer or leading dimension breaks the vector alignment */
   TPDQ_ERR_GIDX = 4,        /* g_idx out of range, or a group without exactly G rows    */
   TPDQ_ERR_WORKSPACE = 5,   /* workspace NULL or smaller than tpdq_workspace_bytes()    */
-  TPDQ_ERR_UNSUPPORTED = 6, /* valid request this build does not implement              */
+  TPDQ_ERR_UNSUPPORTED = 6, /* valid request this build does not implement, e.g. a tensor of
+                             2 GiB or more (the kernels address each tensor with 32-bit
+                             byte offsets)                                             */
   TPDQ_ERR_HIP = 7          /* a HIP runtime call or a kernel launch failed             */
 } tpdq_status;
 

@@ -59,6 +59,13 @@ tpdq_status check_layer(const tpdq_w4* w, const char* name, bool need_gidx, bool
   if (w->ld_q < ldq_min || w->ld_s < w->N || w->ld_z < w->N / 8)
     return fail(TPDQ_ERR_SHAPE, "%s: leading dimensions too small (ld_q=%lld ld_s=%lld ld_z=%lld)",
                 name, (long long)w->ld_q, (long long)w->ld_s, (long long)w->ld_z);
+  // the kernels address each tensor through a buffer resource with 32-bit
+  // byte offsets
+  const int64_t lim = (int64_t)1 << 31;
+  const int64_t qrows = w->layout == TPDQ_LAYOUT_TILED ? (int64_t)(w->N + 15) / 16 : w->K / 8;
+  if (qrows * w->ld_q * 4 >= lim || (int64_t)w->num_groups * w->ld_s * 2 >= lim ||
+      (int64_t)w->num_groups * w->ld_z * 4 >= lim)
+    return fail(TPDQ_ERR_UNSUPPORTED, "%s: qweight, scales or qzeros spans 2 GiB or more", name);
   if (!aligned(w->qweight, 16) || w->ld_q % 4)
     return fail(TPDQ_ERR_ALIGN, "%s: qweight needs 16-byte alignment and ld_q %% 4 == 0", name);
   if (!aligned(w->scales, 8) || w->ld_s % 4)

@@ -83,6 +83,12 @@ def test_gemm_validation(lib):
     assert gemm(lib, w, dtype=2) == _abi.ERR_SHAPE                         # unknown dtype
     assert gemm(lib, w, path=7) == _abi.ERR_SHAPE
     assert gemm(lib, nog, path=_abi.PATH_ACTORDER_GLOBAL) == _abi.ERR_NULL
+    huge = fake_layer()
+    huge.ld_q = 1 << 28                     # 32 word rows x 2^28 words: past 32-bit offsets
+    assert gemm(lib, huge) == _abi.ERR_UNSUPPORTED
+    huge = fake_layer()
+    huge.ld_s = 1 << 28                     # 8 scale rows x 2^28 halves
+    assert gemm(lib, huge) == _abi.ERR_UNSUPPORTED
     need = lib.tpdq_workspace_bytes(_abi.OP_GEMM, 4, ctypes.byref(w), None)
     assert need > 0
     # the query covers the gathered-activation buffer, so ask with a gather
