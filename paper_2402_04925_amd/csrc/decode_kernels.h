@@ -1315,8 +1315,8 @@ DecodeKernel pick_gated_layout(const DecodePlan& p) {
   const int nw = p.nw;
   switch (p.mt) {
     case 1: return nw == 4 ? pick_gated_mt_nw<1, 4, L, DT>(p) : nw == 8 ? pick_gated_mt_nw<1, 8, L, DT>(p) : nullptr;
-    case 2: return nw == 4 ? pick_gated_mt_nw<2, 4, L, DT>(p) : nw == 8 ? pick_gated_mt_nw<2, 8, L, DT>(p) : nullptr;
-    case 4: return nw == 4 ? pick_gated_mt_nw<4, 4, L, DT>(p) : nw == 8 ? pick_gated_mt_nw<4, 8, L, DT>(p) : nullptr;
+    case 2: return nw == 4 ? pick_gated_mt_nw<2, 4, L, DT>(p) : nullptr;  // 4 waves (plan_decode)
+    case 4: return nw == 4 ? pick_gated_mt_nw<4, 4, L, DT>(p) : nullptr;
   }
   return nullptr;
 }

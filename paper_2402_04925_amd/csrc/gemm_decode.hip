@@ -130,6 +130,9 @@ bool plan_decode(int M, int K, int N, int G, int num_groups, int layout, int met
     if (a_global(am) && ntiles >= 384) tn = 2;
   }
   if (gated) tn = 2;  // the gate and up streams of one 16-column tile
+  // two weight streams over two or four row tiles: 8 waves (two per SIMD)
+  // leave too few registers (the compiler spills), so 4
+  if (gated && mt >= 2) nw = 4;
   // the wide kernel when X is read from global memory and the weights are
   // large (the decode kernel re-reads X for every 16 columns): 8 waves over
   // 128 columns share X through LDS, K split until about kWideTargetWgs
