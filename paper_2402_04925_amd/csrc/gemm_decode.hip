@@ -103,12 +103,17 @@ bool plan_decode(int M, int K, int N, int G, int num_groups, int layout, int met
   const size_t xr_bytes = (M >= 2 && M <= 4) ? (size_t)(K / 8 + 1) * 64
                                              : align_up((size_t)M * K * 2, 16) + 16;
   // stage X in LDS when it leaves room for two workgroups per CU (or one,
-  // when the grid has no more workgroups than CUs)
+  // when the grid has no more workgroups than CUs); the ordered kernel only
+  // up to 4 rows: from 8 rows on X read from global memory (two column
+  // tiles per workgroup on large grids) measured faster (Llama-70B TP=8 at
+  // M = 8: GEMM2 8.43 -> 6.26 us, GEMM1 8.74 -> 8.24 us; at M = 4 LDS wins,
+  // GEMM1 6.33 against 7.93 us)
   const size_t budget = ntiles <= 256 ? kLdsMax : kLdsMax / 2;
-  const bool fits = meta_bytes + x_bytes <= budget;
+  const bool small_m = meta != kMetaGroup || M <= 4;
+  const bool fits = meta_bytes + x_bytes <= budget && small_m;
   int am;
   if (operand == kOperandGather) {
-    if (meta_bytes + x_bytes + xr_bytes > budget || meta != kMetaGroup) return false;
+    if (meta_bytes + x_bytes + xr_bytes > budget || meta != kMetaGroup || M > 4) return false;
     am = kALdsGather;
   } else if (operand == kOperandPrepared) {
     am = kAGlobalPrep;
