@@ -187,7 +187,8 @@ tpdq_status tpdq_pack_tiled(const tpdq_w4* w, int32_t* qweight_out, void* stream
  * Y  [M][ldy] output, 8 B aligned, ldy % 4 == 0, ldy >= N.
  * Workspace: at least tpdq_workspace_bytes(1, M, w, NULL) bytes, any content
  * (it holds the gathered X' when the gather cannot be done on chip, and the
- * fp32 split-K partials of the kernels that split K on large weights). A
+ * fp32 split-K partials of the kernels that split K: on large weights, and
+ * on weights of 16M elements or more when X is row-major and M > 16). A
  * call with x_perm always needs one; without x_perm, a call that needs none
  * accepts NULL. Calls that overlap in time must not share a workspace.
  * Deterministic: the same inputs give bit-identical outputs (split-K

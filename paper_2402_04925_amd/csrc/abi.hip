@@ -263,7 +263,12 @@ bool mlp_prepared_y1(int M, int64_t ldx, bool perm, const tpdq_w4* w1, const tpd
   DecodePlan p1, p2;
   bool prepared = false;
   if (!decode_plan_for(M, perm, w1, meta, dt, &p1, &prepared, gated) || p1.wide) return false;
-  if (!decode_plan_for(M, false, w2, meta, dt, &p2, &prepared) || p2.wide || p2.amode != kAGlobal)
+  // GEMM2 would read row-major Y1 from global memory: through the tile
+  // kernel, or through k_wide only because of the row-major rule (on
+  // weights of kWideMinWeights or more GEMM2 stays on k_wide instead)
+  const bool big2 = (int64_t)w2->K * w2->N >= kWideMinWeights;
+  if (!decode_plan_for(M, false, w2, meta, dt, &p2, &prepared) || (p2.wide && big2) ||
+      p2.amode != kAGlobal)
     return false;
   DecodePlan p3;
   return plan_decode(M, w2->K, w2->N, w2->group_size, w2->num_groups, w2->layout, meta,

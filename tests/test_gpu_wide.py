@@ -1,5 +1,5 @@
 """GPU wide decode kernel (ordered path, tiled weights of at least 64M
-elements, X too large to stage whole in LDS: 8 waves over 128 columns share
+elements, or of 16M with row-major X and M > 16; X too large to stage whole in LDS: 8 waves over 128 columns share
 the activations through LDS, K split over workgroups when the columns alone
 give too few) against the oracle on sampled columns."""
 import numpy as np
@@ -17,6 +17,8 @@ pytestmark = pytest.mark.gpu
 SHAPES = [
     (8192, 8192, 128, 8), (8192, 8200, 64, 16), (4096, 16384, 32, 17), (16384, 4096, 256, 32),
     (8192, 28672, 128, 12),
+    # 16M to 64M elements: row-major X with two or more row tiles only
+    (8192, 3584, 128, 32), (3584, 8192, 128, 64), (6144, 6144, 128, 40),
 ]
 
 
