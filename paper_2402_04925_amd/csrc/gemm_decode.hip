@@ -109,11 +109,18 @@ bool plan_decode(int M, int K, int N, int G, int num_groups, int layout, int met
   // M = 8: GEMM2 8.43 -> 6.26 us, GEMM1 8.74 -> 8.24 us; at M = 4 LDS wins,
   // GEMM1 6.33 against 7.93 us)
   const size_t budget = ntiles <= 256 ? kLdsMax : kLdsMax / 2;
+  // On weights of kWideMinWeights or more, from 3 rows on, the wide kernel
+  // (X shared by 8 column tiles through LDS) beats staging all of X per
+  // 16-column workgroup (Llama-70B TP=1 GEMM1 at M = 4: 31.0 -> 24.7 us; at
+  // M <= 2 they are even)
+  const bool wide_pref = layout == TPDQ_LAYOUT_TILED && meta == kMetaGroup && !gated &&
+                         (int64_t)K * N >= kWideMinWeights && M >= 3;
   const bool small_m = meta != kMetaGroup || M <= 4;
-  const bool fits = meta_bytes + x_bytes <= budget && small_m;
+  const bool fits = meta_bytes + x_bytes <= budget && small_m && !wide_pref;
   int am;
   if (operand == kOperandGather) {
-    if (meta_bytes + x_bytes + xr_bytes > budget || meta != kMetaGroup || M > 4) return false;
+    if (meta_bytes + x_bytes + xr_bytes > budget || meta != kMetaGroup || M > 4 || wide_pref)
+      return false;
     am = kALdsGather;
   } else if (operand == kOperandPrepared) {
     am = kAGlobalPrep;
