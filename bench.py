@@ -626,6 +626,25 @@ def prefill_line(dev, steps=10):
            f"gemm2 {g2*1e3:.1f} us; actorder mlp {ma*1e3:.1f} us")
     del c, st
     torch.cuda.synchronize()
+    # context: the same MLP as two dense fp16 GEMMs (torch.matmul, i.e. the
+    # vendor GEMM library) on random fp16 weights of the shard's shapes, the
+    # MFMA throughput a dense GEMM reaches on this part at these sizes
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(1)
+    Xd = torch.randn(M, wl.K1, generator=gen, device=dev).to(torch.float16)
+    Wd1 = (torch.randn(wl.K1, N1, generator=gen, device=dev) * 0.01).to(torch.float16)
+    Wd2 = (torch.randn(K2, wl.N2, generator=gen, device=dev) * 0.01).to(torch.float16)
+    yd1 = torch.empty(M, N1, dtype=torch.float16, device=dev)
+    yd2 = torch.empty(M, wl.N2, dtype=torch.float16, device=dev)
+
+    def dense_mlp():
+        torch.matmul(Xd, Wd1, out=yd1)
+        torch.matmul(yd1, Wd2, out=yd2)
+    md, _ = capture_and_time([dense_mlp], steps, 2, dev)
+    tfd = flops / (md * 1e-3) / 1e12
+    eprint(f"[bench] prefill M={M}: fp16 dense mlp (torch.matmul) {md*1e3:.1f} us ({tfd:.0f} TFLOP/s)")
+    del Xd, Wd1, Wd2, yd1, yd2
+    torch.cuda.synchronize()
     # the same ordered MLP with bf16 activations and scales (bf16 MFMA; the
     # weights are dequantized in fp32 and rounded to bf16)
     st = Setup(wl, dev, min_bytes=0, bf16=True)
@@ -645,6 +664,8 @@ def prefill_line(dev, steps=10):
         actorder_mlp_us=round(ma * 1e3, 1), speedup_vs_actorder=round(ma / ms, 2),
         bf16_ordered_mlp_us=round(mb * 1e3, 1), bf16_tflops=round(tfb, 1),
         bf16_frac=round(tfb / MFMA_F16_PEAK_TFLOPS, 4),
+        fp16_dense_mlp_us=round(md * 1e3, 1), fp16_dense_tflops=round(tfd, 1),
+        ordered_over_fp16_dense_tflops=round(tf / tfd, 3),
         timing="HIP graph replay, events, median of 5")
 
 
