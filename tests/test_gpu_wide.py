@@ -19,6 +19,8 @@ SHAPES = [
     (8192, 28672, 128, 12),
     # 16M to 64M elements: row-major X with two or more row tiles only
     (8192, 3584, 128, 32), (3584, 8192, 128, 64), (6144, 6144, 128, 40),
+    # 64M elements at M = 3 and 4, where X would fit in LDS (wide from 3 rows on)
+    (8192, 8192, 128, 3), (8192, 8192, 128, 4),
 ]
 
 
