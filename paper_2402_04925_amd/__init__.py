@@ -50,6 +50,39 @@ def _dtype_code(dt) -> int:
     raise TypeError(f"activations and scales must be float16 or bfloat16, got {dt}")
 
 
+def _check_args(device, scales_dtype=None, **tensors):
+    """Every tensor argument is on `device`, a GPU, so that the library only
+    ever receives device pointers; int32 index tensors are contiguous; the
+    activations' element type is the scales' (the C ABI takes one type)."""
+    torch = _torch()
+    if device.type != "cuda":
+        raise ValueError(f"the weights must be on a GPU, got {device}")
+    for name, t in tensors.items():
+        if t is None:
+            continue
+        if t.device != device:
+            raise ValueError(f"{name} is on {t.device}, the weights on {device}")
+        if name in ("x_perm", "P1") and (t.dtype != torch.int32 or not t.is_contiguous()):
+            raise ValueError(f"{name} must be a contiguous int32 tensor")
+    X = tensors.get("X")
+    if X is not None and scales_dtype is not None and X.dtype != scales_dtype:
+        raise TypeError(f"X is {X.dtype} but the scales are {scales_dtype}: one element type per call")
+
+
+def _check_layers(X, *layers):
+    """The layers share X's device and element type (their scales')."""
+    for i, w in enumerate(layers):
+        if w.device != X.device:
+            raise ValueError(f"layer {i} is on {w.device}, X on {X.device}")
+        if w.scales.dtype != X.dtype:
+            raise TypeError(f"layer {i} has {w.scales.dtype} scales, X is {X.dtype}")
+
+
+def _check_out(name, t, M, N, dtype):
+    if t is not None and (tuple(t.shape) != (M, N) or t.stride(1) != 1 or t.dtype != dtype):
+        raise ValueError(f"{name} must be [{M}][{N}] of {dtype} with unit column stride")
+
+
 def tiled_ld(K: int) -> int:
     """Words per 16-column tile of a dense tiled qweight with K rows."""
     return (K + 127) // 128 * 256
@@ -83,6 +116,16 @@ class QuantWeight:
         return cls(qweight, scales, qzeros, g_idx, K, N, G, ng, LAYOUT_GPTQ)
 
     def c_struct(self) -> _abi.W4:
+        torch = _torch()
+        for name in ("qweight", "scales", "qzeros", "g_idx"):
+            t = getattr(self, name)
+            if t is None:
+                continue
+            if t.device != self.qweight.device:
+                raise ValueError(f"{name} is on {t.device}, qweight on {self.qweight.device}")
+            want = (torch.float16, torch.bfloat16) if name == "scales" else (torch.int32,)
+            if t.dtype not in want:
+                raise TypeError(f"{name} must be {' or '.join(str(d) for d in want)}, got {t.dtype}")
         for name in ("qweight", "scales", "qzeros"):
             t = getattr(self, name)
             if t.stride(1) != 1:
@@ -229,7 +272,9 @@ def w4a16_gemm(X, w: QuantWeight, path: int, x_perm=None, out=None,
     torch = _torch()
     if X.dim() != 2 or X.stride(1) != 1:
         raise ValueError("X must be 2-D with unit column stride")
+    _check_args(w.device, w.scales.dtype, X=X, x_perm=x_perm, out=out)
     M = X.shape[0]
+    _check_out("out", out, M, w.N, X.dtype)
     if out is None:
         out = torch.empty(M, w.N, dtype=X.dtype, device=X.device)
     cw = w.c_struct()
@@ -249,7 +294,11 @@ def mlp_shard(X, w1: QuantWeight, w2: QuantWeight, path: int, P1=None, y1=None, 
     torch = _torch()
     if X.dim() != 2 or X.stride(1) != 1:
         raise ValueError("X must be 2-D with unit column stride")
+    _check_args(w1.device, w1.scales.dtype, X=X, P1=P1, y1=y1, y2=y2)
+    _check_layers(X, w1, w2)
     M = X.shape[0]
+    _check_out("y1", y1, M, w1.N, X.dtype)
+    _check_out("y2", y2, M, w2.N, X.dtype)
     if y1 is None:
         y1 = torch.empty(M, w1.N, dtype=X.dtype, device=X.device)
     if y2 is None:
@@ -274,7 +323,11 @@ def gated_mlp_shard(X, w_gate: QuantWeight, w_up: QuantWeight, w_down: QuantWeig
     torch = _torch()
     if X.dim() != 2 or X.stride(1) != 1:
         raise ValueError("X must be 2-D with unit column stride")
+    _check_args(w_gate.device, w_gate.scales.dtype, X=X, P1=P1, y1=y1, y2=y2)
+    _check_layers(X, w_gate, w_up, w_down)
     M = X.shape[0]
+    _check_out("y1", y1, M, w_gate.N, X.dtype)
+    _check_out("y2", y2, M, w_down.N, X.dtype)
     if y1 is None:
         y1 = torch.empty(M, w_gate.N, dtype=X.dtype, device=X.device)
     if y2 is None:

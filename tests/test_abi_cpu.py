@@ -192,3 +192,29 @@ def test_gated_mlp_validation(lib):
     for M in (1, 16, 64, 200):
         n = lib.tpdq_workspace_bytes(_abi.OP_GATED_MLP, M, ctypes.byref(wg), ctypes.byref(wd))
         assert n > 0 and n % 256 == 0
+
+
+def test_binding_rejects_host_tensors_and_mismatches():
+    """The Python binding checks devices, element types and output shapes
+    before any library call, so host pointers never reach the C ABI."""
+    import torch
+    import paper_2402_04925_amd as tpdq
+    K, N, G = 256, 64, 32
+    q = torch.zeros(K // 8, N, dtype=torch.int32)
+    s = torch.zeros(K // G, N, dtype=torch.float16)
+    z = torch.zeros(K // G, N // 8, dtype=torch.int32)
+    w = tpdq.QuantWeight(q, s, z, None, K, N, G, K // G)
+    X = torch.zeros(4, K, dtype=torch.float16)
+    with pytest.raises(ValueError, match="GPU"):
+        tpdq.w4a16_gemm(X, w, tpdq.PATH_ORDERED)
+    with pytest.raises(ValueError, match="GPU"):
+        tpdq.mlp_shard(X, w, w, tpdq.PATH_ORDERED)
+    with pytest.raises(TypeError):
+        tpdq.QuantWeight(q.to(torch.int64), s, z, None, K, N, G, K // G).c_struct()
+    with pytest.raises(TypeError):
+        tpdq.QuantWeight(q, s.to(torch.float32), z, None, K, N, G, K // G).c_struct()
+    with pytest.raises(ValueError, match="out must be"):
+        tpdq._check_out("out", torch.zeros(4, N + 8, dtype=torch.float16), 4, N, torch.float16)
+    wb = tpdq.QuantWeight(q, s.to(torch.bfloat16), z, None, K, N, G, K // G)
+    with pytest.raises(TypeError, match="scales"):
+        tpdq._check_layers(X, w, wb)                 # fp16 X, a layer with bf16 scales
