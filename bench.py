@@ -676,7 +676,9 @@ def main():
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--workload", default="llama70b_tp8")
     ap.add_argument("--M", type=int, default=16)
-    ap.add_argument("--sweep", default="1,4,16", help="extra batch sizes reported alongside")
+    ap.add_argument("--sweep", default=None,
+                    help="batch sizes reported alongside (default 1,2,4,8,16,32,64; with "
+                         "--profile-run 1,4,16, the workload's own M set)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-configs", action="store_true",
                     help="skip the Granite-20B TP=4 and Llama-70B TP=1 decode lines")
@@ -705,7 +707,8 @@ def main():
     dev = torch.device("cuda:0")
     wl = inputs.WORKLOADS[args.workload]
     st = Setup(wl, dev)
-    Ms = sorted(set([args.M] + [int(m) for m in args.sweep.split(",") if m]))
+    sweep = args.sweep if args.sweep is not None else ("1,4,16" if args.profile_run else "1,2,4,8,16,32,64")
+    Ms = sorted(set([args.M] + [int(m) for m in sweep.split(",") if m]))
     if args.profile_run:
         profile_run(st, Ms, args.steps, dev)
         return
