@@ -151,7 +151,8 @@ bool plan_decode(int M, int K, int N, int G, int num_groups, int layout, int met
   // workgroups stream
   p->wide = !gated && meta == kMetaGroup && layout == TPDQ_LAYOUT_TILED && a_global(am) &&
             ((int64_t)K * N >= kWideMinWeights ||
-             (am == kAGlobal && mt >= 2 && (int64_t)K * N >= kWideMinWeightsRowMajor));
+             (am == kAGlobal && (mt == 4 || (mt == 2 && K >= N)) &&
+              (int64_t)K * N >= kWideMinWeightsRowMajor));
   p->ks = 1;
   if (p->wide) {
     const int nblk = (K + 127) / 128;

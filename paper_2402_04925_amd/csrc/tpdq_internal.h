@@ -101,9 +101,10 @@ struct DecodePlan {
 // kWideTargetWgs workgroups stream.
 constexpr int kWideWaves = 8;
 constexpr int64_t kWideMinWeights = (int64_t)64 << 20;
-// ... and from 16M elements when X is row-major with two or more row tiles
-// (M > 16): the tile kernel's loads of row-major X then touch 16 rows a row
-// apart per instruction, which the wide kernel's staging avoids
+// ... and from 16M elements when X is row-major with four row tiles
+// (M > 32), or two with K >= N: the tile kernel's loads of row-major X then
+// touch 16 rows a row apart per instruction, which the wide kernel's staging
+// avoids (with two row tiles and K < N the tile kernel stays faster)
 constexpr int64_t kWideMinWeightsRowMajor = (int64_t)16 << 20;
 constexpr int kWideTargetWgs = 200;
 
