@@ -222,7 +222,9 @@ def cpu_detail():
     every decode workload at its largest decode M, with the BLAS thread pool
     at its default size and at one thread, and the tiny single GEMM on both
     paths. One run per item except the tiny GEMM (median of 20); the
-    unsharded Llama-70B shard computes 512 of the 8192 GEMM2 columns."""
+    unsharded Llama-70B shard computes 512 of the 8192 GEMM2 columns. The
+    TP=2 prefill shard (M = 2048) runs once, with the default pool, on 1024
+    of its GEMM2 columns."""
     from threadpoolctl import threadpool_info, threadpool_limits
     from oracle import tpdq_oracle as o
     from paper_2402_04925_amd import inputs
@@ -267,6 +269,22 @@ def cpu_detail():
         out["items"][name] = it
         eprint(f"[bench] oracle on the host, {name} M={M}: {it}")
         del L1, L2
+    # the TP=2 prefill shard once (M = 2048; about 240 GFLOP of float64 GEMM1),
+    # the default pool only, GEMM2 on 1024 of its 8192 columns
+    w = inputs.WORKLOADS["llama70b_tp2_prefill"]
+    L1, L2 = inputs.make_workload(w)
+    M = w.Ms[0]
+    X = inputs.make_x(w, M)
+    P2, _ = o.reorder(L2.g_idx)
+    l1 = (L1.qweight, L1.scales, L1.qzeros, L1.g_idx)
+    l2 = (L2.qweight, L2.scales, L2.qzeros, L2.g_idx)
+    cols = np.arange(0, w.N2, w.N2 // 1024)
+    it = dict(M=M, reorder_us=round(timed(lambda: (o.reorder(L1.g_idx), o.reorder(L2.g_idx))), 1),
+              mlp_shard_us=round(timed(lambda: o.mlp_rank_from_global(X, l1, l2, 0, w.tp, True, P2=P2,
+                                                                      cols2=cols)), 1),
+              gemm2_columns=f"1024 of {w.N2}")
+    out["items"][w.name] = it
+    eprint(f"[bench] oracle on the host, {w.name} M={M}: {it}")
     return out
 
 
