@@ -377,18 +377,19 @@ bool plan_mtile(int M, int64_t ldx, const tpdq_w4* w, int meta, MtilePlan* p) {
   } else {
     // below prefill sizes the weight stream bounds the product; worth it
     // only when the weights are large enough that the decode kernels'
-    // per-workgroup re-reads of X dominate: 64-row tiles, 4 waves (two
-    // workgroups per CU, i.e. two waves per SIMD), K split as far as the
-    // workgroups still fit those kMtileSlots slots in one round (Llama-70B
-    // TP=1 at M = 64: GEMM1 448 workgroups 56.8 -> 51.9 us, GEMM2 512
-    // workgroups 54.9 -> 51.0 us, against about 256 before: one wave per
-    // SIMD left the loads' latency exposed)
+    // per-workgroup re-reads of X dominate: 64 x 512 tiles, 8 waves (two per
+    // SIMD, one workgroup per CU), K split as far as the workgroups still
+    // fit the kMtileSlots CUs in one round. Llama-70B TP=1 at M = 64 (MLP):
+    // 109.5 us with 64 x 256 tiles of 4 waves in 512 slots (two per CU),
+    // 106.3 us here (GEMM2 52.4 -> 48.9 us: 8 waves share one copy of the
+    // activations); more splits than fit one round are slower (8 waves in
+    // 320 slots: GEMM1 280 workgroups, 144 us), and so is one wave per SIMD
     if ((int64_t)K * N < kMtileMinWeights) return false;
     q.rt = 4;
-    q.nw = 4;
+    q.nw = 8;
     q.st = 2;
     const int nblk = (K + 127) / 128;
-    const int tiles = ((M + 63) / 64) * ((N + 255) / 256);
+    const int tiles = ((M + 63) / 64) * ((N + 511) / 512);
     int ks = kMtileSlots / tiles;
     ks = std::max(1, std::min(ks, nblk / 4));
     if ((int64_t)ks * M * N * 4 >= lim) ks = 1;
@@ -430,8 +431,8 @@ hipError_t launch_mtile(const GemmArgs& a0, const MtilePlan& p, float* part, hip
   const bool bf = a.dt == kBF16;
   if (p.rt == 8 && p.nw == 8 && p.st == 2)
     e = bf ? launch_mtile_t<8, 2, 8, kBF16>(a, p.ks, s) : launch_mtile_t<8, 2, 8, kF16>(a, p.ks, s);
-  else if (p.rt == 4 && p.nw == 4 && p.st == 2)
-    e = bf ? launch_mtile_t<4, 2, 4, kBF16>(a, p.ks, s) : launch_mtile_t<4, 2, 4, kF16>(a, p.ks, s);
+  else if (p.rt == 4 && p.nw == 8 && p.st == 2)
+    e = bf ? launch_mtile_t<8, 2, 4, kBF16>(a, p.ks, s) : launch_mtile_t<8, 2, 4, kF16>(a, p.ks, s);
   else
     return hipErrorInvalidValue;
   if (e != hipSuccess || p.ks == 1) return e;

@@ -128,7 +128,7 @@ hipError_t launch_gather_prep(const uint16_t* X, int64_t ldx, int M, int K, cons
 
 // M-tiled MFMA GEMM (gemm_prefill.hip): sorted rows, tiled weights. At
 // M >= kPrefillMinM, 128 x 512 tiles over the whole K; from kMtileMinM rows,
-// on weights of at least kMtileMinWeights elements, 64 x 256 tiles with K
+// on weights of at least kMtileMinWeights elements, 64 x 512 tiles with K
 // split over ks workgroups (fp32 partials in the workspace, summed in split
 // order by a second kernel). Below kMtileMinM rows the decode kernels are
 // faster (measured on the Llama-70B TP=1 shapes: at M = 16 the decode GEMMs
@@ -137,7 +137,7 @@ hipError_t launch_gather_prep(const uint16_t* X, int64_t ldx, int M, int K, cons
 constexpr int kPrefillMinM = 256;
 constexpr int kMtileMinM = 33;
 constexpr int64_t kMtileMinWeights = (int64_t)64 << 20;
-constexpr int kMtileSlots = 512;  // two workgroups per CU on 256 CUs
+constexpr int kMtileSlots = 256;  // one 8-wave workgroup per CU on 256 CUs
 struct MtilePlan {
   int rt, nw, st, ks;  // row tiles and waves per workgroup, LDS stages, K splits
 };
