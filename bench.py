@@ -189,20 +189,20 @@ def cpu_baseline(wl, M, L1, L2, budget_s=20.0):
     P2, _ = o.reorder(L2.g_idx)
     l1 = (L1.qweight, L1.scales, L1.qzeros, L1.g_idx)
     l2 = (L2.qweight, L2.scales, L2.qzeros, L2.g_idx)
+    # one thread: the oracle's dequantization is single-threaded numpy, which
+    # is most of its time, so its BLAS pool is held to one thread as well and
+    # the core count reported is the one it used
+    from threadpoolctl import threadpool_limits
     runs = []
     t_start = time.time()
-    while not runs or (time.time() - t_start < budget_s and len(runs) < 20):
-        t0 = time.perf_counter()
-        o.mlp_rank_from_global(X, l1, l2, 0, wl.tp, True, P2=P2)
-        runs.append(time.perf_counter() - t0)
-    try:
-        from threadpoolctl import threadpool_info
-        cores = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
-    except Exception:
-        cores = os.cpu_count() or 1
-    return dict(value=float(np.median(runs)) * 1e6, unit="us", cores=int(cores), kind="oracle",
+    with threadpool_limits(limits=1):
+        while not runs or (time.time() - t_start < budget_s and len(runs) < 20):
+            t0 = time.perf_counter()
+            o.mlp_rank_from_global(X, l1, l2, 0, wl.tp, True, P2=P2)
+            runs.append(time.perf_counter() - t0)
+    return dict(value=float(np.median(runs)) * 1e6, unit="us", cores=1, kind="oracle",
                 sample=f"{len(runs)} runs of the oracle's rank-0 MLP shard ({wl.name}, M={M}, "
-                       f"ordered, float64 dequant + GEMM), median")
+                       f"ordered, float64 dequant + GEMM, one thread), median")
 
 
 def cpu_model() -> str:

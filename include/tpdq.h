@@ -179,8 +179,8 @@ tpdq_status tpdq_pack_tiled(const tpdq_w4* w, int32_t* qweight_out, void* stream
  * X  [M][ldx] activations (K columns used); X' = X, or X[:, x_perm] when
  *    x_perm (int32 [K], device) is given: column j of X' is column x_perm[j]
  *    of X (the X[:, P1] gather of Alg. 2 and Alg. 3); x_perm values outside
- *    [0, K) are clamped. Alignment 16 B and ldx % 8 == 0 when x_perm is NULL;
- *    2 B otherwise.
+ *    [0, K) are clamped. Alignment 16 B and ldx % 8 == 0 (with or without
+ *    x_perm: rows are read with 16-byte loads).
  * w  the layer; path selects the metadata load (see tpdq_path). The
  *    act-order paths need w->g_idx; values outside [0, num_groups) are
  *    clamped into range (no fault; such rows give unspecified results).
@@ -210,7 +210,8 @@ tpdq_status tpdq_w4a16_gemm(const void* X, int64_t ldx, int32_t M, const int32_t
  *   shard of W1 with its g_idx, w2 the row shard of W2 with its rows' global
  *   g_idx values and the full metadata (num_groups = K2_global/G); P1 must be
  *   NULL.
- * Requirements: w2->K == w1->N. X [M][ldx] with w1->K columns used.
+ * Requirements: w2->K == w1->N. X [M][ldx] with w1->K columns used, 16-byte
+ * aligned, ldx % 8 == 0 (on every path).
  * Y1 [M][w1->N] and Y2_partial [M][w2->N], dense, written in the activation
  * dtype; Y2_partial is this rank's summand of the AllReduce(SUM) of Alg. 3.
  * Workspace: tpdq_workspace_bytes(2, M, w1, w2) bytes, any content.

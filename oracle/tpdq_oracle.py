@@ -79,63 +79,6 @@ def pack_cols(z: np.ndarray) -> np.ndarray:
     return w.view(np.int32)
 
 
-def tiled_ld(K: int) -> int:
-    return (K + 127) // 128 * 256
-
-
-def _tiled_nibble_shifts():
-    """Bit position, in a tiled word, of the code of row 8 r + i: even rows in
-    the low half-word, odd rows in the high one (i // 2 nibbles up)."""
-    return [4 * (i // 2) + 16 * (i % 2) for i in range(8)]
-
-
-def interleave_word(w: np.ndarray) -> np.ndarray:
-    """GPTQ words (row 8 r + i at bits 4 i) -> the tiled nibble order."""
-    w = np.asarray(w).view(np.uint32)
-    out = np.zeros_like(w)
-    for i, sh in enumerate(_tiled_nibble_shifts()):
-        out |= ((w >> np.uint32(4 * i)) & np.uint32(0xF)) << np.uint32(sh)
-    return out
-
-
-def deinterleave_word(w: np.ndarray) -> np.ndarray:
-    """Inverse of interleave_word."""
-    w = np.asarray(w).view(np.uint32)
-    out = np.zeros_like(w)
-    for i, sh in enumerate(_tiled_nibble_shifts()):
-        out |= ((w >> np.uint32(sh)) & np.uint32(0xF)) << np.uint32(4 * i)
-    return out
-
-
-def untile(qt: np.ndarray, K: int, N: int) -> np.ndarray:
-    """GPTQ words [K/8][N] of a qweight stored in the tiled order: for tile t
-    (16 columns), block b (128 rows), lane l = 16 kq + j and step u,
-    tiled[t][256 b + 4 l + u] is GPTQ word [4 (4 b + u) + kq][16 t + j] with
-    its codes interleaved (interleave_word)."""
-    qt = np.asarray(qt).view(np.uint32)
-    r = np.arange(K // 8)[:, None]
-    c = np.arange(N)[None, :]
-    s, kq = r // 4, r % 4
-    b, u = s // 4, s % 4
-    t, jj = c // 16, c % 16
-    return deinterleave_word(qt[t, 256 * b + 4 * (16 * kq + jj) + u]).view(np.int32)
-
-
-def tile(qw: np.ndarray) -> np.ndarray:
-    """Inverse of untile, with zero padding past K and N."""
-    qw = np.asarray(qw).view(np.uint32)
-    kw, N = qw.shape
-    K = kw * 8
-    out = np.zeros(((N + 15) // 16, tiled_ld(K)), dtype=np.uint32)
-    r = np.arange(kw)[:, None]
-    c = np.arange(N)[None, :]
-    s, kq = r // 4, r % 4
-    b, u = s // 4, s % 4
-    t, jj = c // 16, c % 16
-    out[t, 256 * b + 4 * (16 * kq + jj) + u] = interleave_word(qw)
-    return out.view(np.int32)
-
-
 # ----------------------------------------------------------------------------
 # Group index arrays (section 1.1, Eq. 1-3) and the reorder (section 2.1, Alg. 1)
 # ----------------------------------------------------------------------------
@@ -455,21 +398,24 @@ def gated_mlp_tp_aware_rank(X, P1, gate_f, up_f, down_f, G, acc="f64", y1_fp16=T
 
 
 def gated_rank_from_global(X, lg, lu, l2, rank, tp, ordered, P2=None, cols2=None, acc="f64",
-                           dtype="fp16"):
+                           dtype="fp16", y1_round=True, round_y2=True):
     """One rank's (Y1, Y2 partial[:, cols2]) of the gated MLP from the
     unpermuted global layers lg, lu = (qweight, scales, qzeros, g_idx) with a
     shared g_idx, and l2; column block `rank` of gate and up (original columns
-    P2[block] when ordered), as in mlp_rank_from_global."""
+    P2[block] when ordered), as in mlp_rank_from_global. y1_round / round_y2
+    False keep Y1 / Y2 in float64."""
     N1 = np.asarray(lg[0]).shape[1]
     n = N1 // tp
     blk = np.arange(rank * n, (rank + 1) * n)
     sel = np.asarray(P2, dtype=np.int64)[blk] if ordered else blk
     yg = matmul(X, dequant(*lg, cols=sel), acc)
     yu = matmul(X, dequant(*lu, cols=sel), acc)
-    Y1 = round_to(silu(yg) * yu, dtype)
+    Y1 = silu(yg) * yu
+    if y1_round:
+        Y1 = round_to(Y1, dtype)
     W2 = dequant(*l2, cols=cols2)[sel]
-    Y2 = round_to(matmul(Y1, W2, acc), dtype)
-    return Y1, Y2
+    Y2 = matmul(Y1, W2, acc)
+    return Y1, (round_to(Y2, dtype) if round_y2 else Y2)
 
 
 def fold_sample(qweight, P_row, P_col, rows, cols):
@@ -485,7 +431,7 @@ def fold_sample(qweight, P_row, P_col, rows, cols):
 
 
 def mlp_rank_from_global(X, l1, l2, rank, tp, ordered, P2=None, cols2=None, acc="f64",
-                         dtype="fp16"):
+                         dtype="fp16", y1_round=True, round_y2=True):
     """One rank's (Y1, Y2 partial[:, cols2]) computed from the unpermuted
     global layers l1 = (qweight, scales, qzeros, g_idx) and l2.
 
@@ -495,15 +441,18 @@ def mlp_rank_from_global(X, l1, l2, rank, tp, ordered, P2=None, cols2=None, acc=
     P2[block] with rows relabelled by P1, and its W2[P2] row block holds
     original rows P2[block]; since relabelling the rows of W1 together with
     the columns of X (X[:, P1]) leaves every dot product's terms unchanged, the
-    partial is X @ deq(W1)[:, P2[block]] then @ deq(W2)[P2[block], :]."""
+    partial is X @ deq(W1)[:, P2[block]] then @ deq(W2)[P2[block], :].
+    y1_round / round_y2 False keep Y1 / Y2 in float64."""
     N1 = np.asarray(l1[0]).shape[1]
     n = N1 // tp
     blk = np.arange(rank * n, (rank + 1) * n)
     sel = np.asarray(P2, dtype=np.int64)[blk] if ordered else blk
-    Y1 = round_to(matmul(X, dequant(*l1, cols=sel), acc), dtype)
+    Y1 = matmul(X, dequant(*l1, cols=sel), acc)
+    if y1_round:
+        Y1 = round_to(Y1, dtype)
     W2 = dequant(*l2, cols=cols2)[sel]
-    Y2 = round_to(matmul(Y1, W2, acc), dtype)
-    return Y1, Y2
+    Y2 = matmul(Y1, W2, acc)
+    return Y1, (round_to(Y2, dtype) if round_y2 else Y2)
 
 
 # ----------------------------------------------------------------------------

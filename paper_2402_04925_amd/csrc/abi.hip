@@ -448,11 +448,10 @@ tpdq_status tpdq_w4a16_gemm(const void* X, int64_t ldx, int32_t M, const int32_t
   if (ldx < w->K || ldy < w->N)
     return fail(TPDQ_ERR_SHAPE, "ldx=%lld < K=%d or ldy=%lld < N=%d", (long long)ldx, w->K,
                 (long long)ldy, w->N);
-  if (x_perm) {
-    if (!aligned(X, 2)) return fail(TPDQ_ERR_ALIGN, "X needs 2-byte alignment");
-  } else if (!aligned(X, 16) || ldx % 8) {
+  // every path reads X (gathered or not) with 16-byte vector loads of row m at
+  // column 8r
+  if (!aligned(X, 16) || ldx % 8)
     return fail(TPDQ_ERR_ALIGN, "X needs 16-byte alignment and ldx %% 8 == 0");
-  }
   if (!aligned(Y, 8) || ldy % 4) return fail(TPDQ_ERR_ALIGN, "Y needs 8-byte alignment, ldy %% 4 == 0");
   // a call that uses a workspace (a gather always does) takes the documented
   // tpdq_workspace_bytes(1, ...), an upper bound of what it uses
@@ -482,12 +481,8 @@ tpdq_status tpdq_mlp_shard(const void* X, int64_t ldx, int32_t M, const int32_t*
   if (act && P1) return fail(TPDQ_ERR_SHAPE, "the act-order paths take no P1");
   if (!act && !P1) return fail(TPDQ_ERR_NULL, "the ordered path needs P1");
   if (ldx < w1->K) return fail(TPDQ_ERR_SHAPE, "ldx=%lld < K1=%d", (long long)ldx, w1->K);
-  if (act) {
-    if (!aligned(X, 16) || ldx % 8)
-      return fail(TPDQ_ERR_ALIGN, "X needs 16-byte alignment and ldx %% 8 == 0");
-  } else if (!aligned(X, 2)) {
-    return fail(TPDQ_ERR_ALIGN, "X needs 2-byte alignment");
-  }
+  if (!aligned(X, 16) || ldx % 8)
+    return fail(TPDQ_ERR_ALIGN, "X needs 16-byte alignment and ldx %% 8 == 0");
   if (!aligned(Y1, 16) || !aligned(Y2_partial, 8))
     return fail(TPDQ_ERR_ALIGN, "Y1 needs 16-byte and Y2_partial 8-byte alignment");
   const int meta = meta_mode(path);
@@ -541,12 +536,8 @@ tpdq_status tpdq_gated_mlp_shard(const void* X, int64_t ldx, int32_t M, const in
   if (act && P1) return fail(TPDQ_ERR_SHAPE, "the act-order paths take no P1");
   if (!act && !P1) return fail(TPDQ_ERR_NULL, "the ordered path needs P1");
   if (ldx < w_gate->K) return fail(TPDQ_ERR_SHAPE, "ldx=%lld < K1=%d", (long long)ldx, w_gate->K);
-  if (act) {
-    if (!aligned(X, 16) || ldx % 8)
-      return fail(TPDQ_ERR_ALIGN, "X needs 16-byte alignment and ldx %% 8 == 0");
-  } else if (!aligned(X, 2)) {
-    return fail(TPDQ_ERR_ALIGN, "X needs 2-byte alignment");
-  }
+  if (!aligned(X, 16) || ldx % 8)
+    return fail(TPDQ_ERR_ALIGN, "X needs 16-byte alignment and ldx %% 8 == 0");
   if (!aligned(Y1, 16) || !aligned(Y2_partial, 8))
     return fail(TPDQ_ERR_ALIGN, "Y1 needs 16-byte and Y2_partial 8-byte alignment");
   const int meta = meta_mode(path);

@@ -356,45 +356,129 @@ def pin_distinct_groups(o, seed=13):
     assert np.all(o.distinct_groups_per_tile(gs, T) == 1)
 
 
-def pin_tiled_layout(o):
-    """The tiled storage order, walked lane by lane: for K = 256, N = 32 and
-    random codes q[k][n] (packed by pack_rows), the word a lane finds at
-    tiled[t][256 b + 4 l + u] covers rows 8 (4 (4 b + u) + l // 16) .. +7 of
-    column 16 t + l % 16, and the code of row 8 r + i sits at bits
-    4 (i // 2) + 16 (i % 2); so the 16-bit masks the unpack uses
-    (0x000F000F and 0x00F000F0, on the word and on the word >> 8) pick two
-    consecutive rows each, low half first. The round trip is the identity
-    for a ragged shape (padding is zero)."""
-    K, N = 256, 32
-    q = np.random.default_rng(5).integers(0, 16, size=(K, N))
-    qt = o.tile(o.pack_rows(q)).view(np.uint32)
-    assert qt.shape == (2, 512)
-    for t in range(2):
-        for b in range(2):
-            for lane in range(64):
-                for u in range(4):
-                    r = 4 * (4 * b + u) + lane // 16
-                    col = 16 * t + lane % 16
-                    w = int(qt[t, 256 * b + 4 * lane + u])
-                    for i in range(8):
-                        assert (w >> (4 * (i // 2) + 16 * (i % 2))) & 0xF == q[8 * r + i, col]
-                    pairs = [(w & 0x000F000F), (w & 0x00F000F0) >> 4,
-                             ((w >> 8) & 0x000F000F), ((w >> 8) & 0x00F000F0) >> 4]
-                    for p_, v in enumerate(pairs):
-                        assert v & 0xF == q[8 * r + 2 * p_, col]
-                        assert (v >> 16) & 0xF == q[8 * r + 2 * p_ + 1, col]
-    assert np.array_equal(o.untile(qt, K, N), o.pack_rows(q))
-    w1, _ = inputs.make_custom(160, 24, 0, 32, 14)          # K % 128 != 0, N % 16 != 0
-    qt2 = o.tile(w1.qweight)
-    assert qt2.shape == (2, 512)
-    assert np.array_equal(o.untile(qt2, 160, 24), w1.qweight)
-    used = np.zeros(qt2.shape, bool)
-    r = np.arange(20)[:, None]
-    c = np.arange(24)[None, :]
-    used[c // 16, 256 * ((r // 4) // 4) + 4 * (16 * (r % 4) + c % 16) + (r // 4) % 4] = True
-    assert np.all(qt2.view(np.uint32)[~used] == 0)
+
+# ------------------------------------------------ full-size checkers ---
+# The GPU tests at full size cannot build W1[P1, P2] on the host in reasonable
+# time, so their expected values come from helpers that read the unpermuted
+# global layers (mlp_rank_from_global, gated_rank_from_global, fold_sample).
+# These pins tie each helper to the step-by-step construction it shortcuts.
+
+def _close(a, b, tol=1e-12):
+    a = np.asarray(a, dtype=np.float64)
+    b = np.asarray(b, dtype=np.float64)
+    assert a.shape == b.shape, (a.shape, b.shape)
+    assert np.max(np.abs(a - b)) <= tol * max(1e-300, np.max(np.abs(b))), np.max(np.abs(a - b))
 
 
+def _glob(L):
+    return L.qweight, L.scales, L.qzeros, L.g_idx
+
+
+def pin_rank_from_global(o, seed=27, tps=(1, 2, 4, 8)):
+    """mlp_rank_from_global against the step-by-step Alg. 3 rank (fold, then
+    the column shard of W1[P1, P2] and the row shard of W2[P2], X[:, P1]) and
+    against the act-order rank (Megatron shards of the unpermuted layers, W2's
+    shard with its rows' global g_idx and all the metadata), for every rank
+    and TP degree, in float64 to 1e-12; a subset of Y2's columns equals those
+    columns of the full result; the ranks sum to the unsharded MLP; with the
+    fp16 roundings on, within 2e-3 of the step-by-step rank."""
+    K1, N1, N2, G = 256, 512, 128, 32
+    w1, w2, d1, d2, X = _mlp_case(K1, N1, N2, G, seed)
+    l1, l2 = _glob(w1), _glob(w2)
+    P1, _ = o.reorder(w1.g_idx)
+    P2, _ = o.reorder(w2.g_idx)
+    w1f, w2f = o.fold(d1, d2, P1, P2)
+    ref = o.w4a16_gemm(o.w4a16_gemm(X, *_l(d1, w1.g_idx), round_fp16=False),
+                       *_l(d2, w2.g_idx), round_fp16=False)
+    cols = np.array([0, 5, 77, N2 - 1])
+    f64 = dict(y1_round=False, round_y2=False)
+    for tp in tps:
+        n = N1 // tp
+        tot_o = np.zeros_like(ref)
+        tot_a = np.zeros_like(ref)
+        for r in range(tp):
+            y1, y2 = o.mlp_rank_from_global(X, l1, l2, r, tp, True, P2=P2, **f64)
+            e1, e2 = o.mlp_tp_aware_rank(X, P1, o.column_shard(w1f, r, tp), o.row_shard(w2f, r, tp, G),
+                                         G, y1_fp16=False, round_y2=False)
+            _close(y1, e1)
+            _close(y2, e2)
+            a1, a2 = o.mlp_rank_from_global(X, l1, l2, r, tp, False, P2=P2, **f64)
+            f1, f2 = o.mlp_actorder_rank(X, o.column_shard(d1, r, tp), w1.g_idx,
+                                         o.row_shard(d2, r, tp, G, keep_all_groups=True),
+                                         w2.g_idx[r * n:(r + 1) * n], y1_fp16=False, round_y2=False)
+            _close(a1, f1)
+            _close(a2, f2)
+            _, c2 = o.mlp_rank_from_global(X, l1, l2, r, tp, True, P2=P2, cols2=cols, **f64)
+            _close(c2, y2[:, cols])
+            h1, h2 = o.mlp_rank_from_global(X, l1, l2, r, tp, True, P2=P2)
+            g1, g2 = o.mlp_tp_aware_rank(X, P1, o.column_shard(w1f, r, tp), o.row_shard(w2f, r, tp, G), G)
+            assert h1.dtype == np.float16 and h2.dtype == np.float16
+            assert o.rel_err(h1, g1) <= 2e-3 and o.rel_err(h2, g2) <= 2e-3, (tp, r)
+            tot_o += y2
+            tot_a += a2
+        _close(tot_o, ref)
+        _close(tot_a, ref)
+
+
+def pin_gated_rank_from_global(o, seed=28, tps=(1, 2, 4)):
+    """gated_rank_from_global against the step-by-step gated Alg. 3 rank
+    (gate and up folded with W[P1, P2], down with W[P2], column and row
+    shards) and against the act-order gated rank built from the pinned
+    gated_y1 and GEMM on Megatron shards of the unpermuted layers, every rank,
+    float64 to 1e-12; the ranks sum to the unsharded gated MLP."""
+    gate, up, down, dg, du, dd, X, G = _gated_case(seed)
+    lg, lu, l2 = _glob(gate), _glob(up), _glob(down)
+    P1, _ = o.reorder(gate.g_idx)
+    P2, _ = o.reorder(down.g_idx)
+    gf, df = o.fold(dg, dd, P1, P2)
+    uf, _ = o.fold(du, None, P1, P2)
+    ref = o.w4a16_gemm(o.gated_y1(X, o._triple(dg), o._triple(du), gate.g_idx, round_fp16=False),
+                       *o._triple(dd), down.g_idx, round_fp16=False)
+    f64 = dict(y1_round=False, round_y2=False)
+    N1 = gate.N
+    for tp in tps:
+        n = N1 // tp
+        tot = np.zeros_like(ref)
+        for r in range(tp):
+            y1, y2 = o.gated_rank_from_global(X, lg, lu, l2, r, tp, True, P2=P2, **f64)
+            e1, e2 = o.gated_mlp_tp_aware_rank(X, P1, o.column_shard(gf, r, tp), o.column_shard(uf, r, tp),
+                                               o.row_shard(df, r, tp, G), G, y1_fp16=False,
+                                               round_y2=False)
+            _close(y1, e1)
+            _close(y2, e2)
+            a1, a2 = o.gated_rank_from_global(X, lg, lu, l2, r, tp, False, P2=P2, **f64)
+            f1 = o.gated_y1(X, o._triple(o.column_shard(dg, r, tp)), o._triple(o.column_shard(du, r, tp)),
+                            gate.g_idx, round_fp16=False)
+            f2 = o.w4a16_gemm(f1, *o._triple(o.row_shard(dd, r, tp, G, keep_all_groups=True)),
+                              down.g_idx[r * n:(r + 1) * n], round_fp16=False)
+            _close(a1, f1)
+            _close(a2, f2)
+            tot += y2
+        _close(tot, ref)
+
+
+def pin_fold_sample(o, seed=29):
+    """fold_sample (codes of W[P_row, P_col] read from the source words one
+    by one) against the codes of the folded and the row-permuted layer, on
+    every row and column of a tiny layer, and against the hex spelling of the
+    source words on a few elements."""
+    K, N, G = 64, 24, 16
+    w1, _ = inputs.make_custom(K, N, 0, G, seed)
+    d = dict(qweight=w1.qweight, scales=w1.scales, qzeros=w1.qzeros)
+    rng = np.random.default_rng(seed)
+    Pr, Pc = rng.permutation(K), rng.permutation(N)
+    rows, cols = np.arange(K), np.arange(N)
+    full = o.unpack_rows(o.fold(d, None, Pr, Pc)[0]["qweight"])
+    assert np.array_equal(o.fold_sample(w1.qweight, Pr, Pc, rows, cols), full)
+    perm_only = o.unpack_rows(o.permute_rows(d, Pr)["qweight"])
+    assert np.array_equal(o.fold_sample(w1.qweight, Pr, None, rows, cols), perm_only)
+    sr, sc = np.array([3, 17, 40, 63]), np.array([0, 9, 23])
+    got = o.fold_sample(w1.qweight, Pr, Pc, sr, sc)
+    words = w1.qweight.view(np.uint32)
+    for a, r in enumerate(sr):
+        for b, c in enumerate(sc):
+            src_r, src_c = int(Pr[r]), int(Pc[c])
+            assert got[a, b] == nibble_by_hex(int(words[src_r // 8, src_c]), src_r % 8)
 
 # ------------------------------------------------------------- bfloat16 ---
 
@@ -538,6 +622,7 @@ ALL_PINS = [
     pin_reorder_closed_form, pin_identity_phi, pin_check_groups, pin_golden_gemm,
     pin_gemm_bruteforce, pin_one_hot_rows, pin_special_cases, pin_ordered_equals_actorder,
     pin_tp_aware_mlp, pin_actorder_shard_mlp, pin_alg2_equals_alg3, pin_fold_elementwise,
-    pin_distinct_groups, pin_tiled_layout, pin_bf16_rounding, pin_bf16_gemm, pin_silu,
+    pin_distinct_groups, pin_bf16_rounding, pin_bf16_gemm, pin_silu,
     pin_gated_tp_aware_mlp, pin_gated_special_cases, pin_gated_bruteforce,
+    pin_rank_from_global, pin_gated_rank_from_global, pin_fold_sample,
 ]

@@ -73,6 +73,9 @@ def test_gemm_validation(lib):
     assert gemm(lib, w, ldx=128) == _abi.ERR_SHAPE                          # ldx < K
     assert gemm(lib, w, X=(1 << 24) + 2) == _abi.ERR_ALIGN                  # X 16-B
     assert gemm(lib, w, ldx=260) == _abi.ERR_ALIGN                          # ldx % 8
+    # the gather path reads rows of X with 16-byte loads too
+    assert gemm(lib, w, X=(1 << 24) + 2, perm=1 << 27, ws=1 << 26, ws_bytes=1 << 26) == _abi.ERR_ALIGN
+    assert gemm(lib, w, ldx=260, perm=1 << 27, ws=1 << 26, ws_bytes=1 << 26) == _abi.ERR_ALIGN
     assert gemm(lib, w, Y=(1 << 25) + 4) == _abi.ERR_ALIGN                  # Y 8-B
     bad = fake_layer()
     bad.qweight += 4
@@ -108,6 +111,11 @@ def test_mlp_validation(lib):
     assert f(w1, w2, P1=None) == _abi.ERR_NULL                                # ordered needs P1
     assert f(w1, w2, path=_abi.PATH_ACTORDER) == _abi.ERR_SHAPE               # act-order takes no P1
     assert f(w1, w2) == _abi.ERR_WORKSPACE
+    for path, P1 in ((_abi.PATH_ORDERED, 1 << 27), (_abi.PATH_ACTORDER, None)):
+        g = lambda X, ldx: lib.tpdq_mlp_shard(X, ldx, 4, P1, ctypes.byref(w1), ctypes.byref(w2), path,
+                                              _abi.FP16, 1 << 25, 1 << 26, 1 << 27, 1 << 26, None)
+        assert g((1 << 24) + 2, 256) == _abi.ERR_ALIGN                       # X 16-B, both paths
+        assert g(1 << 24, 260) == _abi.ERR_ALIGN                             # ldx % 8, both paths
 
 
 @needs_no_gpu

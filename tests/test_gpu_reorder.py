@@ -5,6 +5,7 @@ import pytest
 
 from oracle import tpdq_oracle as o
 from paper_2402_04925_amd import inputs
+from tests import tiled_codec as tc
 from tests.gpu_util import layer_to_dev, log, np_of, torch_dev
 
 pytestmark = pytest.mark.gpu
@@ -18,7 +19,7 @@ def words_of(w):
     """GPTQ words of a device QuantWeight, whatever its layout."""
     import paper_2402_04925_amd as tpdq
     q = np_of(w.qweight)
-    return o.untile(q, w.K, w.N) if w.layout == tpdq.LAYOUT_TILED else q
+    return tc.untile(q, w.K, w.N) if w.layout == tpdq.LAYOUT_TILED else q
 
 
 @pytest.mark.parametrize("K1,N1,N2,G,seed", [
@@ -45,8 +46,8 @@ def test_reorder_pair_exact(K1, N1, N2, G, seed, layout):
     assert np.array_equal(np_of(w1o.qzeros), f1["qzeros"])
     assert np.array_equal(words_of(w2o), f2["qweight"])
     if layout == "tiled":   # the padding past K and N is zero
-        assert np.array_equal(np_of(w1o.qweight), o.tile(f1["qweight"]))
-        assert np.array_equal(np_of(w2o.qweight), o.tile(f2["qweight"]))
+        assert np.array_equal(np_of(w1o.qweight), tc.tile(f1["qweight"]))
+        assert np.array_equal(np_of(w2o.qweight), tc.tile(f2["qweight"]))
 
 
 @pytest.mark.parametrize("K,N,seed", [(256, 64, 1), (160, 24, 2), (1024, 1000, 3)])
@@ -57,7 +58,7 @@ def test_pack_tiled_exact(K, N, seed):
     w1, _ = inputs.make_custom(K, N, 0, 32, seed)
     wt = tpdq.pack_tiled(layer_to_dev(w1, dev))
     torch.cuda.synchronize()
-    assert np.array_equal(np_of(wt.qweight), o.tile(w1.qweight))
+    assert np.array_equal(np_of(wt.qweight), tc.tile(w1.qweight))
 
 
 @pytest.mark.parametrize("K,N,G,seed", [(256, 128, 32, 7), (1024, 96, 128, 8), (40, 16, 8, 9)])
@@ -148,10 +149,10 @@ def test_reorder_full_size(name):
     _, _, _, _, w1t, w2t = tpdq.reorder(d1, d2, layout=tpdq.LAYOUT_TILED)
     torch.cuda.synchronize()
     for t in (0, 7, w.N1 // 16 - 1):
-        got = o.untile(np_of(w1t.qweight[t:t + 1]), w.K1, 16)
+        got = tc.untile(np_of(w1t.qweight[t:t + 1]), w.K1, 16)
         exp = o.fold_sample(w1.qweight, eP1, eP2, np.arange(w.K1), np.arange(16 * t, 16 * t + 16))
         assert np.array_equal(o.unpack_rows(got), exp), t
     for t in (0, w.N2 // 16 - 1):
-        got = o.untile(np_of(w2t.qweight[t:t + 1]), w.K2, 16)
+        got = tc.untile(np_of(w2t.qweight[t:t + 1]), w.K2, 16)
         exp = o.fold_sample(w2.qweight, eP2, None, np.arange(w.K2), np.arange(16 * t, 16 * t + 16))
         assert np.array_equal(o.unpack_rows(got), exp), t

@@ -120,6 +120,68 @@ def _gated_silu_on_up(X, gate, up, g_idx, x_perm=None, acc="f64", cols=None, rou
     return _orig["gated_y1"](X, up, gate, g_idx, x_perm, acc, cols, round_fp16, dtype)
 
 
+def _rank_mutant(kind, gated):
+    """mlp_rank_from_global / gated_rank_from_global with one planted mistake:
+    'blk' the unpermuted column block on the ordered path, 'inv' P2's inverse
+    in place of P2, 'w2cols' the selection applied to W2's columns instead of
+    its rows (W2's rows then taken in block order)."""
+    def f(X, l1, *rest, **kw):
+        if gated:
+            lu, l2, rank, tp, ordered = rest[0], rest[1], rest[2], rest[3], rest[4]
+        else:
+            l2, rank, tp, ordered = rest[0], rest[1], rest[2], rest[3]
+        P2 = kw.get("P2")
+        cols2 = kw.get("cols2")
+        acc = kw.get("acc", "f64")
+        dtype = kw.get("dtype", "fp16")
+        y1_round = kw.get("y1_round", True)
+        round_y2 = kw.get("round_y2", True)
+        N1 = np.asarray(l1[0]).shape[1]
+        n = N1 // tp
+        blk = np.arange(rank * n, (rank + 1) * n)
+        P2 = np.asarray(P2, dtype=np.int64)
+        if kind == "inv":
+            inv = np.empty_like(P2)
+            inv[P2] = np.arange(len(P2))
+            P2 = inv
+        sel = P2[blk] if (ordered and kind != "blk") else blk
+        if gated:
+            Y1 = o.silu(o.matmul(X, o.dequant(*l1, cols=sel), acc)) * o.matmul(X, o.dequant(*lu, cols=sel), acc)
+        else:
+            Y1 = o.matmul(X, o.dequant(*l1, cols=sel), acc)
+        if y1_round:
+            Y1 = o.round_to(Y1, dtype)
+        if kind == "w2cols":
+            W2 = o.dequant(*l2, cols=cols2)[blk]  # W2's rows in block order
+        else:
+            W2 = o.dequant(*l2, cols=cols2)[sel]
+        Y2 = o.matmul(Y1, W2, acc)
+        return Y1, (o.round_to(Y2, dtype) if round_y2 else Y2)
+    return f
+
+
+def _fold_sample_unpermuted_rows(qweight, P_row, P_col, rows, cols):
+    return _orig["fold_sample"](qweight, np.arange(len(P_row)), P_col, rows, cols)
+
+
+def _fold_sample_shift(qweight, P_row, P_col, rows, cols):
+    src_rows = np.asarray(P_row, dtype=np.int64)[np.asarray(rows, dtype=np.int64)]
+    cols = np.asarray(cols, dtype=np.int64)
+    src_cols = cols if P_col is None else np.asarray(P_col, dtype=np.int64)[cols]
+    words = np.asarray(qweight).view(np.uint32)[np.ix_(src_rows // 8, src_cols)]
+    shift = (4 * (7 - src_rows % 8)).astype(np.uint32)[:, None]
+    return ((words >> shift) & np.uint32(0xF)).astype(np.int64)
+
+
+def _fold_sample_inverse_cols(qweight, P_row, P_col, rows, cols):
+    if P_col is not None:
+        P_col = np.asarray(P_col, dtype=np.int64)
+        inv = np.empty_like(P_col)
+        inv[P_col] = np.arange(len(P_col))
+        P_col = inv
+    return _orig["fold_sample"](qweight, P_row, P_col, rows, cols)
+
+
 MUTANTS = {
     "unpack_rows": _unpack_rows_reversed,
     "unpack_cols": _unpack_cols_reversed,
@@ -139,6 +201,15 @@ MUTANTS = {
     "round_to:fp16": _round_to_fp16_always,
     "silu:sigmoid": _silu_is_sigmoid,
     "gated_y1:swapped": _gated_silu_on_up,
+    "mlp_rank_from_global:blk": _rank_mutant("blk", False),
+    "mlp_rank_from_global:inverse_P2": _rank_mutant("inv", False),
+    "mlp_rank_from_global:w2_columns": _rank_mutant("w2cols", False),
+    "gated_rank_from_global:blk": _rank_mutant("blk", True),
+    "gated_rank_from_global:inverse_P2": _rank_mutant("inv", True),
+    "gated_rank_from_global:w2_columns": _rank_mutant("w2cols", True),
+    "fold_sample:rows": _fold_sample_unpermuted_rows,
+    "fold_sample:shift": _fold_sample_shift,
+    "fold_sample:inverse_cols": _fold_sample_inverse_cols,
 }
 
 
