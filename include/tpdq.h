@@ -222,6 +222,27 @@ tpdq_status tpdq_mlp_shard(const void* X, int64_t ldx, int32_t M, const int32_t*
                            void* workspace, size_t ws_bytes, void* stream);
 
 /*
+ * tpdq_mlp_shard_noalloc - tpdq_mlp_shard for callers that cannot allocate
+ * device memory (code under HIP graph capture, tight serving loops, harnesses
+ * that forbid hipMalloc): the same computation, kernels and results, without a
+ * workspace argument. The workspace is a static scratch array of 64 MiB that
+ * the library holds on each GPU it runs on until the process ends; this call
+ * never allocates or frees device memory and calls no allocating routine.
+ * Arguments, alignment and results as for tpdq_mlp_shard; the scratch serves
+ * the stream's device. A call whose tpdq_workspace_bytes(2, M, w1, w2) exceeds
+ * 64 MiB returns TPDQ_ERR_WORKSPACE before any device work (every decode and
+ * prefill shape of the paper's workloads fits; e.g. M = 2048 on the Llama-70B
+ * TP = 2 shard uses 32 MiB). The scratch needs no particular content. All
+ * calls on one GPU share its scratch: calls that overlap in time on one GPU
+ * (two streams, two threads) race and must be serialised by the caller. The
+ * first call on a device resolves that device's scratch address (a runtime
+ * symbol lookup, no allocation).
+ */
+tpdq_status tpdq_mlp_shard_noalloc(const void* X, int64_t ldx, int32_t M, const int32_t* P1,
+                                   const tpdq_w4* w1, const tpdq_w4* w2, tpdq_path path,
+                                   tpdq_dtype dtype, void* Y1, void* Y2_partial, void* stream);
+
+/*
  * tpdq_gated_mlp_shard - one rank's share of an MLP with a gate projection,
  * up to its AllReduce: Y1 = silu(X' W_gate) * (X' W_up) (silu(x) =
  * x / (1 + e^-x), both products in fp32, one rounding), Y2_partial = Y1 @

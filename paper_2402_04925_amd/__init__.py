@@ -16,7 +16,8 @@ from ._abi import (BF16, FP16, LAYOUT_GPTQ, LAYOUT_TILED, OP_GATED_MLP, OP_GEMM,
                    PATH_ACTORDER, PATH_ACTORDER_GLOBAL, PATH_ORDERED, TpdqError)
 
 __all__ = [
-    "QuantWeight", "reorder", "pack_tiled", "w4a16_gemm", "mlp_shard", "gated_mlp_shard",
+    "QuantWeight", "reorder", "pack_tiled", "w4a16_gemm", "mlp_shard", "mlp_shard_noalloc",
+    "gated_mlp_shard",
     "workspace_bytes", "Workspace",
     "LAYOUT_GPTQ", "LAYOUT_TILED", "tiled_ld",
     "TpdqError", "PATH_ACTORDER", "PATH_ORDERED", "PATH_ACTORDER_GLOBAL", "FP16", "BF16", "version",
@@ -311,6 +312,29 @@ def mlp_shard(X, w1: QuantWeight, w2: QuantWeight, path: int, P1=None, y1=None, 
         _ptr(X), X.stride(0), M, _ptr(P1), ctypes.byref(c1), ctypes.byref(c2), path,
         _dtype_code(X.dtype), _ptr(y1), _ptr(y2), _ptr(buf), buf.numel(),
         _stream_handle(X.device)))
+    return y1, y2
+
+
+def mlp_shard_noalloc(X, w1: QuantWeight, w2: QuantWeight, path: int, P1=None, y1=None, y2=None):
+    """mlp_shard through tpdq_mlp_shard_noalloc: the library's static scratch
+    instead of a workspace, so the call itself allocates no device memory
+    when y1 and y2 are given. Returns (Y1, Y2_partial)."""
+    torch = _torch()
+    if X.dim() != 2 or X.stride(1) != 1:
+        raise ValueError("X must be 2-D with unit column stride")
+    _check_args(w1.device, w1.scales.dtype, X=X, P1=P1, y1=y1, y2=y2)
+    _check_layers(X, w1, w2)
+    M = X.shape[0]
+    _check_out("y1", y1, M, w1.N, X.dtype)
+    _check_out("y2", y2, M, w2.N, X.dtype)
+    if y1 is None:
+        y1 = torch.empty(M, w1.N, dtype=X.dtype, device=X.device)
+    if y2 is None:
+        y2 = torch.empty(M, w2.N, dtype=X.dtype, device=X.device)
+    c1, c2 = w1.c_struct(), w2.c_struct()
+    _abi.check(_abi.lib().tpdq_mlp_shard_noalloc(
+        _ptr(X), X.stride(0), M, _ptr(P1), ctypes.byref(c1), ctypes.byref(c2), path,
+        _dtype_code(X.dtype), _ptr(y1), _ptr(y2), _stream_handle(X.device)))
     return y1, y2
 
 

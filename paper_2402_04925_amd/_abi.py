@@ -14,7 +14,8 @@ OP_REORDER, OP_GEMM, OP_MLP, OP_GATED_MLP = 0, 1, 2, 3
 LAYOUT_GPTQ, LAYOUT_TILED = 0, 1
 
 EXPORTED = (
-    "tpdq_reorder", "tpdq_pack_tiled", "tpdq_w4a16_gemm", "tpdq_mlp_shard", "tpdq_gated_mlp_shard",
+    "tpdq_reorder", "tpdq_pack_tiled", "tpdq_w4a16_gemm", "tpdq_mlp_shard", "tpdq_mlp_shard_noalloc",
+    "tpdq_gated_mlp_shard",
     "tpdq_workspace_bytes",
     "tpdq_status_string", "tpdq_last_error", "tpdq_version",
 )
@@ -51,6 +52,9 @@ def _declare(lib):
     lib.tpdq_mlp_shard.argtypes = [vp, i64, i32, vp, pw, pw, ctypes.c_int, ctypes.c_int, vp, vp, vp,
                                    sz, vp]
     lib.tpdq_mlp_shard.restype = ctypes.c_int
+    lib.tpdq_mlp_shard_noalloc.argtypes = [vp, i64, i32, vp, pw, pw, ctypes.c_int, ctypes.c_int, vp,
+                                           vp, vp]
+    lib.tpdq_mlp_shard_noalloc.restype = ctypes.c_int
     lib.tpdq_gated_mlp_shard.argtypes = [vp, i64, i32, vp, pw, pw, pw, ctypes.c_int, ctypes.c_int, vp,
                                          vp, vp, sz, vp]
     lib.tpdq_gated_mlp_shard.restype = ctypes.c_int

@@ -5,11 +5,22 @@
 #include <stdio.h>
 
 #include <algorithm>
+#include <mutex>
 #include <string>
 
 #include "tpdq_internal.h"
 
 using namespace tpdq;
+
+// Scratch of tpdq_mlp_shard_noalloc: a workspace owned by the library for
+// callers that cannot allocate device memory. Every GPU the library runs on
+// holds its own copy from the time the code object is loaded until the
+// process ends. In host code `scratch` is only a stand-in for the symbol:
+// the device address of a GPU's copy comes from hipGetSymbolAddress, taken
+// once per device with that device current (scratch_ptr), and only that
+// address is ever handed to a kernel or a copy.
+constexpr size_t kScratchBytes = (size_t)64 << 20;
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
 
 namespace {
 
@@ -275,6 +286,35 @@ bool mlp_prepared_y1(int M, int64_t ldx, bool perm, const tpdq_w4* w1, const tpd
                      kOperandPrepared, dt, &p3) && !p3.wide;
 }
 
+// The device address of each GPU's copy of `scratch`, taken once per device.
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_dev[kMaxDevices] = {};
+
+// The device address of the scratch copy of the stream's GPU.
+tpdq_status scratch_ptr(hipStream_t stream, void** out) {
+  int dev = -1;
+  hipError_t e = stream ? hipStreamGetDevice(stream, &dev) : hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_fail(e, "device of the stream");
+  if (dev < 0 || dev >= kMaxDevices)
+    return fail(TPDQ_ERR_UNSUPPORTED, "device %d: at most %d devices", dev, kMaxDevices);
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_dev[dev]) {
+    int cur = -1;
+    e = hipGetDevice(&cur);
+    if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+    if (cur != dev && (e = hipSetDevice(dev)) != hipSuccess) return hip_fail(e, "hipSetDevice");
+    void* p = nullptr;
+    const hipError_t es = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (cur != dev && (e = hipSetDevice(cur)) != hipSuccess) return hip_fail(e, "hipSetDevice");
+    if (es != hipSuccess) return hip_fail(es, "hipGetSymbolAddress(scratch)");
+    if (!p) return fail(TPDQ_ERR_HIP, "hipGetSymbolAddress(scratch) gave NULL");
+    g_scratch_dev[dev] = p;
+  }
+  *out = g_scratch_dev[dev];
+  return TPDQ_OK;
+}
+
 tpdq_status check_common(int32_t M, tpdq_path path, tpdq_dtype dtype) {
   if (M < 1) return fail(TPDQ_ERR_SHAPE, "M=%d must be >= 1", M);
   if (path != TPDQ_PATH_ACTORDER && path != TPDQ_PATH_ORDERED && path != TPDQ_PATH_ACTORDER_GLOBAL)
@@ -465,10 +505,17 @@ tpdq_status tpdq_w4a16_gemm(const void* X, int64_t ldx, int32_t M, const int32_t
                   (char*)workspace, (hipStream_t)stream);
 }
 
-tpdq_status tpdq_mlp_shard(const void* X, int64_t ldx, int32_t M, const int32_t* P1,
-                           const tpdq_w4* w1, const tpdq_w4* w2, tpdq_path path, tpdq_dtype dtype,
-                           void* Y1, void* Y2_partial, void* workspace, size_t ws_bytes,
-                           void* stream) {
+}  // extern "C"
+
+namespace {
+
+// tpdq_mlp_shard, with the caller's workspace or (noalloc) the library's
+// scratch: every argument is validated first; the scratch address is taken
+// only after that.
+tpdq_status mlp_shard(const void* X, int64_t ldx, int32_t M, const int32_t* P1, const tpdq_w4* w1,
+                      const tpdq_w4* w2, tpdq_path path, tpdq_dtype dtype, void* Y1,
+                      void* Y2_partial, void* workspace, size_t ws_bytes, void* stream,
+                      bool noalloc) {
   tpdq_status st = check_common(M, path, dtype);
   if (st != TPDQ_OK) return st;
   const bool act = is_actorder(path);
@@ -489,6 +536,15 @@ tpdq_status tpdq_mlp_shard(const void* X, int64_t ldx, int32_t M, const int32_t*
   const size_t bound = tpdq_workspace_bytes(2, M, w1, w2);
   const size_t need = std::max(gemm_ws_need(M, ldx, !act, w1, meta, dtype),
                                gemm_ws_need(M, w1->N, false, w2, meta, dtype));
+  if (noalloc) {
+    if (bound > kScratchBytes)
+      return fail(TPDQ_ERR_WORKSPACE,
+                  "MLP needs %zu bytes of scratch; the library's static scratch holds %zu "
+                  "(use tpdq_mlp_shard with a workspace)", bound, kScratchBytes);
+    st = scratch_ptr((hipStream_t)stream, &workspace);
+    if (st != TPDQ_OK) return st;
+    ws_bytes = kScratchBytes;
+  }
   if ((!act || need) && (!workspace || ws_bytes < bound))
     return fail(TPDQ_ERR_WORKSPACE, "MLP needs %zu workspace bytes, got %zu", bound, ws_bytes);
   if (workspace && !aligned(workspace, 16))
@@ -511,6 +567,24 @@ tpdq_status tpdq_mlp_shard(const void* X, int64_t ldx, int32_t M, const int32_t*
                     io2);
   return run_gemm((const uint16_t*)Y1, w1->N, M, nullptr, w2, path, dtype, (uint16_t*)Y2_partial,
                   w2->N, ws, s);
+}
+
+}  // namespace
+
+extern "C" {
+
+tpdq_status tpdq_mlp_shard(const void* X, int64_t ldx, int32_t M, const int32_t* P1,
+                           const tpdq_w4* w1, const tpdq_w4* w2, tpdq_path path, tpdq_dtype dtype,
+                           void* Y1, void* Y2_partial, void* workspace, size_t ws_bytes,
+                           void* stream) {
+  return mlp_shard(X, ldx, M, P1, w1, w2, path, dtype, Y1, Y2_partial, workspace, ws_bytes, stream,
+                   false);
+}
+
+tpdq_status tpdq_mlp_shard_noalloc(const void* X, int64_t ldx, int32_t M, const int32_t* P1,
+                                   const tpdq_w4* w1, const tpdq_w4* w2, tpdq_path path,
+                                   tpdq_dtype dtype, void* Y1, void* Y2_partial, void* stream) {
+  return mlp_shard(X, ldx, M, P1, w1, w2, path, dtype, Y1, Y2_partial, nullptr, 0, stream, true);
 }
 
 tpdq_status tpdq_gated_mlp_shard(const void* X, int64_t ldx, int32_t M, const int32_t* P1,

@@ -119,6 +119,31 @@ def test_mlp_validation(lib):
 
 
 @needs_no_gpu
+def test_mlp_noalloc_validation(lib):
+    """The no-allocation MLP validates like tpdq_mlp_shard and rejects a shape
+    whose workspace exceeds its 64 MiB scratch, before any device call."""
+    w1 = fake_layer(K=256, N=512)
+    w2 = fake_layer(K=512, N=128, base=1 << 22)
+    w2bad = fake_layer(K=256, N=128, base=1 << 22)
+    f = lambda a, b, M=4, P1=1 << 27, path=_abi.PATH_ORDERED, X=1 << 24, ldx=256: \
+        lib.tpdq_mlp_shard_noalloc(X, ldx, M, P1, ctypes.byref(a), ctypes.byref(b), path, _abi.FP16,
+                                   1 << 25, 1 << 26, None)
+    assert f(w1, w2bad) == _abi.ERR_SHAPE
+    assert f(w1, w2, P1=None) == _abi.ERR_NULL
+    assert f(w1, w2, X=(1 << 24) + 2) == _abi.ERR_ALIGN
+    big1 = fake_layer(K=8192, N=1024, G=128)
+    big1.layout = _abi.LAYOUT_TILED
+    big1.ld_q = 64 * 256
+    big2 = fake_layer(K=1024, N=1024, G=128, base=1 << 22)
+    big2.layout = _abi.LAYOUT_TILED
+    big2.ld_q = 8 * 256
+    need = lib.tpdq_workspace_bytes(_abi.OP_MLP, 8192, ctypes.byref(big1), ctypes.byref(big2))
+    assert need > 64 << 20
+    assert f(big1, big2, M=8192, ldx=8192) == _abi.ERR_WORKSPACE
+    assert b"scratch" in lib.tpdq_last_error()
+
+
+@needs_no_gpu
 def test_reorder_validation(lib):
     w1 = fake_layer(K=256, N=512)
     w2 = fake_layer(K=512, N=128, base=1 << 22)

@@ -1,0 +1,99 @@
+"""tpdq_mlp_shard_noalloc (the library's static scratch instead of a
+workspace) against tpdq_mlp_shard on the same inputs: two calls in a row,
+the second with a smaller input, so the second call runs on scratch that
+holds the first call's contents. Results must be bit-identical (the same
+kernels run on the same data). Runs alone in a fresh process and after the
+other tests."""
+import numpy as np
+import pytest
+
+from oracle import tpdq_oracle as o
+from paper_2402_04925_amd import inputs
+from tests.gpu_util import TOL_FP16, layer_to_dev, log, np_of, to_dev, torch_dev, workload_layers
+
+pytestmark = pytest.mark.gpu
+
+
+def _same(a, b):
+    return np.array_equal(np_of(a).view(np.uint16), np_of(b).view(np.uint16))
+
+
+def _pair(tpdq, X, s1, s2, path, P1):
+    """(workspace call, no-allocation call) outputs on the same inputs."""
+    import torch
+    ref = tpdq.mlp_shard(X, s1, s2, path, P1=P1)
+    got = tpdq.mlp_shard_noalloc(X, s1, s2, path, P1=P1)
+    torch.cuda.synchronize()
+    return ref, got
+
+
+@pytest.mark.parametrize("path", ["ordered", "actorder"])
+def test_noalloc_matches_workspace_call(path):
+    """Llama-70B TP = 8 rank 0 at M = 16 (the prepared operands of X and Y1
+    live in the scratch), then a smaller layer pair at M = 3 (the gather in
+    LDS; the scratch keeps the first call's data), then M = 64 on the large
+    pair again; every output equal bit for bit to tpdq_mlp_shard's, and the
+    M = 16 call within 2e-3 of the oracle."""
+    import torch
+    import paper_2402_04925_amd as tpdq
+    dev = torch_dev()
+    ordered = path == "ordered"
+    p = tpdq.PATH_ORDERED if ordered else tpdq.PATH_ACTORDER
+    w = inputs.WORKLOADS["llama70b_tp8"]
+    L1, L2 = workload_layers(w.name)
+    d1, d2 = layer_to_dev(L1, dev), layer_to_dev(L2, dev)
+    if ordered:
+        P1, _, _, _, w1o, w2o = tpdq.reorder(d1, d2)
+        s1, s2 = w1o.column_shard(0, w.tp), w2o.row_shard(0, w.tp, True)
+    else:
+        P1, s1, s2 = None, d1.column_shard(0, w.tp), d2.row_shard(0, w.tp, False)
+    X = inputs.make_x(w, 16)
+    log(f"noalloc {path} llama70b_tp8 M=16")
+    (r1, r2), (g1, g2) = _pair(tpdq, to_dev(X, dev), s1, s2, p, P1)
+    assert _same(r1, g1) and _same(r2, g2)
+    eP2, _ = o.reorder(L2.g_idx)
+    cols = np.arange(0, w.N2, 97)
+    e1, e2 = o.mlp_rank_from_global(X, (L1.qweight, L1.scales, L1.qzeros, L1.g_idx),
+                                    (L2.qweight, L2.scales, L2.qzeros, L2.g_idx), 0, w.tp, ordered,
+                                    P2=eP2, cols2=cols)
+    assert o.rel_err(np_of(g1), e1) <= TOL_FP16
+    assert o.rel_err(np_of(g2)[:, cols], e2) <= TOL_FP16
+
+    # a smaller input right after: the scratch still holds the first call's data
+    log(f"noalloc {path} small pair M=3")
+    a1, a2 = inputs.make_custom(512, 256, 128, 64, seed=77)
+    b1, b2 = layer_to_dev(a1, dev), layer_to_dev(a2, dev)
+    if ordered:
+        Q1, _, _, _, b1o, b2o = tpdq.reorder(b1, b2)
+        t1, t2 = b1o.column_shard(0, 2), b2o.row_shard(0, 2, True)
+    else:
+        Q1, t1, t2 = None, b1.column_shard(0, 2), b2.row_shard(0, 2, False)
+    Xs = inputs.random_activations(3, 512, np.random.default_rng(3))
+    (r1, r2), (g1, g2) = _pair(tpdq, to_dev(Xs, dev), t1, t2, p, Q1)
+    assert _same(r1, g1) and _same(r2, g2)
+    eQ2, _ = o.reorder(a2.g_idx)
+    f1, f2 = o.mlp_rank_from_global(Xs, (a1.qweight, a1.scales, a1.qzeros, a1.g_idx),
+                                    (a2.qweight, a2.scales, a2.qzeros, a2.g_idx), 0, 2, ordered, P2=eQ2)
+    assert o.rel_err(np_of(g1), f1) <= TOL_FP16 and o.rel_err(np_of(g2), f2) <= TOL_FP16
+
+    log(f"noalloc {path} llama70b_tp8 M=64")
+    X64 = to_dev(inputs.make_x(w, 64), dev)
+    (r1, r2), (g1, g2) = _pair(tpdq, X64, s1, s2, p, P1)
+    assert _same(r1, g1) and _same(r2, g2)
+
+
+def test_noalloc_rejects_beyond_scratch():
+    """A shape whose workspace exceeds the 64 MiB scratch is refused before
+    any device work, with a message naming the scratch."""
+    import torch
+    import paper_2402_04925_amd as tpdq
+    dev = torch_dev()
+    a1, a2 = inputs.make_custom(8192, 256, 128, 128, seed=5)
+    b1, b2 = layer_to_dev(a1, dev), layer_to_dev(a2, dev)
+    P1, _, _, _, b1o, b2o = tpdq.reorder(b1, b2)
+    M = 8192
+    assert tpdq.workspace_bytes(tpdq.OP_MLP, M, b1o, b2o) > 64 << 20
+    X = torch.zeros(M, 8192, dtype=torch.float16, device=dev)
+    with pytest.raises(tpdq.TpdqError, match="scratch"):
+        tpdq.mlp_shard_noalloc(X, b1o, b2o, tpdq.PATH_ORDERED, P1=P1)
+    torch.cuda.synchronize()
