@@ -14,7 +14,13 @@ the activations and scales are bfloat16) Y1 and Y2 are rounded to bfloat16
 instead, also once and to nearest even (to_bf16).
 
 Readings of the paper taken here (the paper is silent on them):
-  * dequant is asymmetric: w = s * (q - z) with q, z the stored int4 codes;
+  * dequant is asymmetric: w = s * (q - z) with q the stored int4 code and z
+    the stored zero code plus the layer's zero offset (0 by default; 1 for
+    packers that store z - 1, so that z = 16 is reachable);
+  * groups: Eq. 3 with a permutation phi gives every group G rows except a
+    partial last group of K - (ng - 1) G rows when G does not divide K
+    (ng = ceil(K / G)); a checkpoint may also carry groups of unequal sizes
+    (G = 0 here), given by g_idx alone;
   * storage: qweight int32 [K/8][N], nibble j of word [r][n] is row 8r+j;
     qzeros int32 [K/G][N/8], nibble j of word [g][c] is column 8c+j;
   * the argsort of Alg. 1 is stable (ties by ascending row index) and
@@ -98,20 +104,36 @@ class GroupIndexError(ValueError):
     pass
 
 
+def eq3_group_counts(K: int, G: int) -> np.ndarray:
+    """Rows per group that Eq. 3 gives for a permutation phi of 0..K-1: the
+    values phi(i) in [g G, (g + 1) G) are exactly those of group g, so every
+    group has G rows except the last, which has K - (ng - 1) G (ng =
+    ceil(K / G))."""
+    ng = -(-K // G)
+    counts = np.full(ng, G, dtype=np.int64)
+    counts[-1] = K - (ng - 1) * G
+    return counts
+
+
 def check_groups(g_idx: np.ndarray, G: int, num_groups: int | None = None) -> None:
-    """Every group must be a valid index and hold exactly G rows, which is what
-    Eq. 3 gives for a permutation phi when G divides K."""
+    """G > 0: every g_idx value is a group index and the groups hold the rows
+    Eq. 3 gives (eq3_group_counts: G each, a partial last group when G does
+    not divide K). G == 0: groups of any size (a checkpoint's own grouping);
+    only the range [0, num_groups) is checked."""
     g = np.asarray(g_idx, dtype=np.int64)
     K = g.shape[0]
-    if num_groups is None:
-        if K % G:
-            raise GroupIndexError("K must be a multiple of G")
-        num_groups = K // G
+    if G == 0:
+        if num_groups is None:
+            raise GroupIndexError("groups of unequal size need num_groups")
+    elif num_groups is None:
+        num_groups = -(-K // G)
     if g.size and (g.min() < 0 or g.max() >= num_groups):
         raise GroupIndexError("g_idx value out of range")
+    if G == 0:
+        return
     counts = np.bincount(g, minlength=num_groups)
-    if np.any(counts != G):
-        raise GroupIndexError("a group does not hold exactly G rows")
+    if num_groups != -(-K // G) or np.any(counts != eq3_group_counts(K, G)):
+        raise GroupIndexError("the groups do not hold the rows Eq. 3 gives")
 
 
 def reorder(g_idx: np.ndarray):
@@ -129,8 +151,9 @@ def reorder(g_idx: np.ndarray):
 # ----------------------------------------------------------------------------
 
 
-def dequant(qweight, scales, qzeros, g_idx, cols=None) -> np.ndarray:
-    """W[k][n] = s[g_idx[k]][n] * (q[k][n] - z[g_idx[k]][n]) in float64.
+def dequant(qweight, scales, qzeros, g_idx, cols=None, zero_offset=0) -> np.ndarray:
+    """W[k][n] = s[g_idx[k]][n] * (q[k][n] - z[g_idx[k]][n]) in float64, with
+    z the stored zero code plus zero_offset.
 
     Row k takes its scale and zero from group g_idx[k] (Eq. 3 for act-order,
     Eq. 1 / the sorted g_idx for ordered weights). `cols` restricts the result
@@ -146,7 +169,7 @@ def dequant(qweight, scales, qzeros, g_idx, cols=None) -> np.ndarray:
         q = unpack_rows(np.asarray(qweight)[:, cols])
         z = unpack_cols(qzeros)[:, cols]
         s = np.asarray(scales)[:, cols].astype(np.float64)
-    return s[g, :] * (q - z[g, :]).astype(np.float64)
+    return s[g, :] * (q - (z[g, :] + int(zero_offset))).astype(np.float64)
 
 
 def matmul(X, W, acc="f64") -> np.ndarray:
@@ -182,14 +205,14 @@ def round_to(a, dtype="fp16") -> np.ndarray:
 
 
 def w4a16_gemm(X, qweight, scales, qzeros, g_idx, x_perm=None, acc="f64", cols=None,
-               round_fp16=True, dtype="fp16"):
+               round_fp16=True, dtype="fp16", zero_offset=0):
     """Y[m][n] = sum_k X'[m][k] * W[k][n] with X' = X[:, x_perm] when a gather
     is given (the X[:, P1] of Alg. 2 and Alg. 3), rounded to fp16 (or to
     bfloat16 with dtype="bf16"; round_fp16=False keeps the float64 sum)."""
     X = np.asarray(X)
     if x_perm is not None:
         X = X[:, np.asarray(x_perm, dtype=np.int64)]
-    Y = matmul(X, dequant(qweight, scales, qzeros, g_idx, cols), acc)
+    Y = matmul(X, dequant(qweight, scales, qzeros, g_idx, cols, zero_offset), acc)
     return round_to(Y, dtype) if round_fp16 else Y
 
 
@@ -278,18 +301,22 @@ def mlp_reference(X, w1, g1, w2, g2, acc="f64", y1_fp16=True, dtype="fp16"):
 
 
 def mlp_tp_aware_rank(X, P1, w1f_shard, w2f_shard, G, acc="f64", y1_fp16=True, round_y2=True,
-                      dtype="fp16"):
+                      dtype="fp16", g1=None, g2=None):
     """Alg. 3 on one rank, up to its AllReduce:
       Y1_local = X[:, P1] @ W1_local   (W1_local a column shard of W1[P1, P2])
       Y2_local = Y1_local @ W2_local   (W2_local a row shard of W2[P2])
     Both shards hold sorted rows, so their group of local row k is floor(k/G)
-    (Eq. 1 applied to the shard)."""
+    (Eq. 1 applied to the shard). With groups of unequal size (G = 0) the
+    sorted group indices of the shards' rows are given instead (g1, g2; a
+    row shard of W2 then keeps every group's metadata)."""
     K1 = w1f_shard["qweight"].shape[0] * 8
     K2 = w2f_shard["qweight"].shape[0] * 8
-    Y1 = w4a16_gemm(X, *_layer(w1f_shard, g_idx_naive(K1, G)), x_perm=P1, acc=acc,
-                    round_fp16=y1_fp16, dtype=dtype)
-    Y2 = w4a16_gemm(Y1, *_layer(w2f_shard, g_idx_naive(K2, G)), acc=acc, round_fp16=round_y2,
-                    dtype=dtype)
+    g1 = g_idx_naive(K1, G) if g1 is None else g1
+    g2 = g_idx_naive(K2, G) if g2 is None else g2
+    Y1 = w4a16_gemm(X, *_layer(w1f_shard, g1), x_perm=P1, acc=acc, round_fp16=y1_fp16, dtype=dtype,
+                    zero_offset=w1f_shard.get("zero_offset", 0))
+    Y2 = w4a16_gemm(Y1, *_layer(w2f_shard, g2), acc=acc, round_fp16=round_y2, dtype=dtype,
+                    zero_offset=w2f_shard.get("zero_offset", 0))
     return Y1, Y2
 
 
@@ -430,6 +457,11 @@ def fold_sample(qweight, P_row, P_col, rows, cols):
     return ((words >> shift) & np.uint32(0xF)).astype(np.int64)
 
 
+def _split_layer(l):
+    """(qweight, scales, qzeros, g_idx[, zero_offset]) -> the four arrays and the offset."""
+    return tuple(l[:4]), (int(l[4]) if len(l) > 4 else 0)
+
+
 def mlp_rank_from_global(X, l1, l2, rank, tp, ordered, P2=None, cols2=None, acc="f64",
                          dtype="fp16", y1_round=True, round_y2=True):
     """One rank's (Y1, Y2 partial[:, cols2]) computed from the unpermuted
@@ -443,14 +475,15 @@ def mlp_rank_from_global(X, l1, l2, rank, tp, ordered, P2=None, cols2=None, acc=
     the columns of X (X[:, P1]) leaves every dot product's terms unchanged, the
     partial is X @ deq(W1)[:, P2[block]] then @ deq(W2)[P2[block], :].
     y1_round / round_y2 False keep Y1 / Y2 in float64."""
+    (l1, zo1), (l2, zo2) = _split_layer(l1), _split_layer(l2)
     N1 = np.asarray(l1[0]).shape[1]
     n = N1 // tp
     blk = np.arange(rank * n, (rank + 1) * n)
     sel = np.asarray(P2, dtype=np.int64)[blk] if ordered else blk
-    Y1 = matmul(X, dequant(*l1, cols=sel), acc)
+    Y1 = matmul(X, dequant(*l1, cols=sel, zero_offset=zo1), acc)
     if y1_round:
         Y1 = round_to(Y1, dtype)
-    W2 = dequant(*l2, cols=cols2)[sel]
+    W2 = dequant(*l2, cols=cols2, zero_offset=zo2)[sel]
     Y2 = matmul(Y1, W2, acc)
     return Y1, (round_to(Y2, dtype) if round_y2 else Y2)
 

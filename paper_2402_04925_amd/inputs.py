@@ -125,16 +125,51 @@ class QuantLinear:
 
 def make_layer(K: int, N: int, G: int, cfg_id: int, t_phi: int, t_qw: int, t_s: int, t_z: int,
                seed: int = BASE_SEED, scale_dtype=np.float16) -> QuantLinear:
-    if K % 8 or N % 8 or K % G or G % 8:
+    """An act-order layer by Eq. 2-3; when G does not divide K the last of the
+    ceil(K / G) groups is partial."""
+    if K % 8 or N % 8 or G % 8 or G <= 0:
         raise ValueError(f"unsupported layer shape K={K} N={N} G={G}")
+    ng = -(-K // G)
     phi = random_permutation(K, rng_for(cfg_id, t_phi, seed))
     return QuantLinear(
         qweight=random_words((K // 8, N), rng_for(cfg_id, t_qw, seed)),
-        scales=random_scales((K // G, N), rng_for(cfg_id, t_s, seed), dtype=scale_dtype),
-        qzeros=random_words((K // G, N // 8), rng_for(cfg_id, t_z, seed)),
+        scales=random_scales((ng, N), rng_for(cfg_id, t_s, seed), dtype=scale_dtype),
+        qzeros=random_words((ng, N // 8), rng_for(cfg_id, t_z, seed)),
         g_idx=actorder_gidx(phi, G),
         phi=phi,
         G=G,
+    )
+
+
+def unequal_gidx(phi: np.ndarray, sizes: np.ndarray) -> np.ndarray:
+    """Input synthesis for groups of unequal size (a checkpoint's own
+    grouping): row i belongs to group g when phi(i) lies in
+    [sizes[0] + .. + sizes[g-1], sizes[0] + .. + sizes[g]), the unequal-size
+    form of Eq. 3."""
+    bounds = np.cumsum(np.asarray(sizes, dtype=np.int64))
+    return np.searchsorted(bounds, np.asarray(phi, dtype=np.int64), side="right").astype(np.int32)
+
+
+T_SIZES = 12  # stream of the group sizes of an unequal-group layer
+
+
+def make_unequal_layer(K: int, N: int, ng: int, seed: int, cfg_id: int = 101, layer: int = 0,
+                       scale_dtype=np.float16) -> QuantLinear:
+    """An act-order layer whose ng groups have unequal sizes (multinomial over
+    the groups, so some may be small or empty); G = 0 marks the grouping as
+    given by g_idx alone."""
+    if K % 8 or N % 8 or ng < 1:
+        raise ValueError(f"unsupported layer shape K={K} N={N} ng={ng}")
+    t = 16 * layer
+    sizes = rng_for(cfg_id, t + T_SIZES, seed).multinomial(K, np.full(ng, 1.0 / ng))
+    phi = random_permutation(K, rng_for(cfg_id, t + T_PHI1, seed))
+    return QuantLinear(
+        qweight=random_words((K // 8, N), rng_for(cfg_id, t + T_QW1, seed)),
+        scales=random_scales((ng, N), rng_for(cfg_id, t + T_S1, seed), dtype=scale_dtype),
+        qzeros=random_words((ng, N // 8), rng_for(cfg_id, t + T_Z1, seed)),
+        g_idx=unequal_gidx(phi, sizes),
+        phi=phi,
+        G=0,
     )
 
 

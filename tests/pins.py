@@ -480,6 +480,140 @@ def pin_fold_sample(o, seed=29):
             src_r, src_c = int(Pr[r]), int(Pc[c])
             assert got[a, b] == nibble_by_hex(int(words[src_r // 8, src_c]), src_r % 8)
 
+
+# -------------------------------------------- checkpoint conventions ---
+
+def pin_zero_offset(o, seed=30):
+    """A layer whose packer stores z - 1 (zero_offset = 1): dequantizing stored
+    zeros z' with the offset equals dequantizing stored zeros z' + 1 without
+    it (zeros of at most 14 stored); a hand value where the offset reaches the
+    zero 16 that four bits cannot store: q = 5, stored z' = 15 gives
+    s (5 - 16) = -11 s; and the GEMM with the offset against a triple loop
+    over hex spellings."""
+    K, N, G = 32, 16, 8
+    w1, _ = inputs.make_custom(K, N, 0, G, seed)
+    z = o.unpack_cols(w1.qzeros)
+    z14 = np.minimum(z, 14)
+    a = o.dequant(w1.qweight, w1.scales, o.pack_cols(z14), w1.g_idx, zero_offset=1)
+    b = o.dequant(w1.qweight, w1.scales, o.pack_cols(z14 + 1), w1.g_idx)
+    assert np.array_equal(a, b)
+    qw = np.zeros((1, 8), dtype=np.uint32)
+    qw[0, 0] = 0x5                                # row 0, column 0: code 5
+    qz = np.array([[0xF]], dtype=np.uint32)       # column 0: stored zero 15
+    sc = np.full((1, 8), 0.25, dtype=np.float16)
+    W = o.dequant(qw.view(np.int32), sc, qz.view(np.int32), np.zeros(8, np.int64), zero_offset=1)
+    assert W[0, 0] == 0.25 * (5 - 16) and W[1, 0] == 0.25 * (0 - 16)
+    M = 2
+    X = inputs.random_activations(M, K, np.random.default_rng(seed))
+    words, zw = w1.qweight.view(np.uint32), w1.qzeros.view(np.uint32)
+    Y = o.w4a16_gemm(X, w1.qweight, w1.scales, w1.qzeros, w1.g_idx, round_fp16=False, zero_offset=1)
+    for m in range(M):
+        for n in range(N):
+            acc = 0.0
+            for k in range(K):
+                g = int(w1.g_idx[k])
+                q = nibble_by_hex(int(words[k // 8, n]), k % 8)
+                zz = nibble_by_hex(int(zw[g, n // 8]), n % 8) + 1
+                acc += float(X[m, k]) * float(w1.scales[g, n]) * (q - zz)
+            assert abs(Y[m, n] - acc) <= 1e-12 * max(1.0, abs(acc)), (m, n)
+
+
+def pin_partial_last_group(o, seed=31):
+    """G not dividing K (K = 72, G = 32): Eq. 3 gives groups of 32, 32 and 8
+    rows, which check_groups accepts (and a last group of 9 rows it rejects);
+    Alg. 1 still yields Eq. 1, g_sorted[j] = floor(j / G); the ordered product
+    equals the act-order product; a triple loop over hex spellings fixes the
+    GEMM; the TP-aware MLP with a partial last group in both layers equals the
+    unsharded act-order MLP (TP = 1), and the act-order rank sum does at
+    TP = 2."""
+    K1, N1, N2, G = 72, 80, 16, 32
+    w1, w2 = inputs.make_custom(K1, N1, N2, G, seed)
+    assert w1.scales.shape[0] == 3 and w2.scales.shape[0] == 3
+    assert np.array_equal(np.bincount(w1.g_idx), [32, 32, 8])
+    assert np.array_equal(np.bincount(w2.g_idx), [32, 32, 16])
+    o.check_groups(w1.g_idx, G)
+    bad = w1.g_idx.copy()
+    bad[np.flatnonzero(bad == 1)[0]] = 2          # groups of 31, 32, 9 rows
+    try:
+        o.check_groups(bad, G)
+        raise AssertionError("a wrong partial group accepted")
+    except o.GroupIndexError:
+        pass
+    P, gs = o.reorder(w1.g_idx)
+    assert np.array_equal(gs, np.arange(K1) // G)
+    X = inputs.random_activations(3, K1, np.random.default_rng(seed))
+    ref = o.w4a16_gemm(X, w1.qweight, w1.scales, w1.qzeros, w1.g_idx, round_fp16=False)
+    ws = o.permute_rows(dict(qweight=w1.qweight, scales=w1.scales, qzeros=w1.qzeros), P)
+    Yo = o.w4a16_gemm(X, ws["qweight"], ws["scales"], ws["qzeros"], o.g_idx_naive(K1, G), x_perm=P,
+                      round_fp16=False)
+    _close(Yo, ref)
+    words, zw = w1.qweight.view(np.uint32), w1.qzeros.view(np.uint32)
+    for m in range(3):
+        for n in (0, 7, 41, 79):
+            acc = 0.0
+            for k in range(K1):
+                g = int(w1.g_idx[k])
+                q = nibble_by_hex(int(words[k // 8, n]), k % 8)
+                zz = nibble_by_hex(int(zw[g, n // 8]), n % 8)
+                acc += float(X[m, k]) * float(w1.scales[g, n]) * (q - zz)
+            assert abs(ref[m, n] - acc) <= 1e-12 * max(1.0, abs(acc))
+    d1 = dict(qweight=w1.qweight, scales=w1.scales, qzeros=w1.qzeros)
+    d2 = dict(qweight=w2.qweight, scales=w2.scales, qzeros=w2.qzeros)
+    mref = o.w4a16_gemm(ref, *_l(d2, w2.g_idx), round_fp16=False)
+    P2, _ = o.reorder(w2.g_idx)
+    w1f, w2f = o.fold(d1, d2, P, P2)
+    _, y2 = o.mlp_tp_aware_rank(X, P, w1f, w2f, G, y1_fp16=False, round_y2=False)
+    _close(y2, mref)
+    tot = np.zeros_like(mref)
+    for r in range(2):
+        n = N1 // 2
+        _, a2 = o.mlp_actorder_rank(X, o.column_shard(d1, r, 2), w1.g_idx,
+                                    o.row_shard(d2, r, 2, G, keep_all_groups=True),
+                                    w2.g_idx[r * n:(r + 1) * n], y1_fp16=False, round_y2=False)
+        tot += a2
+    _close(tot, mref)
+
+
+def pin_unequal_groups(o, seed=32):
+    """Groups of unequal size (G = 0: the grouping is g_idx alone): the
+    generator's group sizes are the bincount of g_idx; check_groups accepts
+    them only in the unequal mode; Alg. 1's sorted g_idx is the runs of those
+    sizes in group order (closed form); the ordered product through the
+    sorted g_idx equals the act-order product; the TP-aware MLP (W2's row
+    shards keep every group's metadata and their rows' sorted group indices)
+    sums over ranks to the unsharded MLP at TP = 1, 2 and 4."""
+    K1, N1, N2, ng1, ng2 = 96, 128, 24, 7, 9
+    w1 = inputs.make_unequal_layer(K1, N1, ng1, seed, layer=0)
+    w2 = inputs.make_unequal_layer(N1, N2, ng2, seed, layer=1)
+    sizes1 = np.bincount(w1.g_idx, minlength=ng1)
+    assert sizes1.sum() == K1 and len(set(sizes1.tolist())) > 1
+    o.check_groups(w1.g_idx, 0, num_groups=ng1)
+    try:
+        o.check_groups(w1.g_idx, K1 // ng1 // 8 * 8 or 8)
+        raise AssertionError("unequal groups accepted as equal ones")
+    except o.GroupIndexError:
+        pass
+    P1, g1s = o.reorder(w1.g_idx)
+    assert np.array_equal(g1s, np.repeat(np.arange(ng1), sizes1))
+    P2, g2s = o.reorder(w2.g_idx)
+    X = inputs.random_activations(4, K1, np.random.default_rng(seed))
+    d1 = dict(qweight=w1.qweight, scales=w1.scales, qzeros=w1.qzeros)
+    d2 = dict(qweight=w2.qweight, scales=w2.scales, qzeros=w2.qzeros)
+    ref1 = o.w4a16_gemm(X, *_l(d1, w1.g_idx), round_fp16=False)
+    ws = o.permute_rows(d1, P1)
+    _close(o.w4a16_gemm(X, *_l(ws, g1s), x_perm=P1, round_fp16=False), ref1)
+    mref = o.w4a16_gemm(ref1, *_l(d2, w2.g_idx), round_fp16=False)
+    w1f, w2f = o.fold(d1, d2, P1, P2)
+    for tp in (1, 2, 4):
+        n = N1 // tp
+        tot = np.zeros_like(mref)
+        for r in range(tp):
+            sh2 = o.row_shard(w2f, r, tp, 0, keep_all_groups=True)
+            _, y2 = o.mlp_tp_aware_rank(X, P1, o.column_shard(w1f, r, tp), sh2, 0, y1_fp16=False,
+                                        round_y2=False, g1=g1s, g2=g2s[r * n:(r + 1) * n])
+            tot += y2
+        _close(tot, mref)
+
 # ------------------------------------------------------------- bfloat16 ---
 
 def pin_bf16_rounding(o, seed=21):
@@ -625,4 +759,5 @@ ALL_PINS = [
     pin_distinct_groups, pin_bf16_rounding, pin_bf16_gemm, pin_silu,
     pin_gated_tp_aware_mlp, pin_gated_special_cases, pin_gated_bruteforce,
     pin_rank_from_global, pin_gated_rank_from_global, pin_fold_sample,
+    pin_zero_offset, pin_partial_last_group, pin_unequal_groups,
 ]

@@ -182,6 +182,28 @@ def _fold_sample_inverse_cols(qweight, P_row, P_col, rows, cols):
     return _orig["fold_sample"](qweight, P_row, P_col, rows, cols)
 
 
+def _dequant_offset_ignored(qweight, scales, qzeros, g_idx, cols=None, zero_offset=0):
+    return _orig["dequant"](qweight, scales, qzeros, g_idx, cols, 0)
+
+
+def _dequant_offset_sign(qweight, scales, qzeros, g_idx, cols=None, zero_offset=0):
+    return _orig["dequant"](qweight, scales, qzeros, g_idx, cols, -zero_offset)
+
+
+def _check_groups_strict(g_idx, G, num_groups=None):
+    g = np.asarray(g_idx, dtype=np.int64)
+    if G == 0:
+        return _orig["check_groups"](g_idx, G, num_groups)
+    if len(g) % G:
+        raise o.GroupIndexError("K must be a multiple of G")
+    return _orig["check_groups"](g_idx, G, num_groups)
+
+
+def _eq3_counts_full(K, G):
+    ng = -(-K // G)
+    return np.full(ng, G, dtype=np.int64)
+
+
 MUTANTS = {
     "unpack_rows": _unpack_rows_reversed,
     "unpack_cols": _unpack_cols_reversed,
@@ -210,6 +232,10 @@ MUTANTS = {
     "fold_sample:rows": _fold_sample_unpermuted_rows,
     "fold_sample:shift": _fold_sample_shift,
     "fold_sample:inverse_cols": _fold_sample_inverse_cols,
+    "dequant:zero_offset_ignored": _dequant_offset_ignored,
+    "dequant:zero_offset_sign": _dequant_offset_sign,
+    "check_groups:no_partial_group": _check_groups_strict,
+    "eq3_group_counts:full_last_group": _eq3_counts_full,
 }
 
 
