@@ -33,9 +33,14 @@
  *   qzeros  int32 [num_groups][ld_z]     nibble j of word [g][c] is the
  *                               4-bit zero code z of group g, column 8c+j
  *   g_idx   int32 [K]           group of row k
- *   dequantized weight: W[k][n] = s[g][n] * (q[k][n] - z[g][n]), g = g_idx[k]
- * A sorted ("ordered") layer has g_idx[k] == floor(k / G) (Eq. 1); the
- * ordered kernels then never read g_idx.
+ *   dequantized weight: W[k][n] = s[g][n] * (q[k][n] - z[g][n]), g = g_idx[k],
+ *   with z the stored zero code plus the layer's zero_offset
+ * Groups: with a group size G > 0, Eq. 3 gives every group G rows except a
+ * partial last group when G does not divide K (ceil(K/G) groups); a sorted
+ * ("ordered") layer then has g_idx[k] == floor(k / G) (Eq. 1) and the ordered
+ * kernels never read g_idx. G == 0 marks groups of unequal sizes given by
+ * g_idx alone (a checkpoint's own grouping); a sorted layer of that kind is
+ * read through its sorted (non-decreasing) g_idx.
  */
 #ifndef TPDQ_H
 #define TPDQ_H
@@ -50,9 +55,9 @@ extern "C" {
 typedef enum {
   TPDQ_OK = 0,
   TPDQ_ERR_NULL = 1,        /* a required pointer is NULL                              */
-  TPDQ_ERR_SHAPE = 2,       /* K%8, N%8, G%8, K%G (sorted rows), K2 != N1, M < 1, ld too small */
+  TPDQ_ERR_SHAPE = 2,       /* K%8, N%8, G%8, too few groups, K2 != N1, M < 1, ld too small */
   TPDQ_ERR_ALIGN = 3,       /* a pointer or leading dimension breaks the vector alignment */
-  TPDQ_ERR_GIDX = 4,        /* g_idx out of range, or a group without exactly G rows    */
+  TPDQ_ERR_GIDX = 4,        /* g_idx out of range, or groups other than Eq. 3's (G > 0)  */
   TPDQ_ERR_WORKSPACE = 5,   /* workspace NULL or smaller than tpdq_workspace_bytes()    */
   TPDQ_ERR_UNSUPPORTED = 6, /* valid request this build does not implement, e.g. a tensor of
                              2 GiB or more (the kernels address each tensor with 32-bit
@@ -96,7 +101,10 @@ typedef enum {
      metadata of a 16-column tile (all num_groups groups) is staged in LDS. */
   TPDQ_PATH_ACTORDER = 0,
   /* Rows sorted by group (Alg. 1; the optimized load of Fig. 2): the group of
-     local row k is floor(k / G); g_idx is ignored and may be NULL. */
+     local row k is floor(k / G); g_idx is ignored and may be NULL. With
+     group_size 0 (groups of unequal sizes) g_idx is the sorted, non-decreasing
+     group index of each row and is required; the rows then take their
+     metadata through it (the per-row kernel, on sorted rows). */
   TPDQ_PATH_ORDERED = 1,
   /* As TPDQ_PATH_ACTORDER, but every row fetches its scale and zero from
      global memory (Fig. 1 as drawn, no staging): the baseline for counting
@@ -106,10 +114,14 @@ typedef enum {
 
 /* One quantized layer, or a shard of one given as views (pointer offsets and
  * leading dimensions). K = input features (rows), N = output features.
- * num_groups is the number of metadata rows: K/G for a whole or sorted layer;
- * an act-order row-parallel shard keeps the global metadata and global g_idx
- * values, so there num_groups = K_global/G exceeds K/G. layout is a
+ * num_groups is the number of metadata rows: ceil(K/G) for a whole or sorted
+ * layer; an act-order row-parallel shard keeps the global metadata and global
+ * g_idx values, so there num_groups = ceil(K_global/G) exceeds ceil(K/G) (so
+ * does a sorted row shard of a layer with groups of unequal sizes, G == 0,
+ * whose g_idx then holds its rows' global sorted groups). layout is a
  * tpdq_layout (scales, qzeros and g_idx are always as described above).
+ * zero_offset (0 or 1) is added to every stored zero code: 1 for packers that
+ * store z - 1 (the zero 16 is then reachable).
  * Alignment: qweight 16 B and ld_q % 4 == 0; scales 8 B and ld_s % 4 == 0;
  * qzeros 4 B; g_idx 16 B. */
 typedef struct tpdq_w4 {
@@ -122,9 +134,10 @@ typedef struct tpdq_w4 {
   const int32_t* g_idx;
   int32_t K;
   int32_t N;
-  int32_t group_size;  /* G, a multiple of 8 */
+  int32_t group_size;  /* G, a multiple of 8; 0: groups of unequal sizes given by g_idx */
   int32_t num_groups;
   int32_t layout;      /* tpdq_layout of qweight */
+  int32_t zero_offset; /* 0 or 1, added to each stored zero code */
 } tpdq_w4;
 
 /*
@@ -142,12 +155,15 @@ typedef struct tpdq_w4 {
  * A gather: new index j takes old index P[j]. Ties in the sort keep ascending
  * row order, so P is unique (any stable sort gives the same P).
  *
- * Requirements: every g_idx value in [0, K/G) and every group holding exactly
- * G rows (what Eq. 3 gives for a permutation phi with G | K); K%G == 0,
- * G%8 == 0, N%8 == 0; both inputs in TPDQ_LAYOUT_GPTQ. Outputs are dense:
+ * Requirements: every g_idx value in [0, num_groups); with G > 0,
+ * num_groups == ceil(K/G) and the groups holding the rows Eq. 3 gives for a
+ * permutation phi (G each, the last K - (num_groups - 1) G); with G == 0
+ * (groups of unequal sizes) any group sizes. G%8 == 0, N%8 == 0; both inputs
+ * in TPDQ_LAYOUT_GPTQ. Outputs are dense:
  * qweight1_out and qweight2_out in out_layout (GPTQ: int32 [K/8][N]; TILED:
- * int32 [ceil(N/16)][ceil(K/128)*256]), scales1_out [K1/G][N1] (the dtype of
- * w1->scales), qzeros1_out int32 [K1/G][N1/8], P and g_sorted int32 [K].
+ * int32 [ceil(N/16)][ceil(K/128)*256]), scales1_out [num_groups][N1] (the
+ * dtype of w1->scales), qzeros1_out int32 [num_groups][N1/8], P and g_sorted
+ * int32 [K]. The zero offset of each layer carries over unchanged.
  * P2, g2_sorted and qweight2_out must be NULL when w2 is NULL.
  *
  * Workspace: at least tpdq_workspace_bytes(0, 0, w1, w2) bytes, any content.
@@ -259,8 +275,8 @@ tpdq_status tpdq_mlp_shard_noalloc(const void* X, int64_t ldx, int32_t M, const 
  * TPDQ_PATH_ACTORDER / TPDQ_PATH_ACTORDER_GLOBAL: w_gate, w_up and w_down as
  *   for tpdq_mlp_shard; w_gate->g_idx serves both gate and up (w_up->g_idx
  *   is not read); P1 must be NULL.
- * w_up must have w_gate's K, N, group size, num_groups, layout and leading
- * dimensions (TPDQ_ERR_SHAPE otherwise); w_down->K == w_gate->N.
+ * w_up must have w_gate's K, N, group size, num_groups, layout, leading
+ * dimensions and zero offset (TPDQ_ERR_SHAPE otherwise); w_down->K == w_gate->N.
  * X, Y1, Y2_partial, alignment and workspace as for tpdq_mlp_shard, with
  * tpdq_workspace_bytes(3, M, w_gate, w_down). Runs the decode kernels at
  * every M (batches of more than 64 rows in launches of 64).

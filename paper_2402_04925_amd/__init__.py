@@ -96,7 +96,8 @@ class QuantWeight:
     qweight int32: GPTQ layout [K/8][>=N], or tiled layout
     [ceil(N/16)][>=tiled_ld(K)] (see include/tpdq.h); scales fp16
     [num_groups][>=N]; qzeros int32 [num_groups][>=N/8]; g_idx int32 [K] or
-    None.
+    None. G = 0: groups of unequal sizes given by g_idx alone. zero_offset
+    (0 or 1) is added to every stored zero code.
     """
     qweight: object
     scales: object
@@ -107,14 +108,16 @@ class QuantWeight:
     G: int
     num_groups: int
     layout: int = LAYOUT_GPTQ
+    zero_offset: int = 0
 
     @classmethod
-    def from_tensors(cls, qweight, scales, qzeros, g_idx, G: int, num_groups: Optional[int] = None):
+    def from_tensors(cls, qweight, scales, qzeros, g_idx, G: int, num_groups: Optional[int] = None,
+                     zero_offset: int = 0):
         """A GPTQ-layout layer: K and N follow from qweight's shape."""
         K = qweight.shape[0] * 8
         N = qweight.shape[1]
         ng = scales.shape[0] if num_groups is None else num_groups
-        return cls(qweight, scales, qzeros, g_idx, K, N, G, ng, LAYOUT_GPTQ)
+        return cls(qweight, scales, qzeros, g_idx, K, N, G, ng, LAYOUT_GPTQ, zero_offset)
 
     def c_struct(self) -> _abi.W4:
         torch = _torch()
@@ -138,7 +141,7 @@ class QuantWeight:
             scales=_ptr(self.scales), ld_s=self.scales.stride(0),
             qzeros=_ptr(self.qzeros), ld_z=self.qzeros.stride(0),
             g_idx=_ptr(self.g_idx), K=self.K, N=self.N, group_size=self.G,
-            num_groups=self.num_groups, layout=self.layout)
+            num_groups=self.num_groups, layout=self.layout, zero_offset=self.zero_offset)
 
     @property
     def device(self):
@@ -155,12 +158,14 @@ class QuantWeight:
         else:
             qw = self.qweight[:, c0:c0 + n]
         return QuantWeight(qw, self.scales[:, c0:c0 + n], self.qzeros[:, c0 // 8:(c0 + n) // 8],
-                           self.g_idx, self.K, n, self.G, self.num_groups, self.layout)
+                           self.g_idx, self.K, n, self.G, self.num_groups, self.layout, self.zero_offset)
 
     def row_shard(self, rank: int, tp: int, sorted_rows: bool) -> "QuantWeight":
         """Megatron row-parallel shard (views): rows [rank*K/tp, ...).
 
-        Sorted rows keep only their own consecutive groups; act-order rows
+        Sorted rows keep only their own consecutive groups (the shard must
+        start on a group boundary; the last may end in a partial group);
+        act-order rows, and sorted rows in groups of unequal sizes (G = 0),
         keep the global g_idx values of their rows and all the metadata."""
         k = self.K // tp
         r0 = rank * k
@@ -172,12 +177,14 @@ class QuantWeight:
         else:
             qw = self.qweight[r0 // 8:(r0 + k) // 8]
         g = None if self.g_idx is None else self.g_idx[r0:r0 + k]
-        if sorted_rows:
-            g0, ng = r0 // self.G, k // self.G
+        if sorted_rows and self.G > 0:
+            if r0 % self.G:
+                raise ValueError("a sorted row shard must start on a group boundary")
+            g0, ng = r0 // self.G, -(-k // self.G)
             return QuantWeight(qw, self.scales[g0:g0 + ng], self.qzeros[g0:g0 + ng], g, k, self.N,
-                               self.G, ng, self.layout)
+                               self.G, ng, self.layout, self.zero_offset)
         return QuantWeight(qw, self.scales, self.qzeros, g, k, self.N, self.G, self.num_groups,
-                           self.layout)
+                           self.layout, self.zero_offset)
 
 
 class Workspace:
@@ -251,10 +258,11 @@ def reorder(w1: QuantWeight, w2: Optional[QuantWeight] = None, workspace: Option
         ctypes.byref(c1), ctypes.byref(c2) if c2 is not None else None,
         _ptr(P1), _ptr(g1), _ptr(P2), _ptr(g2), _ptr(q1), _ptr(s1), _ptr(z1), _ptr(q2),
         _dtype_code(w1.scales.dtype), layout, _ptr(buf), buf.numel(), _stream_handle(dev)))
-    w1o = QuantWeight(q1, s1, z1, g1, w1.K, w1.N, w1.G, w1.num_groups, layout)
+    w1o = QuantWeight(q1, s1, z1, g1, w1.K, w1.N, w1.G, w1.num_groups, layout, w1.zero_offset)
     w2o = None
     if w2 is not None:
-        w2o = QuantWeight(q2, w2.scales, w2.qzeros, g2, w2.K, w2.N, w2.G, w2.num_groups, layout)
+        w2o = QuantWeight(q2, w2.scales, w2.qzeros, g2, w2.K, w2.N, w2.G, w2.num_groups, layout,
+                          w2.zero_offset)
     return P1, g1, P2, g2, w1o, w2o
 
 
@@ -264,7 +272,8 @@ def pack_tiled(w: QuantWeight) -> QuantWeight:
     out = torch.empty((w.N + 15) // 16, tiled_ld(w.K), dtype=torch.int32, device=w.device)
     c = w.c_struct()
     _abi.check(_abi.lib().tpdq_pack_tiled(ctypes.byref(c), _ptr(out), _stream_handle(w.device)))
-    return QuantWeight(out, w.scales, w.qzeros, w.g_idx, w.K, w.N, w.G, w.num_groups, LAYOUT_TILED)
+    return QuantWeight(out, w.scales, w.qzeros, w.g_idx, w.K, w.N, w.G, w.num_groups, LAYOUT_TILED,
+                       w.zero_offset)
 
 
 def w4a16_gemm(X, w: QuantWeight, path: int, x_perm=None, out=None,

@@ -30,7 +30,7 @@ class W4(ctypes.Structure):
         ("g_idx", ctypes.c_void_p),
         ("K", ctypes.c_int32), ("N", ctypes.c_int32),
         ("group_size", ctypes.c_int32), ("num_groups", ctypes.c_int32),
-        ("layout", ctypes.c_int32),
+        ("layout", ctypes.c_int32), ("zero_offset", ctypes.c_int32),
     ]
 
 

@@ -43,26 +43,30 @@ tpdq_status hip_fail(hipError_t e, const char* what) {
 bool aligned(const void* p, size_t a) { return ((uintptr_t)p % a) == 0; }
 
 // Shape and pointer checks of one layer. `need_gidx`: the act-order path
-// reads g_idx; `sorted`: the group of row k is k / G, so G must divide K and
-// num_groups cover K / G.
+// reads g_idx; `sorted`: the rows are sorted by group, so with G > 0 the group
+// of row k is k / G (the last group may be partial) and num_groups must cover
+// ceil(K / G); with G == 0 (groups of unequal sizes) the sorted g_idx gives
+// each row's group and is required.
 tpdq_status check_layer(const tpdq_w4* w, const char* name, bool need_gidx, bool sorted) {
   if (!w) return fail(TPDQ_ERR_NULL, "%s is NULL", name);
   if (!w->qweight || !w->scales || !w->qzeros)
     return fail(TPDQ_ERR_NULL, "%s: qweight, scales and qzeros are required", name);
   if (need_gidx && !w->g_idx) return fail(TPDQ_ERR_NULL, "%s: g_idx is required", name);
-  if (w->K <= 0 || w->N <= 0 || w->group_size <= 0 || w->num_groups <= 0)
-    return fail(TPDQ_ERR_SHAPE, "%s: K=%d N=%d G=%d num_groups=%d must be positive", name, w->K,
-                w->N, w->group_size, w->num_groups);
+  if (w->K <= 0 || w->N <= 0 || w->group_size < 0 || w->num_groups <= 0)
+    return fail(TPDQ_ERR_SHAPE, "%s: K=%d N=%d num_groups=%d must be positive, G=%d not negative",
+                name, w->K, w->N, w->num_groups, w->group_size);
   if (w->K % 8 || w->N % 8 || w->group_size % 8)
     return fail(TPDQ_ERR_SHAPE, "%s: K=%d, N=%d and G=%d must be multiples of 8", name, w->K, w->N,
                 w->group_size);
+  if (w->zero_offset != 0 && w->zero_offset != 1)
+    return fail(TPDQ_ERR_SHAPE, "%s: zero_offset=%d must be 0 or 1", name, w->zero_offset);
   if (sorted) {
-    if (w->K % w->group_size)
-      return fail(TPDQ_ERR_SHAPE, "%s: sorted rows need G | K (K=%d G=%d)", name, w->K,
-                  w->group_size);
-    if (w->num_groups < w->K / w->group_size)
-      return fail(TPDQ_ERR_SHAPE, "%s: num_groups=%d < K/G=%d", name, w->num_groups,
-                  w->K / w->group_size);
+    if (w->group_size == 0 && !w->g_idx)
+      return fail(TPDQ_ERR_NULL, "%s: sorted rows in groups of unequal sizes (G = 0) need their g_idx",
+                  name);
+    const int ngk = w->group_size ? (w->K + w->group_size - 1) / w->group_size : 1;
+    if (w->num_groups < ngk)
+      return fail(TPDQ_ERR_SHAPE, "%s: num_groups=%d < ceil(K/G)=%d", name, w->num_groups, ngk);
   }
   if (w->layout != TPDQ_LAYOUT_GPTQ && w->layout != TPDQ_LAYOUT_TILED)
     return fail(TPDQ_ERR_SHAPE, "%s: unknown layout %d", name, w->layout);
@@ -166,7 +170,9 @@ tpdq_status run_gemm(const uint16_t* X, int64_t ldx, int M, const int32_t* perm,
                      tpdq_path path, int dt, uint16_t* Y, int64_t ldy, char* ws, hipStream_t st,
                      const GemmIO& io = GemmIO()) {
   const int meta = meta_mode(path);
-  const int32_t* gidx = path == TPDQ_PATH_ORDERED ? nullptr : w->g_idx;
+  // sorted rows in groups of G read no g_idx; in groups of unequal sizes their
+  // sorted g_idx gives each row's group (the per-row kernel, on sorted rows)
+  const int32_t* gidx = path == TPDQ_PATH_ORDERED && w->group_size > 0 ? nullptr : w->g_idx;
   MtilePlan mp;
   const bool gated = io.up != nullptr;
   if (!gated && plan_mtile(M, perm ? (int64_t)w->K : ldx, w, meta, &mp)) {
@@ -194,6 +200,7 @@ tpdq_status run_gemm(const uint16_t* X, int64_t ldx, int M, const int32_t* perm,
     a.N = w->N;
     a.G = w->group_size;
     a.num_groups = w->num_groups;
+    a.zoff = w->zero_offset;
     a.dt = dt;
     a.Y = Y;
     a.ldy = ldy;
@@ -239,6 +246,7 @@ tpdq_status run_gemm(const uint16_t* X, int64_t ldx, int M, const int32_t* perm,
     a.N = w->N;
     a.G = w->group_size;
     a.num_groups = w->num_groups;
+    a.zoff = w->zero_offset;
     a.dt = dt;
     a.Y = Y + (int64_t)m0 * ldy;
     a.ldy = ldy;
@@ -346,7 +354,7 @@ const char* tpdq_status_string(tpdq_status s) {
 const char* tpdq_last_error(void) { return g_last_error.c_str(); }
 
 size_t tpdq_workspace_bytes(int op, int32_t M, const tpdq_w4* a, const tpdq_w4* b) {
-  if (!a || a->K <= 0 || a->N <= 0 || a->group_size <= 0) return 0;
+  if (!a || a->K <= 0 || a->N <= 0 || a->group_size < 0 || a->num_groups <= 0) return 0;
   if (op == 0) {
     size_t n = 256 + align_up((size_t)a->num_groups * 4);
     if (b) n += align_up((size_t)b->num_groups * 4);
@@ -385,23 +393,28 @@ tpdq_status tpdq_reorder(const tpdq_w4* w1, const tpdq_w4* w2, int32_t* P1, int3
                          void* scales1_out, int32_t* qzeros1_out, int32_t* qweight2_out,
                          tpdq_dtype dtype, tpdq_layout out_layout, void* workspace,
                          size_t ws_bytes, void* stream) {
-  tpdq_status st = check_layer(w1, "w1", true, true);
+  tpdq_status st = check_layer(w1, "w1", true, false);
   if (st != TPDQ_OK) return st;
   if (w1->layout != TPDQ_LAYOUT_GPTQ || (w2 && w2->layout != TPDQ_LAYOUT_GPTQ))
     return fail(TPDQ_ERR_SHAPE, "reorder takes GPTQ-layout inputs");
   if (out_layout != TPDQ_LAYOUT_GPTQ && out_layout != TPDQ_LAYOUT_TILED)
     return fail(TPDQ_ERR_SHAPE, "unknown output layout %d", (int)out_layout);
   if (dtype != TPDQ_FP16 && dtype != TPDQ_BF16) return fail(TPDQ_ERR_SHAPE, "unknown dtype");
-  if (w1->num_groups != w1->K / w1->group_size)
-    return fail(TPDQ_ERR_SHAPE, "w1: a global act-order layer has num_groups == K/G");
+  // Eq. 3 over a whole layer: ceil(K/G) groups; groups of unequal sizes (G == 0)
+  // come with their own count
+  auto global_groups_ok = [](const tpdq_w4* w) {
+    return w->group_size == 0 || w->num_groups == (w->K + w->group_size - 1) / w->group_size;
+  };
+  if (!global_groups_ok(w1))
+    return fail(TPDQ_ERR_SHAPE, "w1: a global act-order layer has num_groups == ceil(K/G)");
   if (!P1 || !g1_sorted || !qweight1_out || !scales1_out || !qzeros1_out)
     return fail(TPDQ_ERR_NULL, "P1, g1_sorted, qweight1_out, scales1_out, qzeros1_out are required");
   if (w2) {
-    st = check_layer(w2, "w2", true, true);
+    st = check_layer(w2, "w2", true, false);
     if (st != TPDQ_OK) return st;
     if (w2->K != w1->N) return fail(TPDQ_ERR_SHAPE, "w2->K=%d != w1->N=%d", w2->K, w1->N);
-    if (w2->num_groups != w2->K / w2->group_size)
-      return fail(TPDQ_ERR_SHAPE, "w2: a global act-order layer has num_groups == K/G");
+    if (!global_groups_ok(w2))
+      return fail(TPDQ_ERR_SHAPE, "w2: a global act-order layer has num_groups == ceil(K/G)");
     if (!P2 || !g2_sorted || !qweight2_out)
       return fail(TPDQ_ERR_NULL, "P2, g2_sorted and qweight2_out are required with w2");
   } else if (P2 || g2_sorted || qweight2_out) {
@@ -436,13 +449,14 @@ tpdq_status tpdq_reorder(const tpdq_w4* w1, const tpdq_w4* w2, int32_t* P1, int3
   if (e != hipSuccess) return hip_fail(e, "g_idx validation readback");
   for (int l = 0; l < 2; ++l) {
     if (hflags[l] & 1u)
-      return fail(TPDQ_ERR_GIDX, "w%d: a g_idx value is outside [0, K/G)", l + 1);
+      return fail(TPDQ_ERR_GIDX, "w%d: a g_idx value is outside [0, num_groups)", l + 1);
     if (hflags[l] & 2u)
-      return fail(TPDQ_ERR_GIDX, "w%d: a group does not hold exactly G rows", l + 1);
+      return fail(TPDQ_ERR_GIDX, "w%d: the groups do not hold the rows Eq. 3 gives (G each, the last "
+                  "K - (num_groups - 1) G)", l + 1);
   }
 
-  e = launch_gidx_rank(L1, s);
-  if (e == hipSuccess && w2) e = launch_gidx_rank(L2, s);
+  e = launch_gidx_rank(L1, counts1, s);
+  if (e == hipSuccess && w2) e = launch_gidx_rank(L2, counts2, s);
   if (e != hipSuccess) return hip_fail(e, "argsort launch");
 
   const int32_t* pcol = w2 ? P2 : nullptr;
@@ -602,8 +616,10 @@ tpdq_status tpdq_gated_mlp_shard(const void* X, int64_t ldx, int32_t M, const in
   if (st != TPDQ_OK) return st;
   if (w_up->K != w_gate->K || w_up->N != w_gate->N || w_up->group_size != w_gate->group_size ||
       w_up->num_groups != w_gate->num_groups || w_up->layout != w_gate->layout ||
-      w_up->ld_q != w_gate->ld_q || w_up->ld_s != w_gate->ld_s || w_up->ld_z != w_gate->ld_z)
-    return fail(TPDQ_ERR_SHAPE, "w_up must match w_gate in shape, groups, layout and leading dimensions");
+      w_up->ld_q != w_gate->ld_q || w_up->ld_s != w_gate->ld_s || w_up->ld_z != w_gate->ld_z ||
+      w_up->zero_offset != w_gate->zero_offset)
+    return fail(TPDQ_ERR_SHAPE,
+                "w_up must match w_gate in shape, groups, layout, leading dimensions and zero offset");
   if (w_down->K != w_gate->N)
     return fail(TPDQ_ERR_SHAPE, "w_down->K=%d != w_gate->N=%d", w_down->K, w_gate->N);
   if (!X || !Y1 || !Y2_partial) return fail(TPDQ_ERR_NULL, "X, Y1 and Y2_partial are required");

@@ -86,9 +86,10 @@ struct MetaStage {
 #pragma unroll
     for (int i = 0; i < R; ++i) fetch(a, n0, rows, tid + i * NT, s[i], z[i]);
   }
+  // the stored zero code plus the layer's offset (up to 16) in the high half
   __device__ __forceinline__ static void put(u4_t* meta, int idx, int n, uint32_t sbits,
-                                             uint32_t zw) {
-    const uint32_t zc = (zw >> (4 * (n & 7))) & 0xFu;
+                                             uint32_t zw, int zoff) {
+    const uint32_t zc = ((zw >> (4 * (n & 7))) & 0xFu) + (uint32_t)zoff;
     ((uint32_t*)&meta[idx])[COMP] = sbits | (zc << 16);
   }
   // Entries past the last group go to the spare entry meta[items], so every
@@ -99,7 +100,7 @@ struct MetaStage {
 #pragma unroll
     for (int i = 0; i < R; ++i) {
       const int idx = tid + i * NT;
-      put(meta, min(idx, items), n0 + (idx & 15), s[i], z[i]);
+      put(meta, min(idx, items), n0 + (idx & 15), s[i], z[i], a.zoff);
     }
     for (int base = tid + R * NT; base < items; base += 4 * NT) {
       uint32_t ss[4], zz[4];
@@ -108,7 +109,7 @@ struct MetaStage {
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const int idx = base + i * NT;
-        if (idx < items) put(meta, idx, n0 + (idx & 15), ss[i], zz[i]);
+        if (idx < items) put(meta, idx, n0 + (idx & 15), ss[i], zz[i], a.zoff);
       }
       wait_vmcnt<0>();  // no load of this loop outlives it (see wait_vmcnt)
     }
@@ -533,6 +534,7 @@ struct ChunkMeta {
   uint32_t soff, zoff;    // this lane's pair in group row g0 = 0
   uint32_t sgrp, zgrp;    // bytes per group row
   uint32_t shift;         // nibble of column n0 + j in its zeros word
+  uint32_t zadd;          // the layer's zero offset, added to each zero code
   uint32_t raw_s[NL], raw_z[NL];
   float s[NL];
   uint32_t z1024[NL], z64[NL];
@@ -544,6 +546,7 @@ struct ChunkMeta {
     soff = (uint32_t)q * sgrp + (uint32_t)col * 2u;
     zoff = (uint32_t)q * zgrp + (uint32_t)(col >> 3) * 4u;
     shift = 4u * (uint32_t)(col & 7);
+    zadd = (uint32_t)a.zoff;
   }
   // the chunk whose first group is g0 (groups past ng load zeros)
   __device__ __forceinline__ void load(int g0, bool valid, int ng, int q) {
@@ -560,7 +563,7 @@ struct ChunkMeta {
   __device__ __forceinline__ void decode() {
 #pragma unroll
     for (int n = 0; n < NL; ++n) {
-      const uint32_t zc = (raw_z[n] >> shift) & 0xFu;
+      const uint32_t zc = ((raw_z[n] >> shift) & 0xFu) + zadd;  // up to 16
       s[n] = bits_to_float<DT>(raw_s[n]);
       if constexpr (DT == kBF16) {
         z1024[n] = __builtin_bit_cast(uint32_t, 128.f + (float)zc);
@@ -608,7 +611,7 @@ __global__ __launch_bounds__(NW * 64) void k_ordered(GemmArgs a) {
   const int tile0 = xcd_tile(blockIdx.x, gridDim.x) * (GATED ? 1 : TN);
   const int ntiles = (a.N + kTileN - 1) / kTileN;
   const int kw = a.K >> 3;
-  const int ng = a.K / (32 * SPG);
+  const int ng = (a.K + 32 * SPG - 1) / (32 * SPG);  // the last group may be partial
   const int nblk = (a.K + 127) >> 7;
   const int b0 = (int)((int64_t)nblk * wave / NW);
   const int b1 = (int)((int64_t)nblk * (wave + 1) / NW);
@@ -805,9 +808,9 @@ __global__ __launch_bounds__(NW * 64) void k_wide(GemmArgs a) {
   const int tg = lt - kidx * wgs;
   const int tile0 = (tg * NW + wave) * TN;  // this wave's first tile
   const int ntiles = (a.N + kTileN - 1) / kTileN;
-  const int ng = a.K / (32 * SPG);
+  const int ng = (a.K + 32 * SPG - 1) / (32 * SPG);  // the last group may be partial
   const int nblk = (a.K + 127) >> 7;
-  const int nsteps = a.K >> 5;
+  const int kw = a.K >> 3;
   const int b0 = (int)((int64_t)nblk * kidx / ks);
   const int b1 = (int)((int64_t)nblk * (kidx + 1) / ks);
   const UnpackConsts<DT> kc;
@@ -835,7 +838,9 @@ __global__ __launch_bounds__(NW * 64) void k_wide(GemmArgs a) {
       const int r = wave * RPW + i;
       const int t = r / (4 * CB), sl = r % (4 * CB);
       const int st = 4 * cb0 + sl;
-      uint32_t off = st < nsteps ? x_lane + (uint32_t)t * x_t + (uint32_t)st * x_st : kOutOfRange;
+      // the lane's octet 4 st + kq: octets past K load zeros (a partial last
+      // step when K % 32 != 0; the padding of X past K is never read)
+      uint32_t off = 4 * st + kq < kw ? x_lane + (uint32_t)t * x_t + (uint32_t)st * x_st : kOutOfRange;
       asm("" : "+v"(off));
       __builtin_amdgcn_raw_ptr_buffer_load_lds(
           rx, (__attribute__((address_space(3))) void*)(smem + buf * CHUNK + r * 1024), 16, off, 0,
@@ -1073,6 +1078,7 @@ __global__ __launch_bounds__(NW * 64) void k_rowmeta(GemmArgs a) {
   }
   const uint32_t gmax = (uint32_t)(a.num_groups - 1);
   const int zshift = 4 * (col & 7);
+  const uint32_t zoff = (uint32_t)a.zoff;
   for (int b = b0; b < b1; ++b) {
     const bool more = b + 1 < b1;
     u4_t wn = u4_t{0u, 0u, 0u, 0u};
@@ -1113,10 +1119,10 @@ __global__ __launch_bounds__(NW * 64) void k_rowmeta(GemmArgs a) {
           }
         } else {
           sr[r] = col_ok ? (uint32_t)a.sc[(int64_t)g * a.lds + col] : 0u;
-          zr[r] = col_ok ? (a.qz[(int64_t)g * a.ldz + (col >> 3)] >> zshift) & 0xFu : 0u;
+          zr[r] = col_ok ? ((a.qz[(int64_t)g * a.ldz + (col >> 3)] >> zshift) & 0xFu) + zoff : 0u;
           if constexpr (GATED) {
             sru[r] = col_ok ? (uint32_t)au.sc[(int64_t)g * a.lds + col] : 0u;
-            zru[r] = col_ok ? (au.qz[(int64_t)g * a.ldz + (col >> 3)] >> zshift) & 0xFu : 0u;
+            zru[r] = col_ok ? ((au.qz[(int64_t)g * a.ldz + (col >> 3)] >> zshift) & 0xFu) + zoff : 0u;
           }
         }
       }

@@ -80,7 +80,7 @@ bool plan_decode(int M, int K, int N, int G, int num_groups, int layout, int met
   int meta = meta_pref;
   const int spg = G / 32;
   if (meta == kMetaGroup &&
-      (G % 32 != 0 || K % G != 0 || !(spg == 1 || spg == 2 || spg == 4 || spg == 8)))
+      (G <= 0 || G % 32 != 0 || !(spg == 1 || spg == 2 || spg == 4 || spg == 8)))
     meta = kMetaRowLds;  // sorted rows of another G: per-row groups floor(k / G)
   if ((meta != kMetaGroup || mt == 4) && nw > 8) nw = 8;
   if (meta != kMetaGroup && mt == 4) nw = 4;  // four row tiles of per-row dequant: registers

@@ -164,7 +164,9 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2))) vo
     if (k < AREC) {
       const int rec = AREC * wave + k;  // record (rt, u) = (rec / 4, rec % 4)
       const int rt = rec >> 2, u = rec & 3;
-      const bool ok = bok && 128 * b + 32 * u < a.K;
+      // the lane's octet: columns past K load zeros (the padding of X past K
+      // is never read)
+      const bool ok = bok && 128 * b + 32 * u + 8 * kq < a.K;
       uint32_t off = ok ? x_lane + (uint32_t)rt * x_rt + (uint32_t)(128 * b + 32 * u) * 2u : kOutOfRange;
       asm("" : "+v"(off));
       dma_to_lds<16>(rx, sb + rec * 1024, off);
@@ -219,7 +221,7 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2))) vo
           const int c = 16 * i + j;
           const uint32_t sv = *(const uint16_t*)(mb + gi * 128 + 2 * c);
           const uint32_t zw = *(const uint32_t*)(mb + 512 + gi * 32 + 4 * (c >> 3));
-          const uint32_t zc = (zw >> (4 * (c & 7))) & 0xFu;
+          const uint32_t zc = ((zw >> (4 * (c & 7))) & 0xFu) + (uint32_t)a.zoff;  // up to 16
           if constexpr (DT == kBF16) {
             sf[i] = bits_to_float<kBF16>(sv);
             zs[i] = (128.f + (float)zc) * sf[i];
@@ -355,7 +357,7 @@ __global__ __launch_bounds__(256) void k_gather_rows(const uint16_t* __restrict_
 bool plan_mtile(int M, int64_t ldx, const tpdq_w4* w, int meta, MtilePlan* p) {
   if (meta != kMetaGroup || w->layout != TPDQ_LAYOUT_TILED) return false;
   const int K = w->K, N = w->N, G = w->group_size;
-  if (M < kMtileMinM || K % 8 != 0 || G % 32 != 0 || K % G != 0) return false;
+  if (M < kMtileMinM || K % 8 != 0 || G <= 0 || G % 32 != 0) return false;
   const int spg = G / 32;
   if (!(spg == 1 || spg == 2 || spg == 4 || spg == 8)) return false;
   // activation rows on 16 bytes, scale rows on 4 (the LDS loads move 16 and

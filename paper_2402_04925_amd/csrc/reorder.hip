@@ -2,12 +2,14 @@
 // and the permutations of the packed weights and their metadata (section 2.2:
 // W1[P1, P2], W2[P2]).
 //
-// The sort exploits what the method guarantees and the host validates first:
-// every group holds exactly G rows, so the sorted position of row i is
-//   g_idx[i] * G + #{ j < i : g_idx[j] == g_idx[i] }
-// (ascending groups, ties by ascending row: the stable order). One workgroup
-// per group sweeps g_idx in row order and ranks the group's members with
-// wave ballots, so the result does not depend on scheduling.
+// The sort is a counting sort: with off[g] the number of rows in groups
+// before g (an exclusive scan of the group counts, which the validation pass
+// computes anyway), the sorted position of row i is
+//   off[g_idx[i]] + #{ j < i : g_idx[j] == g_idx[i] }
+// (ascending groups, ties by ascending row: the stable order). For Eq. 3's
+// groups off[g] = g G. One workgroup per group sweeps g_idx in row order and
+// ranks the group's members with wave ballots, so the result does not depend
+// on scheduling.
 #include "tpdq_internal.h"
 
 namespace tpdq {
@@ -20,7 +22,7 @@ __global__ void k_fill_u32(uint32_t* p, size_t n, uint32_t v) {
 }
 
 // flag bit 0: a g_idx value out of [0, num_groups); bit 1: a group whose
-// count differs from G (set by k_check_counts).
+// count differs from what Eq. 3 gives (set by k_check_counts).
 __global__ void k_count_groups(const int32_t* __restrict__ g_idx, int K, int num_groups,
                                uint32_t* __restrict__ counts, uint32_t* __restrict__ flag) {
   for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < K; i += gridDim.x * blockDim.x) {
@@ -32,18 +34,48 @@ __global__ void k_count_groups(const int32_t* __restrict__ g_idx, int K, int num
   }
 }
 
-__global__ void k_check_counts(const uint32_t* __restrict__ counts, int num_groups, int G,
+// Eq. 3 with a permutation phi of 0..K-1: G rows in every group but the last,
+// which holds K - (num_groups - 1) G (a partial group when G does not divide K)
+__global__ void k_check_counts(const uint32_t* __restrict__ counts, int num_groups, int G, int K,
                                uint32_t* __restrict__ flag) {
-  for (int g = blockIdx.x * blockDim.x + threadIdx.x; g < num_groups; g += gridDim.x * blockDim.x)
-    if (counts[g] != (uint32_t)G) atomicOr(flag, 2u);
+  for (int g = blockIdx.x * blockDim.x + threadIdx.x; g < num_groups; g += gridDim.x * blockDim.x) {
+    const uint32_t want = g == num_groups - 1 ? (uint32_t)(K - (num_groups - 1) * G) : (uint32_t)G;
+    if (counts[g] != want) atomicOr(flag, 2u);
+  }
 }
 
-// One workgroup (256 threads = 4 waves) per group g.
-__global__ __launch_bounds__(256) void k_rank_group(const int32_t* __restrict__ g_idx, int K, int G,
+// counts -> exclusive prefix sums, in place (one workgroup: 256 counts per
+// pass into LDS, scanned serially there by thread 0, which carries the
+// running total from pass to pass)
+__global__ __launch_bounds__(256) void k_scan_counts(uint32_t* __restrict__ counts, int num_groups) {
+  __shared__ uint32_t buf[256];
+  uint32_t carry = 0;
+  for (int c0 = 0; c0 < num_groups; c0 += 256) {
+    const int g = c0 + (int)threadIdx.x;
+    buf[threadIdx.x] = g < num_groups ? counts[g] : 0u;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+      for (int i = 0; i < 256; ++i) {
+        const uint32_t v = buf[i];
+        buf[i] = carry;
+        carry += v;
+      }
+    }
+    __syncthreads();
+    if (g < num_groups) counts[g] = buf[threadIdx.x];
+    __syncthreads();
+  }
+}
+
+// One workgroup (256 threads = 4 waves) per group g; offs from k_scan_counts.
+__global__ __launch_bounds__(256) void k_rank_group(const int32_t* __restrict__ g_idx, int K,
+                                                    const uint32_t* __restrict__ offs, int num_groups,
                                                     int32_t* __restrict__ P,
                                                     int32_t* __restrict__ g_sorted) {
   __shared__ int wave_count[4];
   const int g = blockIdx.x;
+  const int first = (int)offs[g];
+  const int end = g + 1 < num_groups ? (int)offs[g + 1] : K;
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
   int base = 0;  // members of group g already placed (rows before this chunk)
@@ -59,10 +91,10 @@ __global__ __launch_bounds__(256) void k_rank_group(const int32_t* __restrict__ 
     const int total = wave_count[0] + wave_count[1] + wave_count[2] + wave_count[3];
     __syncthreads();
     if (hit) {
-      const int r = before + below;
-      if (r < G) {
-        P[(int64_t)g * G + r] = i;
-        g_sorted[(int64_t)g * G + r] = g;
+      const int r = first + before + below;
+      if (r < end) {
+        P[r] = i;
+        g_sorted[r] = g;
       }
     }
     base += total;
@@ -195,15 +227,18 @@ hipError_t launch_gidx_validate(const ReorderLayer& L, uint32_t* counts, uint32_
   hipLaunchKernelGGL(k_count_groups, dim3(grid_for(L.K)), dim3(256), 0, s, L.g_idx, L.K,
                      L.num_groups, counts, flag);
   hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
+  if (e != hipSuccess || L.G == 0) return e;  // G == 0: groups of any size
   hipLaunchKernelGGL(k_check_counts, dim3(grid_for(L.num_groups)), dim3(256), 0, s, counts,
-                     L.num_groups, L.G, flag);
+                     L.num_groups, L.G, L.K, flag);
   return hipGetLastError();
 }
 
-hipError_t launch_gidx_rank(const ReorderLayer& L, hipStream_t s) {
-  hipLaunchKernelGGL(k_rank_group, dim3(L.num_groups), dim3(256), 0, s, L.g_idx, L.K, L.G, L.P,
-                     L.g_sorted);
+hipError_t launch_gidx_rank(const ReorderLayer& L, uint32_t* offs, hipStream_t s) {
+  hipLaunchKernelGGL(k_scan_counts, dim3(1), dim3(256), 0, s, offs, L.num_groups);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(k_rank_group, dim3(L.num_groups), dim3(256), 0, s, L.g_idx, L.K, offs,
+                     L.num_groups, L.P, L.g_sorted);
   return hipGetLastError();
 }
 

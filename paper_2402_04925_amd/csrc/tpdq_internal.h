@@ -58,6 +58,7 @@ struct GemmArgs {
   int64_t ldz;
   const int32_t* g_idx;   // [K] (per-row metadata modes)
   int K, N, G, num_groups;
+  int zoff;      // added to every stored zero code (the layer's zero_offset)
   int ks;        // M-tiled kernel: K splits (<= 1: none)
   float* part;   // M-tiled kernel: fp32 partials [ks][M][N] when ks > 1
   int dt;        // tpdq_dtype of X, scales and Y (the kernels take it as a template argument)
@@ -161,7 +162,9 @@ struct ReorderLayer {
 };
 hipError_t launch_fill_u32(uint32_t* p, size_t n, uint32_t v, hipStream_t s);
 hipError_t launch_gidx_validate(const ReorderLayer& L, uint32_t* counts, uint32_t* flag, hipStream_t s);
-hipError_t launch_gidx_rank(const ReorderLayer& L, hipStream_t s);
+// offs: the group counts of launch_gidx_validate, turned into each group's
+// first sorted row (an exclusive scan, in place) before the ranking
+hipError_t launch_gidx_rank(const ReorderLayer& L, uint32_t* offs, hipStream_t s);
 // dst = src[Prow, Pcol] (either permutation may be NULL = identity), src in
 // GPTQ layout, dst dense in dst_layout.
 hipError_t launch_permute_qweight(const uint32_t* src, int64_t ld_src, int K, int N,

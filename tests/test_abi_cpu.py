@@ -50,7 +50,7 @@ def fake_layer(K=256, N=128, G=32, ng=None, base=1 << 20, gidx=True):
     # plausible, well-aligned but never dereferenced addresses
     return _abi.W4(qweight=base, ld_q=N, scales=base + (1 << 16), ld_s=N,
                    qzeros=base + (2 << 16), ld_z=N // 8, g_idx=(base + (3 << 16)) if gidx else None,
-                   K=K, N=N, group_size=G, num_groups=ng if ng is not None else K // G)
+                   K=K, N=N, group_size=G, num_groups=ng if ng is not None else -(-K // G))
 
 
 def gemm(lib, w, M=4, X=1 << 24, ldx=None, Y=1 << 25, ldy=None, path=_abi.PATH_ORDERED, ws=None,
@@ -69,7 +69,13 @@ def test_gemm_validation(lib):
     assert gemm(lib, fake_layer(K=260), ldx=264) == _abi.ERR_SHAPE          # K % 8
     assert gemm(lib, fake_layer(N=100), ldy=100) == _abi.ERR_SHAPE          # N % 8
     assert gemm(lib, fake_layer(G=12)) == _abi.ERR_SHAPE                    # G % 8
-    assert gemm(lib, fake_layer(K=264, G=16, ng=17), ldx=264) == _abi.ERR_SHAPE  # sorted needs G | K
+    assert gemm(lib, fake_layer(K=264, G=16, ng=16), ldx=264) == _abi.ERR_SHAPE  # < ceil(K/G) groups
+    bad = fake_layer()
+    bad.zero_offset = 2
+    assert gemm(lib, bad) == _abi.ERR_SHAPE                                # zero offset 0 or 1
+    bad = fake_layer(G=0, ng=5, gidx=False)
+    assert gemm(lib, bad) == _abi.ERR_NULL                                 # unequal sorted groups: g_idx
+    assert gemm(lib, fake_layer(G=-8)) == _abi.ERR_SHAPE
     assert gemm(lib, w, ldx=128) == _abi.ERR_SHAPE                          # ldx < K
     assert gemm(lib, w, X=(1 << 24) + 2) == _abi.ERR_ALIGN                  # X 16-B
     assert gemm(lib, w, ldx=260) == _abi.ERR_ALIGN                          # ldx % 8
@@ -157,6 +163,8 @@ def test_reorder_validation(lib):
     assert lib.tpdq_reorder(*args(nog, None)) == _abi.ERR_NULL
     shard = fake_layer(K=256, N=512, ng=64)
     assert lib.tpdq_reorder(*args(shard, None)) == _abi.ERR_SHAPE            # not a global layer
+    part = fake_layer(K=264, N=512, G=16, ng=16)
+    assert lib.tpdq_reorder(*args(part, None)) == _abi.ERR_SHAPE             # Eq. 3: ceil(K/G) groups
     assert lib.tpdq_reorder(*args(w1, w2, P2=p)) == _abi.ERR_WORKSPACE
     assert lib.tpdq_reorder(*args(w1, w2, P2=p, lay=5)) == _abi.ERR_SHAPE    # unknown layout
     tiled_in = fake_layer(K=256, N=512)
@@ -194,6 +202,10 @@ def test_workspace_sizes(lib):
         assert m >= min(M, 64) * 8192 * 2
     r = lib.tpdq_workspace_bytes(_abi.OP_REORDER, 0, ctypes.byref(w1), ctypes.byref(w2))
     assert r >= 4 * (64 + 28)
+    # groups of unequal sizes (G = 0): the reorder still needs its counters
+    u1 = fake_layer(K=8192, N=3584, G=0, ng=77)
+    assert lib.tpdq_workspace_bytes(_abi.OP_REORDER, 0, ctypes.byref(u1), None) >= 256 + 4 * 77
+    assert lib.tpdq_workspace_bytes(_abi.OP_GEMM, 16, ctypes.byref(u1), None) > 0
     assert lib.tpdq_workspace_bytes(_abi.OP_MLP, 4, ctypes.byref(w1), None) == 0
     assert lib.tpdq_workspace_bytes(_abi.OP_GEMM, 0, ctypes.byref(w1), None) == 0
 
