@@ -601,8 +601,11 @@ __global__ __launch_bounds__(NW * 64) void k_ordered(GemmArgs a) {
   constexpr int NT = NW * 64;
   constexpr bool AG = a_global(AM);
   // 128-row blocks in flight per wave; with A from global memory its
-  // fragments (4 * MT registers of 16 bytes per block) ride along
-  constexpr int D = AG ? (MT == 4 ? 1 : 2) : 4;
+  // fragments (4 * MT registers of 16 bytes per block) ride along. The
+  // prepared operand with one row tile keeps four (Llama-70B TP=8 MLP at
+  // M = 8: 16.1 -> 14.6 us; at M = 16 equal, 17.1 us), the other global
+  // operands two, or one with four row tiles
+  constexpr int D = AG ? (MT == 4 ? 1 : (AM == kAGlobalPrep && MT == 1 && !GATED ? 4 : 2)) : 4;
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
