@@ -105,15 +105,26 @@ size_t decode_gather_bytes(int M, int K) {
 size_t mtile_gather_bytes(int M, int K, bool perm) { return perm ? align_up((size_t)M * K * 2) : 0; }
 
 // The decode plan of one launch of mc <= 64 rows, as run_gemm makes it: with
-// a perm, the gather inside the kernel's LDS if it fits, else the prepared
-// operand (*prepared).
+// a perm, the gather inside the kernel's LDS if it is planned; else, up to 4
+// rows, X' gathered once row-major when the tile kernel then takes it like
+// any X (*plain); else the prepared operand (*prepared). The workspace of the
+// prepared operand is at least that of the row-major X', so sizes computed
+// without `plain` cover both.
 bool decode_plan_for(int mc, bool perm, const tpdq_w4* w, int meta, int dt, DecodePlan* plan,
-                     bool* prepared, bool gated = false) {
+                     bool* prepared, bool gated = false, bool* plain = nullptr) {
   *prepared = false;
+  if (plain) *plain = false;
   if (perm) {
     if (plan_decode(mc, w->K, w->N, w->group_size, w->num_groups, w->layout, meta, kOperandGather,
                     dt, plan, gated))
       return true;
+    if (plain && mc <= 4 &&
+        plan_decode(mc, w->K, w->N, w->group_size, w->num_groups, w->layout, meta, kOperandPlain, dt,
+                    plan, gated) &&
+        !plan->wide) {
+      *plain = true;
+      return true;
+    }
     *prepared = true;
     return plan_decode(mc, w->K, w->N, w->group_size, w->num_groups, w->layout, meta,
                        kOperandPrepared, dt, plan, gated);
@@ -214,12 +225,21 @@ tpdq_status run_gemm(const uint16_t* X, int64_t ldx, int M, const int32_t* perm,
     const uint16_t* Xc = X + (int64_t)m0 * ldx;
     int64_t ldc = ldx;
     DecodePlan plan;
-    bool prepared = false;
+    bool prepared = false, plain = false;
     const bool ok = io.x_prepared
                         ? plan_decode(mc, w->K, w->N, w->group_size, w->num_groups, w->layout, meta,
                                       kOperandPrepared, dt, &plan, gated)
-                        : decode_plan_for(mc, perm != nullptr, w, meta, dt, &plan, &prepared, gated);
-    int operand = perm ? (prepared ? kOperandPrepared : kOperandGather) : kOperandPlain;
+                        : decode_plan_for(mc, perm != nullptr, w, meta, dt, &plan, &prepared, gated,
+                                          &plain);
+    const int operand =
+        perm ? (prepared ? kOperandPrepared : (plain ? kOperandPlain : kOperandGather)) : kOperandPlain;
+    if (ok && plain) {
+      uint16_t* Xp = (uint16_t*)ws;
+      hipError_t e = launch_gather_plain(Xc, ldx, mc, w->K, perm, Xp, st);
+      if (e != hipSuccess) return hip_fail(e, "activation gather launch");
+      Xc = Xp;
+      ldc = w->K;
+    }
     if (ok && prepared) {
       uint16_t* Xp = (uint16_t*)ws;
       hipError_t e = launch_gather_prep(Xc, ldx, mc, w->K, perm, w->layout, Xp, st);

@@ -13,6 +13,32 @@ namespace {
 // rows 8 (4 s + l / 16) .. +7 in operand order (natural for tiled weights,
 // x0, x4, x1, x5, ... for GPTQ ones), zero past M or K. A decode wave reads one step of one row tile as one
 // contiguous KiB.
+// X'[m][k] = X[m][perm[k]] row-major [M][K], one octet per thread: for a
+// decode GEMM that then stages X' in LDS (or reads it row-major) like any X.
+__global__ __launch_bounds__(64) void k_gather_plain(const uint16_t* __restrict__ X, int64_t ldx,
+                                                     int M, int K, const int32_t* __restrict__ perm,
+                                                     uint16_t* __restrict__ Xp) {
+  const int kw = K >> 3;
+  const int64_t total = (int64_t)M * kw;
+  const uint32_t kmax = (uint32_t)(K - 1);
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < total;
+       i += (int64_t)gridDim.x * blockDim.x) {
+    const int m = (int)(i / kw);
+    const int r = (int)(i - (int64_t)m * kw);
+    const uint16_t* xr = X + (int64_t)m * ldx;
+    const u4_t p0 = *(const u4_t*)(perm + r * 8);
+    const u4_t p1 = *(const u4_t*)(perm + r * 8 + 4);
+    uint32_t x[8];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      x[e] = xr[min(p0[e], kmax)];
+      x[e + 4] = xr[min(p1[e], kmax)];
+    }
+    *(u4_t*)(Xp + (int64_t)m * K + 8 * r) =
+        u4_t{x[0] | (x[1] << 16), x[2] | (x[3] << 16), x[4] | (x[5] << 16), x[6] | (x[7] << 16)};
+  }
+}
+
 __global__ __launch_bounds__(64) void k_gather_prep(const uint16_t* __restrict__ X, int64_t ldx,
                                                     int M, int K, const int32_t* __restrict__ perm,
                                                     int natural, uint16_t* __restrict__ Xp) {
@@ -119,7 +145,11 @@ bool plan_decode(int M, int K, int N, int G, int num_groups, int layout, int met
   const bool fits = meta_bytes + x_bytes <= budget && small_m && !wide_pref;
   int am;
   if (operand == kOperandGather) {
-    if (meta_bytes + x_bytes + xr_bytes > budget || meta != kMetaGroup || M > 4 || wide_pref)
+    // the gather inside the kernel loads the permutation (K x 4 bytes) and X
+    // in every 16-column workgroup: on grids of more than kGatherOnceTiles
+    // tiles the caller gathers X' once instead
+    if (meta_bytes + x_bytes + xr_bytes > budget || meta != kMetaGroup || M > 4 || wide_pref ||
+        ntiles > kGatherOnceTiles)
       return false;
     am = kALdsGather;
   } else if (operand == kOperandPrepared) {
@@ -214,6 +244,16 @@ hipError_t launch_decode(const GemmArgs& a0, const DecodePlan& p, float* part, h
   const int ntiles = (a.N + kTileN - 1) / kTileN;
   const int grid = p.gated ? ntiles : (ntiles + p.tn - 1) / p.tn;  // gated: both streams, one tile
   hipLaunchKernelGGL(k, dim3(grid), dim3(p.nw * 64), p.lds_bytes, s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_gather_plain(const uint16_t* X, int64_t ldx, int M, int K, const int32_t* perm,
+                               uint16_t* Xp, hipStream_t s) {
+  const int64_t total = (int64_t)M * (K >> 3);
+  int blocks = (int)((total + 63) / 64);
+  if (blocks > 16384) blocks = 16384;
+  if (blocks < 1) blocks = 1;
+  hipLaunchKernelGGL(k_gather_plain, dim3(blocks), dim3(64), 0, s, X, ldx, M, K, perm, Xp);
   return hipGetLastError();
 }
 

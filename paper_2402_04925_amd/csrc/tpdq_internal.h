@@ -109,10 +109,18 @@ constexpr int64_t kWideMinWeights = (int64_t)64 << 20;
 constexpr int64_t kWideMinWeightsRowMajor = (int64_t)16 << 20;
 constexpr int kWideTargetWgs = 200;
 
+// The in-LDS gather of X[:, perm] is planned on grids of at most this many
+// 16-column tiles; on larger ones (the unsharded Llama-70B GEMM1: 1792 tiles,
+// each workgroup loading the 32 KiB permutation and X) the caller gathers X'
+// once, row-major, and the kernel stages it like any X (MLP at M = 1:
+// 50.1 -> 48.4 us; at TP = 8, 224 tiles, the in-LDS gather stays: 0.9 us)
+constexpr int kGatherOnceTiles = 512;
 // meta_pref: kMetaGroup for sorted rows (needs G % 32 == 0), otherwise a
 // per-row mode; operand: an Operand. Returns false when no decode kernel
-// covers the request (for kOperandGather: the gather does not fit in LDS, the
-// caller then runs launch_gather_prep and plans with kOperandPrepared).
+// covers the request (for kOperandGather: the gather is not planned inside
+// the kernel, the caller then gathers X' first, row-major (launch_gather_plain,
+// planning with kOperandPlain) or in operand order (launch_gather_prep,
+// kOperandPrepared)).
 bool plan_decode(int M, int K, int N, int G, int num_groups, int layout, int meta_pref, int operand,
                  int dt, DecodePlan* p, bool gated = false);
 // the kernel of a plan, per element type (gemm_decode.hip, gemm_decode_bf16.hip)
@@ -123,6 +131,9 @@ DecodeKernel decode_kernel_gated_f16(const DecodePlan& p);   // gemm_gated.hip
 DecodeKernel decode_kernel_gated_bf16(const DecodePlan& p);  // gemm_gated_bf16.hip
 // part: the workspace for k_wide's split-K partials (ks x M x N floats)
 hipError_t launch_decode(const GemmArgs& a, const DecodePlan& p, float* part, hipStream_t s);
+// Xp [M][K] = X[:, perm] row-major (perm required).
+hipError_t launch_gather_plain(const uint16_t* X, int64_t ldx, int M, int K, const int32_t* perm,
+                               uint16_t* Xp, hipStream_t s);
 // Xp [M][K] = X[:, perm] (perm may be NULL), each octet in operand order.
 hipError_t launch_gather_prep(const uint16_t* X, int64_t ldx, int M, int K, const int32_t* perm,
                               int layout, uint16_t* Xp, hipStream_t s);

@@ -1,6 +1,7 @@
 """Activations with a leading dimension larger than K (X cut from a wider
 buffer) on every route that gathers X[:, perm]: inside the decode kernel's
-LDS (M <= 4), through the prepared operand (M > 4), through the M-tiled
+LDS (M <= 4), gathered once row-major on grids of more than 512 column tiles
+(N = 8320, M <= 4), through the prepared operand (M > 4), through the M-tiled
 kernel's row gather (M >= 256), and in the MLP shard. The contract is 16-byte
 alignment and ldx % 8 == 0 on every path."""
 import numpy as np
@@ -24,7 +25,7 @@ def _strided(X, dev, pad=8):
 
 
 @pytest.mark.parametrize("K,N,G,M", [(256, 128, 32, 3), (1024, 256, 128, 16), (512, 512, 64, 256),
-                                     (8192, 512, 128, 4)])
+                                     (8192, 512, 128, 4), (512, 8320, 64, 1), (1024, 8320, 128, 3)])
 def test_gather_with_ldx(K, N, G, M):
     import torch
     import paper_2402_04925_amd as tpdq
