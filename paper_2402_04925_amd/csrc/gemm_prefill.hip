@@ -130,12 +130,6 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2))) vo
 
   // sources: rows past M, groups past the last one and tiles past N load
   // zeros from the resource bounds
-  const __amdgpu_buffer_rsrc_t rx =
-      buffer_rsrc(a.X + (int64_t)row0 * a.ldx, (uint32_t)(a.M - row0) * (uint32_t)a.ldx * 2u);
-  const __amdgpu_buffer_rsrc_t rw = buffer_rsrc(a.qw, (uint32_t)ntiles * (uint32_t)a.ldq * 4u);
-  const __amdgpu_buffer_rsrc_t rs = buffer_rsrc(a.sc, (uint32_t)ng * (uint32_t)a.lds * 2u);
-  const __amdgpu_buffer_rsrc_t rz = buffer_rsrc(a.qz, (uint32_t)ng * (uint32_t)a.ldz * 4u);
-
   // per-lane parts of the offsets
   // activations: record (rt, u) of block b, lane l = row 16 rt + l % 16,
   // columns 128 b + 32 u + 8 (l / 16) .. +7
@@ -152,9 +146,32 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2))) vo
   const uint32_t w_lane = ((uint32_t)(cw >> 4) * (uint32_t)a.ldq + 4u * (uint32_t)lane) * 4u;
   const uint32_t w_tile = (uint32_t)a.ldq * 4u;
 
-  // load k (0 <= k < LPB) of block b (b >= nblk: zeros, no traffic) into
-  // LDS stage st; every offset is a select kept in one register, so each
-  // item is exactly one load on every path (the wait counts rely on it)
+  // per-lane offsets inside one block's window of each source, the same for
+  // every block; the window (a buffer resource: base and size in scalar
+  // registers) moves with the block, so a load needs no per-block vector
+  // arithmetic. Blocks past the workgroup's range get an empty window: their
+  // loads return zeros and cost no traffic.
+  const int bl = nblk_all - 1;
+  uint32_t offA[AREC], offAt[AREC], offS[NSD], offW[kPWT];
+#pragma unroll
+  for (int k = 0; k < AREC; ++k) {
+    const int rec = AREC * wave + k, rt = rec >> 2, u = rec & 3;
+    offA[k] = x_lane + (uint32_t)rt * x_rt + (uint32_t)(32 * u) * 2u;
+    // the last block: the lane's octet loads zeros past K (the padding of X
+    // past K is never read)
+    offAt[k] = 128 * bl + 32 * u + 8 * kq < a.K ? offA[k] : kOutOfRange;
+  }
+#pragma unroll
+  for (int d = 0; d < NSD; ++d)
+    offS[d] = 2 * d + (lane >> 5) < GPK ? s_lane + (uint32_t)(2 * d) * (uint32_t)a.lds * 2u : kOutOfRange;
+  const uint32_t offZ = z_used ? z_lane : kOutOfRange;
+#pragma unroll
+  for (int i = 0; i < kPWT; ++i) offW[i] = w_lane + (uint32_t)i * w_tile;
+  const uint32_t xbytes = (uint32_t)(a.M - row0) * (uint32_t)a.ldx * 2u;
+  const uint32_t wbytes = (uint32_t)ntiles * (uint32_t)a.ldq * 4u;
+
+  // load k (0 <= k < LPB) of block b into LDS stage st; each item is exactly
+  // one load (the wait counts rely on it)
   auto dma_item = [&](int b, int st, int k) {
     unsigned char* sb = smem + st * STAGE;
     unsigned char* wb = sb + ABYTES + wave * (kPWwave + kPMwave);
@@ -162,31 +179,24 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2))) vo
     const int g0 = (128 * b) / (32 * SPG);
     const bool bok = b < kb1;
     if (k < AREC) {
-      const int rec = AREC * wave + k;  // record (rt, u) = (rec / 4, rec % 4)
-      const int rt = rec >> 2, u = rec & 3;
-      // the lane's octet: columns past K load zeros (the padding of X past K
-      // is never read)
-      const bool ok = bok && 128 * b + 32 * u + 8 * kq < a.K;
-      uint32_t off = ok ? x_lane + (uint32_t)rt * x_rt + (uint32_t)(128 * b + 32 * u) * 2u : kOutOfRange;
-      asm("" : "+v"(off));
-      dma_to_lds<16>(rx, sb + rec * 1024, off);
+      const int rec = AREC * wave + k;
+      const __amdgpu_buffer_rsrc_t r = buffer_rsrc(a.X + (int64_t)row0 * a.ldx + 128 * b,
+                                                   bok ? xbytes - 256u * (uint32_t)b : 0u);
+      dma_to_lds<16>(r, sb + rec * 1024, b == bl ? offAt[k] : offA[k]);
     } else if (k < AREC + NSD) {
       const int d = k - AREC;
-      const int gi = 2 * d + (lane >> 5);
-      const bool ok = bok && gi < GPK && g0 + gi < ng;
-      uint32_t off = ok ? s_lane + (uint32_t)(g0 + 2 * d) * (uint32_t)a.lds * 2u : kOutOfRange;
-      asm("" : "+v"(off));
-      dma_to_lds<4>(rs, mb + d * 256, off);
+      const __amdgpu_buffer_rsrc_t r = buffer_rsrc(a.sc + (int64_t)g0 * a.lds,
+                                                   bok ? (uint32_t)(ng - g0) * (uint32_t)a.lds * 2u : 0u);
+      dma_to_lds<4>(r, mb + d * 256, offS[d]);
     } else if (k == AREC + NSD) {
-      const bool ok = bok && z_used && g0 + (lane >> 3) < ng;
-      uint32_t off = ok ? z_lane + (uint32_t)g0 * (uint32_t)a.ldz * 4u : kOutOfRange;
-      asm("" : "+v"(off));
-      dma_to_lds<4>(rz, mb + 512, off);
+      const __amdgpu_buffer_rsrc_t r = buffer_rsrc(a.qz + (int64_t)g0 * a.ldz,
+                                                   bok ? (uint32_t)(ng - g0) * (uint32_t)a.ldz * 4u : 0u);
+      dma_to_lds<4>(r, mb + 512, offZ);
     } else {
       const int i = k - AREC - NSD - 1;
-      uint32_t off = bok ? w_lane + (uint32_t)i * w_tile + (uint32_t)b * 1024u : kOutOfRange;
-      asm("" : "+v"(off));
-      dma_to_lds<16>(rw, wb + i * 1024, off);
+      const __amdgpu_buffer_rsrc_t r = buffer_rsrc(a.qw + (int64_t)256 * b,
+                                                   bok ? wbytes - 1024u * (uint32_t)b : 0u);
+      dma_to_lds<16>(r, wb + i * 1024, offW[i]);
     }
   };
   auto issue = [&](int b, int st) {

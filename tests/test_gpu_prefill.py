@@ -1,6 +1,6 @@
 """GPU M-tiled GEMM (ordered path, tiled weights) against the oracle: the
 prefill configuration (M >= 256, 128 x 512 tiles over all of K) and the
-medium-M configuration (16 <= M < 256 on large weights, 64 x 256 tiles with
+medium-M configuration (33 <= M < 256 on large weights, 64 x 512 tiles with
 K split over workgroups and the fp32 partials summed by a second kernel)."""
 import numpy as np
 import pytest
@@ -105,12 +105,14 @@ def test_prefill_mlp_llama_tp2(path):
     assert err2 <= TOL_FP16
 
 
-# K, N, G, M for the split-K configuration: at least 64M weights, ragged N and
-# M, every group size, M from 33 rows (one 64-row tile, half padding) to 255
-# (four tiles)
+# K, N, G, M for the split-K configuration: at least 64M weights, ragged N
+# (a last 512-column tile of 8 columns), ragged K (a last 128-row block of 8
+# rows, a partial last group), every group size, M from 33 rows (one 64-row
+# tile, half padding) to 255 (four tiles)
 MT_SHAPES = [
     (8192, 8192, 128, 33), (8192, 8200, 128, 40), (4096, 16384, 64, 64), (16384, 4096, 256, 100),
-    (8192, 8192, 32, 255),
+    (8192, 8192, 32, 255), (8192, 8192, 32, 64), (8200, 8192, 128, 48), (16384, 4096, 256, 64),
+    (8192, 28672, 128, 64),
 ]
 
 
