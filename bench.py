@@ -86,6 +86,40 @@ def read_traffic(workload, M):
         return None
 
 
+def read_mfma_util():
+    """MFMA utilisation of the prefill GEMMs from the committed counter
+    summary: SQ_VALU_MFMA_BUSY_CYCLES over (GRBM_GUI_ACTIVE / 8) x 1024 SIMDs,
+    and the clock the part ran at, averaged per GEMM (by grid); None when the
+    summary is absent."""
+    path = os.path.join(ROOT, "profiles", "prefill_llama70b_tp2_M2048.md")
+    if not os.path.exists(path):
+        return None
+    rows = {}
+    in_util = False
+    with open(path) as f:
+        for line in f:
+            if line.startswith("## MFMA utilisation"):
+                in_util = True
+            elif in_util and line.startswith("| ") and "`k_prefill" in line:
+                c = [x.strip() for x in line.strip().strip("|").split("|")]
+                try:
+                    grid, ghz, util = int(c[2]), float(c[7]), float(c[8])
+                except (IndexError, ValueError):
+                    continue
+                rows.setdefault(grid, []).append((util, ghz))
+    if not rows:
+        return None
+    out = {}
+    for grid, name in ((448, "gemm1"), (256, "gemm2")):
+        v = rows.get(grid)
+        if v:
+            out[name] = dict(mfma_busy_of_clocks=round(sum(u for u, _ in v) / len(v), 3),
+                             clock_ghz=round(sum(g for _, g in v) / len(v), 2))
+    out["denominator"] = "GRBM_GUI_ACTIVE / 8 (the dispatch's clocks) x 1024 SIMDs"
+    out["source"] = "profiles/prefill_llama70b_tp2_M2048.md"
+    return out
+
+
 class Setup:
     """Device-resident shards (rank 0) of one workload, replicated for rotation.
     bf16: bfloat16 scales (and activations, in Calls)."""
@@ -714,6 +748,7 @@ def prefill_line(dev, steps=10):
         bf16_frac=round(tfb / MFMA_F16_PEAK_TFLOPS, 4),
         fp16_dense_mlp_us=round(md * 1e3, 1), fp16_dense_tflops=round(tfd, 1),
         ordered_over_fp16_dense_tflops=round(tf / tfd, 3),
+        mfma_counters=read_mfma_util(),
         timing="HIP graph replay, events, median of 5")
 
 

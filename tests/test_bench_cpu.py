@@ -36,3 +36,15 @@ def test_traffic_summary_is_parsed():
     text = open(path).read()
     assert "kernel_source_hash = " in text and "bytes_per_launch = " in text
     json.dumps(text)  # plain text, nothing to execute
+
+
+def test_mfma_counter_summary_is_parsed():
+    """The committed prefill counter summary gives each GEMM's MFMA-busy
+    fraction of its clocks and the clock it ran at, both in range."""
+    sys.path.insert(0, ROOT)
+    import bench
+    u = bench.read_mfma_util()
+    assert u is not None
+    for g in ("gemm1", "gemm2"):
+        assert 0.0 < u[g]["mfma_busy_of_clocks"] <= 1.0
+        assert 1.0 < u[g]["clock_ghz"] < 3.0
