@@ -104,6 +104,14 @@ size_t decode_gather_bytes(int M, int K) {
 
 size_t mtile_gather_bytes(int M, int K, bool perm) { return perm ? align_up((size_t)M * K * 2) : 0; }
 
+// The M-tiled kernel's plan when it covers the call. With a perm its row
+// gather (k_gather_rows) stages one row of X, K halves, in LDS: past that the
+// call runs through the decode kernels, whose gathers have no such limit.
+bool mtile_for(int M, int64_t ldx, bool perm, const tpdq_w4* w, int meta, MtilePlan* p) {
+  if (perm && (size_t)w->K * 2 > kLdsMax) return false;
+  return plan_mtile(M, perm ? (int64_t)w->K : ldx, w, meta, p);
+}
+
 // The decode plan of one launch of mc <= 64 rows, as run_gemm makes it: with
 // a perm, the gather inside the kernel's LDS if it is planned; else, up to 4
 // rows, X' gathered once row-major when the tile kernel then takes it like
@@ -146,7 +154,7 @@ size_t decode_part_bytes(const DecodePlan& p, int mc, int N) {
 size_t gemm_ws_need(int M, int64_t ldx, bool perm, const tpdq_w4* w, int meta, int dt = TPDQ_FP16,
                     bool gated = false) {
   MtilePlan p;
-  if (!gated && plan_mtile(M, perm ? (int64_t)w->K : ldx, w, meta, &p))
+  if (!gated && mtile_for(M, ldx, perm, w, meta, &p))
     return mtile_gather_bytes(M, w->K, perm) + mtile_part_bytes(p, M, w->N);
   DecodePlan dp;
   bool prepared = false;
@@ -186,7 +194,7 @@ tpdq_status run_gemm(const uint16_t* X, int64_t ldx, int M, const int32_t* perm,
   const int32_t* gidx = path == TPDQ_PATH_ORDERED && w->group_size > 0 ? nullptr : w->g_idx;
   MtilePlan mp;
   const bool gated = io.up != nullptr;
-  if (!gated && plan_mtile(M, perm ? (int64_t)w->K : ldx, w, meta, &mp)) {
+  if (!gated && mtile_for(M, ldx, perm != nullptr, w, meta, &mp)) {
     // M-tiled MFMA GEMM over all rows, the activations gathered first
     const uint16_t* Xa = X;
     int64_t lda = ldx;
@@ -296,7 +304,7 @@ bool mlp_prepared_y1(int M, int64_t ldx, bool perm, const tpdq_w4* w1, const tpd
                      int dt, bool gated = false) {
   if (M > kDecodeMaxM || w1->N % 128 != 0) return false;
   MtilePlan mp;
-  if ((!gated && plan_mtile(M, perm ? (int64_t)w1->K : ldx, w1, meta, &mp)) ||
+  if ((!gated && mtile_for(M, ldx, perm, w1, meta, &mp)) ||
       plan_mtile(M, w1->N, w2, meta, &mp))
     return false;
   DecodePlan p1, p2;

@@ -156,3 +156,30 @@ def test_mtile_deterministic():
     b = np_of(tpdq.w4a16_gemm(X, wo, tpdq.PATH_ORDERED))
     torch.cuda.synchronize()
     assert np.array_equal(a.view(np.uint16), b.view(np.uint16))
+
+
+def test_mtile_gather_beyond_lds():
+    """K past what the M-tiled kernel's row gather stages in LDS (K = 82944,
+    166 KB of fp16 per row): with X[:, P] the call takes the decode kernels'
+    gathers (any K), without a gather the M-tiled kernel; both against the
+    oracle on sampled columns."""
+    import torch
+    import paper_2402_04925_amd as tpdq
+    dev = torch_dev()
+    K, N, G, M = 82944, 1024, 128, 40
+    log(f"mtile beyond LDS K={K} N={N} G={G} M={M}")
+    w1, _ = inputs.make_custom(K, N, 0, G, seed=77)
+    X = inputs.random_activations(M, K, np.random.default_rng(78))
+    P, _, _, _, wo, _ = tpdq.reorder(layer_to_dev(w1, dev), layout=tpdq.LAYOUT_TILED)
+    Xd = to_dev(X, dev)
+    cols = sample_cols(N, np.random.default_rng(79))
+    ref = o.w4a16_gemm(X, w1.qweight, w1.scales, w1.qzeros, w1.g_idx, cols=cols)
+    Y = tpdq.w4a16_gemm(Xd, wo, tpdq.PATH_ORDERED, x_perm=P)
+    torch.cuda.synchronize()
+    assert o.rel_err(np_of(Y)[:, cols], ref) <= TOL_FP16
+    eP, eg = o.reorder(w1.g_idx)
+    ws = o.permute_rows(dict(qweight=w1.qweight, scales=w1.scales, qzeros=w1.qzeros), eP)
+    ref2 = o.w4a16_gemm(X, ws["qweight"], ws["scales"], ws["qzeros"], eg, cols=cols)
+    Y2 = tpdq.w4a16_gemm(Xd, wo, tpdq.PATH_ORDERED)
+    torch.cuda.synchronize()
+    assert o.rel_err(np_of(Y2)[:, cols], ref2) <= TOL_FP16
