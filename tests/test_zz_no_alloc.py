@@ -82,6 +82,27 @@ def test_noalloc_matches_workspace_call(path):
     assert _same(r1, g1) and _same(r2, g2)
 
 
+def test_noalloc_mtile_paths():
+    """The M-tiled kernels through the scratch: the unsharded Llama-70B MLP at
+    M = 64 (the row gather of X and the K split's fp32 partials in the
+    scratch), the TP = 2 rank-0 shard at M = 2048 (the prefill tiles), then
+    M = 40 unsharded on the scratch the larger calls left; every output equal
+    bit for bit to tpdq_mlp_shard's."""
+    import torch
+    import paper_2402_04925_amd as tpdq
+    dev = torch_dev()
+    w = inputs.WORKLOADS["llama70b_tp1"]
+    L1, L2 = workload_layers(w.name)
+    d1, d2 = layer_to_dev(L1, dev), layer_to_dev(L2, dev)
+    P1, _, _, _, w1o, w2o = tpdq.reorder(d1, d2)
+    for tp, M in ((1, 64), (2, 2048), (1, 40)):
+        log(f"noalloc ordered llama70b tp={tp} M={M}")
+        s1, s2 = w1o.column_shard(0, tp), w2o.row_shard(0, tp, True)
+        X = to_dev(inputs.random_activations(M, w.K1, np.random.default_rng(M)), dev)
+        (r1, r2), (g1, g2) = _pair(tpdq, X, s1, s2, tpdq.PATH_ORDERED, P1)
+        assert _same(r1, g1) and _same(r2, g2)
+
+
 def test_noalloc_rejects_beyond_scratch():
     """A shape whose workspace exceeds the 64 MiB scratch is refused before
     any device work, with a message naming the scratch."""
